@@ -1,0 +1,147 @@
+"""Make the reference answer unique on a generated workload (test infrastructure).
+
+TEST INFRASTRUCTURE. Used by the test suite and the smoke check only.
+
+Two discrete decisions of the path are taken from real numbers: the budget
+K_t = ceil(M_vis,max * N_v) (Eq. (7)) and the Top-K_t cut of the scores
+(Eq. (3)). An fp32 GPU path and the fp64 reference agree on them only when the
+real numbers are not within rounding distance of the decision boundary. This
+module edits the stored keys of a workload, a few rows at a time, until
+
+* budget margin: budget(M (1 - mu)) == budget(M (1 + mu)) with mu = 1e-4, and
+* score gap: S_(k) >= (1 + gap) * S_(k+1) with gap = 1e-3 (S sorted descending),
+
+both measured by the fp64 reference. Edits move a key row along the unit
+direction q_hat_g of its KV group (the same direction the generator spikes
+along) and are re-rounded to the stored precision, so the stored tensor is
+exactly what both sides read. Every edit is logged (sequence, position).
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+from . import vp_oracle as O
+
+MU = 1e-4
+GAP = 1e-3
+BAND = 2.5e-3          # tokens this close (in log S) to the cut are pushed apart
+PUSH = 0.05            # step along q_hat_g, in key units
+
+
+def _round_like(x32: np.ndarray, stored_dtype) -> np.ndarray:
+    if stored_dtype == np.uint16:
+        u = np.ascontiguousarray(x32, dtype=np.float32).view(np.uint32)
+        r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+        return r.astype(np.uint16)
+    return x32.astype(stored_dtype)
+
+
+def _to_f32(x):
+    if x.dtype == np.uint16:
+        return (x.astype(np.uint32) << np.uint32(16)).view(np.float32)
+    return x.astype(np.float32)
+
+
+def _group_dirs(q_b, Hkv):
+    q = O.as_f64(q_b)
+    Hq, d = q.shape
+    s = q.reshape(Hkv, Hq // Hkv, d).sum(axis=1)
+    n = np.linalg.norm(s, axis=1, keepdims=True)
+    n[n == 0] = 1.0
+    return (s / n).astype(np.float32)
+
+
+def _push_rows(Kb, dirs, positions, signs, eps):
+    """Kb[g, pos] += sign * eps * dirs[g] for every KV head g, re-rounded in place."""
+    for pos, sgn in zip(positions, signs):
+        row = _to_f32(Kb[:, pos, :]) + np.float32(sgn * eps) * dirs
+        Kb[:, pos, :] = _round_like(row, Kb.dtype)
+
+
+def margin_ok(M_max, n_vis, params: O.OracleParams, mu=MU) -> bool:
+    lo = O.budget(M_max * (1 - mu), n_vis, params.r_lo_bp, params.r_hi_bp, params.clamp)
+    hi = O.budget(M_max * (1 + mu), n_vis, params.r_lo_bp, params.r_hi_bp, params.clamp)
+    return lo == hi
+
+
+def boundary_gap(S: np.ndarray, vis_pos: np.ndarray, k: int) -> float:
+    """Relative gap S_(k)/S_(k+1) - 1 at the cut (inf when there is no cut)."""
+    if k <= 0 or k >= len(S):
+        return math.inf
+    order = np.lexsort((vis_pos, -S))
+    a, b = S[order[k - 1]], S[order[k]]
+    if b <= 0:
+        return math.inf
+    return a / b - 1.0
+
+
+def plant_sequence(q_b, K_b, V_b, seq_len, segments, params: O.OracleParams,
+                   max_iter=12, log=None):
+    """Edit K_b in place until margin and gap hold; returns the final reference result.
+
+    Raises RuntimeError if the conditions cannot be met within ``max_iter`` passes.
+    """
+    Hkv = K_b.shape[0]
+    dirs = _group_dirs(q_b, Hkv)
+    vis_pos = O.visual_positions(seq_len, segments)
+    n_vis = len(vis_pos)
+    edits = []
+    for it in range(max_iter):
+        r = O.decode_step_sequence(q_b, K_b, V_b, seq_len, segments, params)
+        if not margin_ok(r.M_vis_max, n_vis, params):
+            # move the visual token that carries most tempered mass in the
+            # head-max head; try growing steps in both directions
+            Z = O.decode_step_sequence(q_b, K_b, V_b, seq_len, segments, params,
+                                       keep_logits=True).Z
+            h = int(np.argmax(r.mass_head))
+            A = O.tempered_attention(Z[h], params.tau_mass)
+            j = int(vis_pos[np.argmax(A[vis_pos])])
+            saved = K_b[:, j, :].copy()
+            fixed = False
+            for eps in (0.02, -0.02, 0.05, -0.05, 0.1, -0.1, 0.2, -0.2):
+                K_b[:, j, :] = saved
+                _push_rows(K_b, dirs, [j], [1.0], eps)
+                r2 = O.decode_step_sequence(q_b, K_b, V_b, seq_len, segments, params)
+                if margin_ok(r2.M_vis_max, n_vis, params):
+                    fixed = True
+                    break
+            if not fixed:
+                K_b[:, j, :] = saved
+                raise RuntimeError("budget margin could not be planted")
+            edits.append(("margin", j))
+            continue
+        g = boundary_gap(r.scores, vis_pos, r.k)
+        if g >= GAP:
+            if log is not None:
+                log.append({"iterations": it, "edits": edits, "gap": g})
+            return r, edits
+        order = np.lexsort((vis_pos, -r.scores))
+        theta = math.sqrt(r.scores[order[r.k - 1]] * r.scores[order[r.k]])
+        lg = np.abs(np.log(np.maximum(r.scores, 1e-300) / theta))
+        rank = np.empty(n_vis, dtype=np.int64)
+        rank[order] = np.arange(n_vis)
+        band = np.nonzero(lg < BAND)[0]
+        pos = vis_pos[band]
+        sgn = np.where(rank[band] < r.k, 1.0, -1.0)
+        _push_rows(K_b, dirs, pos, sgn, PUSH)
+        edits.extend(("gap", int(p)) for p in pos)
+    raise RuntimeError("score gap could not be planted")
+
+
+def plant(w, params: O.OracleParams, seqs=None):
+    """Plant every sequence of workload ``w`` (in place). Returns {b: SequenceResult}, log."""
+    res, log = {}, []
+    for b in (range(w.B) if seqs is None else seqs):
+        lg = []
+        r, edits = plant_sequence(w.q[b], w.K[b], w.V[b], int(w.seq_len[b]),
+                                  w.segments[b], params, log=lg)
+        res[b] = r
+        log.append({"seq": b, **(lg[0] if lg else {}), "n_edits": len(edits)})
+    return res, log
+
+
+def params_of(w) -> O.OracleParams:
+    return O.OracleParams(tau_mass=w.tau_mass, tau_score=w.tau_score,
+                          r_lo_bp=w.r_lo_bp, r_hi_bp=w.r_hi_bp, clamp=w.clamp)

@@ -1,0 +1,334 @@
+"""Pins for the fp64 reference: facts fixed by the paper's definitions and by
+mathematics, checked without re-typing the reference's own formulas.
+
+Each test names the passage it pins (VisionPulse, arXiv 2605.31457).
+"""
+import itertools
+import json
+import math
+import os
+from fractions import Fraction
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import vp_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rand_case(rng, Hq=4, Hkv=2, d=8, L=24, segs=((3, 9), (15, 5)), scale=1.0):
+    q = rng.standard_normal((Hq, d))
+    K = rng.standard_normal((Hkv, L, d)) * scale
+    V = rng.standard_normal((Hkv, L, d))
+    return q, K, V, L, [tuple(s) for s in segs]
+
+
+# ---------------------------------------------------------------------------
+# worked example (hand-derived; Eq. (2), (3), (5), (6), (7), pruned attention)
+# ---------------------------------------------------------------------------
+def test_worked_example_gqa2():
+    ex = json.load(open(os.path.join(GOLDEN, "worked_example_gqa2.json")))
+    a, b = ex["inputs"]["a"], ex["inputs"]["b"]
+    L = ex["inputs"]["seq_len"]
+    q = np.array([[1.0, 0.0], [0.0, 1.0]])
+    K = np.array([[[math.log(x), math.log(y)] for x, y in zip(a, b)]])
+    V = np.array([[[float(j), 1.0] for j in range(L)]])
+    p = O.OracleParams(tau_mass=ex["inputs"]["tau_mass"], tau_score=ex["inputs"]["tau_score"],
+                       sm_scale=ex["inputs"]["sm_scale"], r_lo_bp=ex["inputs"]["r_lo_bp"],
+                       r_hi_bp=ex["inputs"]["r_hi_bp"], clamp=ex["inputs"]["clamp"])
+    segs = [tuple(s) for s in ex["inputs"]["segments"]]
+    r = O.decode_step_sequence(q, K, V, L, segs, p)
+    e = ex["expected"]
+    frac = lambda f: f[0] / f[1]
+    np.testing.assert_allclose(r.mass_head, [frac(x) for x in e["mass_head"]], rtol=1e-13)
+    assert r.M_vis == pytest.approx(frac(e["M_vis"]), rel=1e-13)
+    assert r.M_vis_max == pytest.approx(frac(e["M_vis_max"]), rel=1e-13)
+    assert r.k == e["k"]
+    np.testing.assert_allclose(r.scores, e["scores"], rtol=1e-13)
+    assert list(r.vis_idx) == e["vis_idx"]
+    want = np.array([[frac(c) for c in row] for row in e["out"]])
+    np.testing.assert_allclose(r.out, want, rtol=1e-13)
+
+
+# ---------------------------------------------------------------------------
+# budget: closed-form table (Eq. (7) + Sec. 5.2 clamp)
+# ---------------------------------------------------------------------------
+def _budget_rows():
+    rows = []
+    for line in open(os.path.join(GOLDEN, "budget_cases.txt")):
+        line = line.split("#")[0].strip()
+        if not line:
+            continue
+        m, n, lo, hi, c, k = line.split()
+        rows.append((float(m), int(n), int(lo), int(hi), bool(int(c)), int(k)))
+    return rows
+
+
+@pytest.mark.parametrize("m,n,lo,hi,c,k", _budget_rows())
+def test_budget_table(m, n, lo, hi, c, k):
+    assert O.budget(m, n, lo, hi, c) == k
+
+
+def test_budget_monotone_and_bounded():
+    for n in (1, 7, 256, 1296, 4096, 6400, 16384):
+        prev = -1
+        k_lo, k_hi = O.retention_bounds(n, 100, 500)
+        for m in np.linspace(0, 1, 1001):
+            k = O.budget(m, n)
+            assert k >= prev and k_lo <= k <= k_hi and 0 <= k <= n
+            prev = k
+        # unclamped: exact inverse of ceil -- k-1 < m*n <= k
+        for m in np.linspace(0, 1, 257):
+            k = O.budget(m, n, clamp=False)
+            assert k - 1 < m * n <= k or (m == 0 and k == 0)
+
+
+def test_retention_bounds_exact_integers():
+    # 5% of 6400 must be exactly 320 and 1% exactly 64 (no float rounding)
+    assert O.retention_bounds(6400, 100, 500) == (64, 320)
+    assert O.retention_bounds(1296, 100, 500) == (13, 64)
+    assert O.retention_bounds(16384, 100, 500) == (164, 819)
+
+
+# ---------------------------------------------------------------------------
+# mass: definition-level invariants (Eq. (5), Eq. (6))
+# ---------------------------------------------------------------------------
+def test_visual_plus_text_mass_is_one():
+    """P1: the tempered softmax of Eq. (6) runs over all tokens, so the visual and
+    text masses of a head add to one."""
+    rng = np.random.default_rng(1)
+    for tau in (0.1, 0.4, 1.0, 3.0):
+        q, K, V, L, segs = _rand_case(rng)
+        p = O.OracleParams(tau_mass=tau)
+        r = O.decode_step_sequence(q, K, V, L, segs, p, keep_logits=True)
+        txt = O.text_positions(L, segs)
+        m_txt, _, _ = O.visual_mass(r.Z, txt, tau)
+        np.testing.assert_allclose(r.mass_head + m_txt, 1.0, rtol=0, atol=1e-14)
+        assert 0 <= r.M_vis <= r.M_vis_max <= 1
+
+
+def test_scores_sum_to_mass_at_equal_temperature():
+    """P2: summing Eq. (2) over visual tokens gives the mean over heads of Eq. (5),
+    when both use the same (untempered) attention."""
+    rng = np.random.default_rng(2)
+    q, K, V, L, segs = _rand_case(rng, Hq=6, Hkv=3)
+    p = O.OracleParams(tau_mass=1.0, tau_score=1.0, clamp=False)
+    r = O.decode_step_sequence(q, K, V, L, segs, p)
+    assert r.scores.sum() == pytest.approx(r.M_vis, rel=1e-13)
+
+
+def test_zero_query_uniform_attention():
+    """P3: q = 0 makes every logit 0, so every tempered softmax is uniform:
+    m_h = N_v / len for any tau, every score is 1/len, and Top-K keeps the
+    lowest positions (tie rule)."""
+    rng = np.random.default_rng(3)
+    q, K, V, L, segs = _rand_case(rng)
+    q[:] = 0.0
+    n_vis = sum(n for _, n in segs)
+    for tau in (0.1, 1.0):
+        p = O.OracleParams(tau_mass=tau, r_lo_bp=1000, r_hi_bp=5000)
+        r = O.decode_step_sequence(q, K, V, L, segs, p)
+        np.testing.assert_allclose(r.mass_head, n_vis / L, rtol=1e-14)
+        np.testing.assert_allclose(r.scores, 1.0 / L, rtol=1e-14)
+        k = r.k
+        assert k == O.budget(n_vis / L, n_vis, 1000, 5000)
+        vis = O.visual_positions(L, segs)
+        assert list(r.vis_idx) == list(vis[:k])
+        # uniform weights over the pruned context: plain mean of its V rows
+        J = np.sort(np.concatenate([vis[:k], O.text_positions(L, segs)]))
+        for h in range(q.shape[0]):
+            np.testing.assert_allclose(r.out[h], V[h // 2][J].mean(axis=0), rtol=1e-12)
+
+
+def test_temperature_limits():
+    """P4: tau -> infinity flattens Eq. (6) (mass -> N_v/len); tau -> 0 puts all
+    tempered mass on the arg-max token (mass -> 1 if it is visual, else 0)."""
+    rng = np.random.default_rng(4)
+    q, K, V, L, segs = _rand_case(rng)
+    n_vis = sum(n for _, n in segs)
+    vis = set(O.visual_positions(L, segs).tolist())
+    r_hot = O.decode_step_sequence(q, K, V, L, segs, O.OracleParams(tau_mass=1e7), keep_logits=True)
+    np.testing.assert_allclose(r_hot.mass_head, n_vis / L, rtol=1e-5)
+    r_cold = O.decode_step_sequence(q, K, V, L, segs, O.OracleParams(tau_mass=1e-4), keep_logits=True)
+    for h in range(q.shape[0]):
+        want = 1.0 if int(np.argmax(r_cold.Z[h])) in vis else 0.0
+        assert r_cold.mass_head[h] == pytest.approx(want, abs=1e-9)
+
+
+def test_head_max_is_max_and_mean_is_mean():
+    """Eq. (5) mean over heads; the head-max variant of Sec. 4.3 upper-bounds it."""
+    rng = np.random.default_rng(5)
+    q, K, V, L, segs = _rand_case(rng, Hq=8, Hkv=2)
+    r = O.decode_step_sequence(q, K, V, L, segs, O.OracleParams())
+    assert r.M_vis_max == max(r.mass_head) and r.M_vis == pytest.approx(sum(r.mass_head) / 8)
+    assert r.M_vis <= r.M_vis_max
+
+
+# ---------------------------------------------------------------------------
+# logits and the GQA head mapping
+# ---------------------------------------------------------------------------
+def test_onehot_logits_are_exact_integers():
+    """P10: with one-hot q and K rows and sm_scale = 1, the logit of Eq. (6) is the
+    product of the two nonzero entries when they share a coordinate, else 0."""
+    d = 8
+    q = np.zeros(d); q[3] = 5.0
+    K = np.zeros((6, d))
+    K[0, 3] = 2.0; K[1, 4] = 7.0; K[2, 3] = -3.0; K[5, 3] = 1.0
+    Z = O.logits(q, K, 1.0)
+    assert list(Z) == [10.0, 0.0, -15.0, 0.0, 0.0, 5.0]
+    assert list(O.logits(q, K, 0.5)) == [5.0, 0.0, -7.5, 0.0, 0.0, 2.5]
+
+
+def test_gqa_head_to_kv_group_mapping():
+    """Query head h reads KV head h // (Hq/Hkv) (reading A4). Group 0 holds a strong
+    key at position 3, group 1 at position 5; heads 0,1 must peak at 3 and heads
+    2,3 at 5 (a modulo mapping would mix them)."""
+    Hq, Hkv, d, L = 4, 2, 4, 8
+    q = np.tile(np.array([1.0, 0, 0, 0]), (Hq, 1))
+    K = np.zeros((Hkv, L, d))
+    K[0, 3, 0] = 20.0
+    K[1, 5, 0] = 20.0
+    V = np.zeros((Hkv, L, d))
+    V[0, 3, 1] = 1.0
+    V[1, 5, 2] = 1.0
+    r = O.decode_step_sequence(q, K, V, L, [(2, 3)], O.OracleParams(sm_scale=1.0, clamp=False),
+                               keep_logits=True)
+    assert [int(np.argmax(r.Z[h])) for h in range(Hq)] == [3, 3, 5, 5]
+    assert r.out[0, 1] > 0.99 and r.out[1, 1] > 0.99 and r.out[2, 2] > 0.99 and r.out[3, 2] > 0.99
+    # heads 0/1 peak inside the visual segment (2..4), heads 2/3 outside it
+    assert r.mass_head[0] > 0.99 and r.mass_head[2] < 0.01
+
+
+# ---------------------------------------------------------------------------
+# selection (Eq. (3)) against brute force
+# ---------------------------------------------------------------------------
+def _brute_top_k(S, pos, k):
+    """The unique k-subset whose every member beats every non-member under the
+    order (larger S first, then lower position), found by enumeration."""
+    n = len(S)
+    found = []
+    for sub in itertools.combinations(range(n), k):
+        inside = set(sub)
+        ok = all((S[i] > S[j]) or (S[i] == S[j] and pos[i] < pos[j])
+                 for i in inside for j in range(n) if j not in inside)
+        if ok:
+            found.append(sorted(pos[i] for i in sub))
+    assert len(found) == 1
+    return found[0]
+
+
+def test_select_top_k_brute_force():
+    """P6: every k on tiny inputs, including exact ties (scores on a coarse grid)."""
+    rng = np.random.default_rng(6)
+    for trial in range(40):
+        n = int(rng.integers(1, 9))
+        pos = np.sort(rng.choice(np.arange(40), size=n, replace=False))
+        S = np.round(rng.random(n) * 4) / 4 if trial % 2 else rng.random(n)
+        for k in range(0, n + 1):
+            got = list(O.select_top_k(S, pos, k))
+            assert got == (_brute_top_k(S, pos, k) if k else [])
+
+
+def test_selection_invariant_min_selected_ge_max_rest():
+    rng = np.random.default_rng(7)
+    q, K, V, L, segs = _rand_case(rng, L=200, segs=((10, 120),), Hq=4, Hkv=1)
+    r = O.decode_step_sequence(q, K, V, L, segs, O.OracleParams(clamp=False, tau_mass=1.0))
+    vis = O.visual_positions(L, segs)
+    sel = np.isin(vis, r.vis_idx)
+    assert sel.sum() == r.k
+    assert r.scores[sel].min() >= r.scores[~sel].max()
+
+
+# ---------------------------------------------------------------------------
+# pruned attention against the library's attention
+# ---------------------------------------------------------------------------
+def _sdpa(qh, Kg, Vg, scale):
+    qt = torch.from_numpy(qh).reshape(1, 1, 1, -1)
+    kt = torch.from_numpy(np.ascontiguousarray(Kg)).reshape(1, 1, Kg.shape[0], -1)
+    vt = torch.from_numpy(np.ascontiguousarray(Vg)).reshape(1, 1, Vg.shape[0], -1)
+    return torch.nn.functional.scaled_dot_product_attention(qt, kt, vt, scale=scale).reshape(-1).numpy()
+
+
+def test_keep_all_equals_dense_attention():
+    """P7: with every visual token kept the pruned context is the whole cache, so
+    the output is ordinary decode attention (torch SDPA, fp64, CPU)."""
+    rng = np.random.default_rng(8)
+    q, K, V, L, segs = _rand_case(rng, Hq=6, Hkv=2, d=16, L=40, segs=((4, 20),))
+    n_vis = 20
+    r = O.decode_step_sequence(q, K, V, L, segs, O.OracleParams(), k_override=n_vis)
+    for h in range(6):
+        want = _sdpa(q[h], K[h // 3], V[h // 3], 1 / 4.0)
+        np.testing.assert_allclose(r.out[h], want, rtol=1e-12, atol=1e-13)
+
+
+def test_no_visual_tokens_and_single_row():
+    """P8: N_v = 0 gives k = 0 and dense attention over the text; a context of a
+    single row returns that row's value; an empty context returns zeros."""
+    rng = np.random.default_rng(9)
+    q, K, V, L, _ = _rand_case(rng, Hq=2, Hkv=1, d=8, L=12)
+    r = O.decode_step_sequence(q, K, V, L, [], O.OracleParams())
+    assert r.k == 0 and len(r.vis_idx) == 0 and r.M_vis == 0.0
+    for h in range(2):
+        np.testing.assert_allclose(r.out[h], _sdpa(q[h], K[0], V[0], 1 / math.sqrt(8)), rtol=1e-12)
+    np.testing.assert_allclose(O.pruned_attention(q[0], K[0], V[0], np.array([7]), 0.3), V[0, 7], rtol=0)
+    assert np.all(O.pruned_attention(q[0], K[0], V[0], np.array([], dtype=np.int64), 0.3) == 0)
+
+
+def test_pruned_attention_subset_equals_sdpa_on_subset():
+    """Dropped tokens are absent from the softmax (A12): identical to SDPA run on
+    the kept rows only, and independent of the order of J (P9)."""
+    rng = np.random.default_rng(10)
+    q, K, V, L, segs = _rand_case(rng, Hq=2, Hkv=1, d=8, L=30)
+    J = np.array([0, 2, 3, 11, 17, 29])
+    out = O.pruned_attention(q[1], K[0], V[0], J, 0.25)
+    np.testing.assert_allclose(out, _sdpa(q[1], K[0][J], V[0][J], 0.25), rtol=1e-12)
+    out_perm = O.pruned_attention(q[1], K[0], V[0], J[::-1].copy(), 0.25)
+    np.testing.assert_allclose(out, out_perm, rtol=1e-13)
+
+
+def test_common_key_shift_is_invisible():
+    """P11: with one query head per KV head, adding c * q_hat to every key adds the
+    same constant to all logits of that head, which softmax ignores: masses,
+    scores, the budget, the selection and the output are unchanged."""
+    rng = np.random.default_rng(11)
+    q, K, V, L, segs = _rand_case(rng, Hq=3, Hkv=3, d=8, L=50, segs=((5, 30),))
+    p = O.OracleParams(tau_mass=0.4, r_lo_bp=500, r_hi_bp=3000)
+    r0 = O.decode_step_sequence(q, K, V, L, segs, p)
+    K2 = K.copy()
+    for g in range(3):
+        K2[g] += 1.7 * q[g] / np.linalg.norm(q[g])
+    r1 = O.decode_step_sequence(q, K2, V, L, segs, p)
+    np.testing.assert_allclose(r1.mass_head, r0.mass_head, rtol=1e-11)
+    np.testing.assert_allclose(r1.scores, r0.scores, rtol=1e-11)
+    assert r1.k == r0.k and list(r1.vis_idx) == list(r0.vis_idx)
+    np.testing.assert_allclose(r1.out, r0.out, rtol=1e-11)
+
+
+def test_bf16_decoding_exact():
+    bits = np.array([0x3F80, 0xBF80, 0x4049, 0x0000, 0x8000, 0x7F80, 0x3C00], dtype=np.uint16)
+    want = [1.0, -1.0, 3.140625, 0.0, -0.0, math.inf, 2.0 ** -7]
+    got = O.as_f64(bits)
+    assert list(got) == want
+
+
+def test_exact_rational_tiny_case():
+    """Cross-check of Eq. (5)/(6)/(2) in exact rational arithmetic: logits ln(w) make
+    exp(Z) = w, so tau = 1 attention is w / sum(w) exactly."""
+    w = [3, 1, 4, 1, 5, 9, 2, 6]
+    L = len(w)
+    q = np.array([[1.0]])
+    K = np.array([[[math.log(x)] for x in w]])
+    V = np.array([[[float(j)] for j in range(L)]])
+    segs = [(2, 4)]
+    r = O.decode_step_sequence(q, K, V, L, segs, O.OracleParams(tau_mass=1.0, sm_scale=1.0, clamp=False))
+    tot = Fraction(sum(w))
+    assert r.mass_head[0] == pytest.approx(float(Fraction(sum(w[2:6])) / tot), rel=1e-14)
+    np.testing.assert_allclose(r.scores, [float(Fraction(x) / tot) for x in w[2:6]], rtol=1e-14)
+    # k = ceil(19/31 * 4) = ceil(2.45) = 3 -> keep positions of 5, 9, 4 -> {2, 4, 5}
+    assert r.k == 3 and list(r.vis_idx) == [2, 4, 5]
+    J = [0, 1, 2, 4, 5, 6, 7]
+    num = sum(Fraction(w[j]) * j for j in J)
+    den = sum(Fraction(w[j]) for j in J)
+    assert r.out[0, 0] == pytest.approx(float(num / den), rel=1e-14)

@@ -1,0 +1,38 @@
+"""Planting makes the reference's discrete decisions robust (no GPU)."""
+import numpy as np
+
+from oracle import plant as P
+from oracle import vp_oracle as O
+from paper_2605_31457_amd import workloads as W
+
+
+def test_plant_cfg2_gap_and_margin():
+    w = W.generate(2)
+    p = P.params_of(w)
+    res, log = P.plant(w, p)
+    r = res[0]
+    vis = O.visual_positions(int(w.seq_len[0]), w.segments[0])
+    assert P.boundary_gap(r.scores, vis, r.k) >= P.GAP
+    assert P.margin_ok(r.M_vis_max, len(vis), p)
+    # the stored tensor is what the reference read
+    r2 = O.decode_step_sequence(w.q[0], w.K[0], w.V[0], int(w.seq_len[0]), w.segments[0], p)
+    assert list(r2.vis_idx) == list(r.vis_idx) and r2.k == r.k
+
+
+def test_plant_creates_a_gap_where_there_was_none():
+    w = W.generate(4, seqs=[0])
+    p = P.params_of(w)
+    vis = O.visual_positions(int(w.seq_len[0]), w.segments[0])
+    r0 = O.decode_step_sequence(w.q[0], w.K[0], w.V[0], int(w.seq_len[0]), w.segments[0], p)
+    before = P.boundary_gap(r0.scores, vis, r0.k)
+    res, log = P.plant(w, p)
+    after = P.boundary_gap(res[0].scores, vis, res[0].k)
+    assert after >= P.GAP
+    assert before < P.GAP and log[0]["n_edits"] > 0   # this seed needs planting
+    assert res[0].k == 819
+
+
+def test_margin_detects_integer_crossing():
+    p = O.OracleParams(clamp=False)
+    assert not P.margin_ok(0.5, 256, p)          # 128 exactly: 127.99 vs 128.01
+    assert P.margin_ok(0.502, 256, p)
