@@ -1,0 +1,219 @@
+#!/usr/bin/env python3
+"""Throughput of the VisionPulse per-decode-step path on one MI355X.
+
+One step = vp_visual_mass -> vp_budget -> vp_select_topk -> vp_sparse_decode_attn
+over the whole batch on one layer's KV cache (the anchor layer), with the text
+attention fused into the mass pass. Inputs are seeded synthetic tensors shaped
+like the paper's LMM decode workloads (paper_2605_31457_amd.workloads), resident
+in HBM before timing. To keep the 256 MB Infinity Cache from serving the cache
+reads, the step rotates over R distinct copies of the KV cache (R * KV bytes
+>= 1 GiB), as a real model's layers would.
+
+Prints one JSON line: steps/s, the roofline of the dominant kernel (the
+streaming pass, timed with HIP events recorded around its launch inside the
+timed steps) and the fp64 reference timed on this host's cores.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import math
+import os
+import sys
+import time
+
+PEAK_HBM_GBS = 8000.0   # MI355X HBM3E, 8 TB/s
+MALL_DEFEAT_BYTES = 1 << 30
+
+WORKLOAD_NAMES = {
+    1: "tiny fp32 check: B=1, 4/1 heads, d=64, 16 text + 256 visual + 112 text",
+    2: "7B-class decode layer: B=1, 28/4 heads, d=128, 1296 visual (36x36) at 14 + 2048 text",
+    3: "7B-class ragged batch: B=16, 28/4 heads, d=128, 4096 visual + U{1024..8192} text",
+    4: "7B-class multi-image 32k: B=64, 28/4 heads, d=128, 4 x 4096 visual + 16384 text",
+    5: "72B-class decode: B=8, 64/8 heads, d=128, 6400 visual + 4097 text (loop step 0)",
+}
+DEFAULT_STEPS = {1: (200, 20), 2: (400, 40), 3: (100, 10), 4: (20, 3), 5: (100, 10)}
+
+
+class Hip:
+    """hipEvent helpers through the HIP runtime's C API."""
+
+    def __init__(self):
+        self.h = ctypes.CDLL("libamdhip64.so")
+        self.h.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.h.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self.h.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.h.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.h.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+    def event(self):
+        e = ctypes.c_void_p()
+        assert self.h.hipEventCreate(ctypes.byref(e)) == 0
+        return e
+
+    def elapsed_ms(self, a, b):
+        t = ctypes.c_float()
+        assert self.h.hipEventElapsedTime(ctypes.byref(t), a, b) == 0
+        return t.value
+
+
+def algorithmic_bytes(w, ks):
+    """Bytes the method must move at least once per step.
+
+    Context pass: every cached K row (the Eq. (6) logits need all of them) and
+    the V rows of text tokens. Kept pass: K and V rows of the k kept visual
+    tokens. q, outputs, scores and indices are < 1% and not counted."""
+    esz = 2 if w.dtype == "bf16" else 4
+    row = w.Hkv * w.d * esz
+    ctx = 0
+    kept = 0
+    for b in range(w.B):
+        L = int(w.seq_len[b])
+        nv = sum(n for _, n in w.segments[b])
+        ctx += L * row + (L - nv) * row
+        kept += 2 * int(ks[b]) * row
+    return ctx, kept
+
+
+def cpu_baseline(w, budget_s: float):
+    """fp64 reference on this host: whole sequences until about budget_s seconds."""
+    import numpy as np
+    from oracle import vp_oracle as O
+    from oracle.plant import params_of
+    p = params_of(w)
+    t0 = time.perf_counter()
+    c0 = time.process_time()
+    n = 0
+    while True:
+        b = n % w.B
+        O.decode_step_sequence(w.q[b], w.K[b], w.V[b], int(w.seq_len[b]), w.segments[b], p)
+        n += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s and n >= 1:
+            break
+    cpu = time.process_time() - c0
+    per_seq = el / n
+    steps_per_s = 1.0 / (per_seq * w.B)
+    del np
+    return {"value": steps_per_s, "unit": "steps/s", "cores": max(1, round(cpu / el)), "kind": "oracle",
+            "sample": f"{n} sequence-steps of this workload's batch (sequences 0..{min(n, w.B) - 1}), "
+                      f"{el:.1f} s wall; steps/s = 1 / (mean time per sequence x B={w.B})"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=None)
+    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--rotate", type=int, default=0, help="KV copies to rotate over (0: >= 1 GiB)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py runs on one GPU only: the VisionPulse step is measured on a single MI355X "
+              "(sequences shard across GPUs with no exchange; see the design notes). Use --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2605_31457_amd import step as S
+    from paper_2605_31457_amd import vp
+    from paper_2605_31457_amd import workloads as W
+
+    cfg = args.config
+    steps, warmup = DEFAULT_STEPS[cfg]
+    steps = args.steps if args.steps is not None else steps
+    warmup = args.warmup if args.warmup is not None else warmup
+
+    vp.lib()  # fail loudly if the HIP library is missing
+    print(f"[bench] generating config {cfg}", file=sys.stderr, flush=True)
+    w = W.generate(cfg)
+    ds = S.DeviceStep(w)
+    kv_bytes = ds.K.numel() * ds.K.element_size() * 2
+    R = args.rotate or max(1, math.ceil(MALL_DEFEAT_BYTES / kv_bytes))
+    bufs = [(ds.K, ds.V)]
+    for _ in range(R - 1):
+        bufs.append((ds.K.clone(), ds.V.clone()))
+    torch.cuda.synchronize()
+    print(f"[bench] {w.name}: KV {kv_bytes / 1e6:.1f} MB x {R} rotated copies; steps={steps} warmup={warmup}",
+          file=sys.stderr, flush=True)
+
+    hip = Hip()
+    stream = torch.cuda.current_stream()
+    sp = stream.cuda_stream
+    ev_b = [hip.event() for _ in range(steps)]
+    ev_e = [hip.event() for _ in range(steps)]
+    ev_t0, ev_t1 = hip.event(), hip.event()
+
+    def one_step(i, evs=(None, None)):
+        K, V = bufs[i % R]
+        vp.vp_visual_mass_timed(ds.shape, ds.layout, ds.params, ds.q, K, V, ds.mass_head, ds.mass_seq,
+                                ds.scores, ds.ws, ds.ws_bytes, sp, evs[0], evs[1])
+        vp.vp_budget(ds.shape, ds.layout, ds.params, ds.mass_seq, ds.k, sp)
+        vp.vp_select_topk(ds.shape, ds.layout, ds.scores, ds.k, ds.vis_idx, sp)
+        vp.vp_sparse_decode_attn(ds.shape, ds.layout, ds.params, ds.q, K, V, ds.vis_idx, ds.k, ds.out,
+                                 vp.VP_ATTN_TEXT_FROM_WORKSPACE, ds.ws, ds.ws_bytes, sp)
+
+    for i in range(warmup):
+        one_step(i)
+    torch.cuda.synchronize()
+    ks = ds.k.cpu().numpy().copy()
+
+    hip.h.hipEventRecord(ev_t0, sp)
+    t0 = time.perf_counter()
+    for i in range(steps):
+        one_step(warmup + i, (ev_b[i], ev_e[i]))
+    hip.h.hipEventRecord(ev_t1, sp)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    gpu_ms = hip.elapsed_ms(ev_t0, ev_t1)
+    kern_ms = [hip.elapsed_ms(ev_b[i], ev_e[i]) for i in range(steps)]
+    assert np.array_equal(ds.k.cpu().numpy(), ks), "budget changed between warm-up and timed steps"
+
+    ctx_bytes, kept_bytes = algorithmic_bytes(w, ks)
+    ms_per_step = wall * 1e3 / steps
+    kern_avg_ms = float(np.mean(kern_ms))
+    achieved = ctx_bytes / (kern_avg_ms * 1e-3) / 1e9
+    step_gbs = (ctx_bytes + kept_bytes) / (ms_per_step * 1e-3) / 1e9
+
+    res = {
+        "metric": "pruned decode-attention steps/s per layer; achieved HBM GB/s vs peak",
+        "value": steps / wall,
+        "unit": "steps/s",
+        "n_gpus": 1,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic (seeded; shapes of the paper's LMM decode workloads)",
+        "config": {"workload": f"config {cfg}: {WORKLOAD_NAMES[cfg]}", "batch": w.B, "q_heads": w.Hq,
+                   "kv_heads": w.Hkv, "head_dim": w.d, "max_seq_len": w.S_cap, "visual_tokens": int(w.n_vis[0]),
+                   "tau_mass": w.tau_mass, "retention_clamp_bp": [w.r_lo_bp, w.r_hi_bp],
+                   "kept_k": [int(x) for x in ks[:8]], "kv_rotation": R, "parallelism": "single GPU"},
+        "step_algorithmic_bytes": ctx_bytes + kept_bytes,
+        "step_achieved_GBps": step_gbs,
+        "step_frac_of_peak": step_gbs / PEAK_HBM_GBS,
+        "gpu_event_ms_per_step": gpu_ms / steps,
+        "roofline": {"kernel": "context pass (scores + mass + text attention partial)", "bound": "hbm",
+                     "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS,
+                     "traffic": None, "algorithmic_bytes_per_launch": ctx_bytes,
+                     "avg_launch_ms": kern_avg_ms},
+    }
+    if not args.no_cpu_baseline:
+        print("[bench] timing the fp64 reference on the host", file=sys.stderr, flush=True)
+        res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

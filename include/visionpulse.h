@@ -1,0 +1,203 @@
+/*
+ * visionpulse.h -- C ABI of the VisionPulse per-decode-step path on AMD
+ * Instinct MI355X (gfx950).
+ *
+ * VisionPulse (arXiv 2605.31457) prunes visual tokens at every decoding step:
+ * at the anchor layer the current query is scored against the whole KV cache,
+ * the tempered attention mass that falls on visual tokens sets a budget k, the
+ * k visual tokens with the largest head-averaged attention are kept, and the
+ * step's attention runs over the kept visual tokens plus every text token.
+ * One step is four calls, in this order, on one stream:
+ *
+ *   vp_visual_mass         Eq. (5)/(6) mass and Eq. (2) scores     (Sec. 4.2, 4.3)
+ *   vp_budget              Eq. (7) budget with the Sec. 5.2 clamp  (Sec. 4.3, 5.2)
+ *   vp_select_topk         Eq. (3) Top-K_t selection               (Sec. 4.2)
+ *   vp_sparse_decode_attn  attention over kept visual + text KV    (Sec. 4.1, 4.2)
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Memory.   All tensor arguments are DEVICE pointers owned by the caller; the
+ *           library allocates nothing and keeps no state between calls, so it
+ *           is reentrant. Scratch memory is the caller's workspace, sized by
+ *           vp_workspace_size().
+ * Streams.  `stream` is a hipStream_t (NULL = the legacy default stream). Every
+ *           call only enqueues kernels on that stream and returns; none
+ *           synchronises. k and the kept indices stay on the device, so a step
+ *           never waits for the host.
+ * Shapes.   q and out are [B, Hq, d] contiguous. K and V caches are addressed as
+ *           base + b*kv_stride_b + h*kv_stride_h + s*kv_stride_s (elements) with
+ *           the d elements of a row contiguous. Query head h reads KV head
+ *           h / (Hq/Hkv) (grouped-query attention).
+ * Layout.   Each sequence b holds seq_len[b] cached tokens. Its visual tokens
+ *           X_v (Sec. 4.2) are the union of the segments
+ *           vis_seg[vis_seg_off[b] .. vis_seg_off[b+1]), each {start, length},
+ *           ascending and disjoint inside [0, seq_len[b]); every other position
+ *           is text (system prompt, question, generated trace, current token).
+ *           A visual token's "rank" is its index among the visual tokens of
+ *           its sequence in position order. Device-resident layout contents are
+ *           trusted; kernels clip them (seq_len to max_seq_len, segments to the
+ *           sequence and to the previous segment's end, ranks to max_vis) so
+ *           that malformed layouts cannot cause out-of-bounds accesses.
+ * Errors.   Host-checkable problems (null pointers, unsupported shapes, small
+ *           workspace, bad parameters) return an error before anything is
+ *           enqueued. A failed kernel launch returns VP_ERR_HIP.
+ * Dtypes.   VP_BF16: q, K, V, out are bfloat16; VP_F32: all float32. Logits,
+ *           softmax statistics, masses and scores are float32; accumulation is
+ *           float32 (bf16 products are exact in float32).
+ */
+#ifndef VISIONPULSE_H
+#define VISIONPULSE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum vp_status {
+  VP_OK = 0,
+  VP_ERR_NULL = 1,         /* a required pointer is NULL */
+  VP_ERR_SHAPE = 2,        /* inconsistent sizes (Hq % Hkv, strides, k_cap ...) */
+  VP_ERR_RANGE = 3,        /* a parameter is outside its domain (tau <= 0, bp ...) */
+  VP_ERR_DTYPE = 4,        /* dtype is neither VP_F32 nor VP_BF16 */
+  VP_ERR_UNSUPPORTED = 5,  /* valid but not implemented (head_dim, group size ...) */
+  VP_ERR_WORKSPACE = 6,    /* workspace NULL or smaller than vp_workspace_size() */
+  VP_ERR_HIP = 7           /* a HIP runtime call or kernel launch failed */
+} vp_status;
+
+typedef enum vp_dtype { VP_F32 = 0, VP_BF16 = 1 } vp_dtype;
+
+/* Host-side description of one step's tensors (validated synchronously). */
+typedef struct vp_shape {
+  int32_t batch;        /* B >= 1 */
+  int32_t n_q_heads;    /* Hq >= 1 */
+  int32_t n_kv_heads;   /* Hkv >= 1, Hq % Hkv == 0, Hq / Hkv <= 16 */
+  int32_t head_dim;     /* d: 64 or 128 */
+  int32_t dtype;        /* vp_dtype of q, K, V and out */
+  int32_t max_seq_len;  /* cache capacity; every seq_len[b] <= max_seq_len */
+  int32_t max_vis;      /* >= N_v of every sequence; row stride of scores */
+  int32_t max_segs;     /* >= visual segments of any sequence; <= 256 */
+  int32_t k_cap;        /* row stride of vis_idx; >= every budget vp_budget can return */
+  int32_t reserved;     /* must be 0 */
+  int64_t kv_stride_b;  /* elements between sequences in K and V */
+  int64_t kv_stride_h;  /* elements between KV heads */
+  int64_t kv_stride_s;  /* elements between token rows (>= head_dim) */
+} vp_shape;
+
+/* Device-resident token layout (Sec. 4.2: X_v = {v_1 .. v_N}; the rest is text). */
+typedef struct vp_layout {
+  const int32_t* seq_len;      /* [B] cached tokens per sequence */
+  const int32_t* vis_seg_off;  /* [B+1] CSR offsets into vis_seg */
+  const int32_t* vis_seg;      /* [n_seg][2] {start, length} visual segments */
+} vp_layout;
+
+/* Method parameters (host-side). */
+typedef struct vp_params {
+  float tau_mass;   /* tau of Eq. (6) for the mass, > 0 (0.1 for the 5% preset, 0.4 for 10%; App. B.1) */
+  float tau_score;  /* temperature of the attention used by the Eq. (2) scores, > 0 (1.0) */
+  float sm_scale;   /* logit scale of Z; <= 0 selects 1/sqrt(head_dim) */
+  int32_t r_lo_bp;  /* budget clamp lower bound, basis points of N_v (100 = 1%, Sec. 5.2) */
+  int32_t r_hi_bp;  /* budget clamp upper bound, basis points of N_v (500 = 5%) */
+  int32_t clamp;    /* 1: clamp K_t to [ceil(r_lo N_v), floor(r_hi N_v)]; 0: K_t = ceil(M N_v) */
+} vp_params;
+
+/* vp_sparse_decode_attn flags */
+#define VP_ATTN_TEXT_FROM_WORKSPACE 1  /* reuse the text-KV partial left by vp_visual_mass (V != NULL) */
+
+/* Human-readable name of a status code (static string). */
+const char* vp_status_string(vp_status status);
+
+/* Detail of the most recent error returned on the calling thread ("" if none). */
+const char* vp_last_error(void);
+
+/* Bytes of device workspace the calls need for `shape` (at most 256-byte
+ * aligned pieces; pass a 256-byte aligned pointer). Pure host computation. */
+vp_status vp_workspace_size(const vp_shape* shape, size_t* bytes);
+
+/*
+ * vp_visual_mass -- Eq. (6) tempered attention of the current query over the
+ * whole cache, Eq. (5) visual mass per head, its head mean and head max
+ * (Sec. 4.3), and the Eq. (2) importance score of every visual token (Sec. 4.2).
+ *
+ *   Z_{h,j}      = sm_scale * <q_h, K_{g(h), j}>                j < seq_len
+ *   mass_head    = sum_{j visual} softmax_j(Z_h / tau_mass)      [B, Hq]
+ *   mass_seq     = {mean_h mass_head, max_h mass_head}           [B, 2]
+ *   scores[b, i] = (1/Hq) sum_h softmax_j(Z_h / tau_score)_{v_i} [B, max_vis], rank order;
+ *                  entries i >= N_v of the sequence are not written.
+ *
+ * q: [B, Hq, d]; K: cache; V: cache or NULL. When V is non-NULL the same pass
+ * over K also accumulates the softmax-weighted text-token values (the text
+ * part of the pruned attention) into `workspace`, for a later
+ * vp_sparse_decode_attn(..., VP_ATTN_TEXT_FROM_WORKSPACE) with the same
+ * q, K, V, layout and workspace. The workspace is used between the kernels of
+ * this call and must not be shared by concurrent calls.
+ */
+vp_status vp_visual_mass(const vp_shape* shape, const vp_layout* layout, const vp_params* params,
+                         const void* q, const void* K, const void* V,
+                         float* mass_head, float* mass_seq, float* scores,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * vp_visual_mass_timed -- vp_visual_mass that also records two caller-created
+ * HIP events (hipEvent_t, may be NULL) on `stream` immediately before and
+ * after the launch of its streaming pass over the cache, so a profiler or
+ * benchmark can time that kernel alone with hipEventElapsedTime. Results are
+ * identical to vp_visual_mass.
+ */
+vp_status vp_visual_mass_timed(const vp_shape* shape, const vp_layout* layout, const vp_params* params,
+                               const void* q, const void* K, const void* V,
+                               float* mass_head, float* mass_seq, float* scores,
+                               void* workspace, size_t workspace_bytes, void* stream,
+                               void* ev_pass_begin, void* ev_pass_end);
+
+/*
+ * vp_budget -- Eq. (7): K_t = M_vis,max * N_v rounded up, clamped to
+ * [ceil(r_lo N_v), floor(r_hi N_v)] (Sec. 5.2; k_hi raised to k_lo if needed)
+ * and to [0, N_v]. The product is formed in double from the float mass, so the
+ * rounding decision is exact. N_v = 0 gives 0.
+ *
+ * mass_seq: [B, 2] device (column 1 = M_vis,max); k: [B] int32 device.
+ */
+vp_status vp_budget(const vp_shape* shape, const vp_layout* layout, const vp_params* params,
+                    const float* mass_seq, int32_t* k, void* stream);
+
+/*
+ * vp_select_topk -- Eq. (3): for every sequence, the k[b] visual tokens with the
+ * largest score, ties to the lower position; written as absolute cache
+ * positions in ascending order to vis_idx[b, 0 .. k[b]) and -1 in
+ * vis_idx[b, k[b] .. k_cap). k[b] is clamped to [0, min(N_v, k_cap)].
+ *
+ * scores: [B, max_vis] float (from vp_visual_mass); k: [B] int32 device;
+ * vis_idx: [B, k_cap] int32 device.
+ */
+vp_status vp_select_topk(const vp_shape* shape, const vp_layout* layout,
+                         const float* scores, const int32_t* k, int32_t* vis_idx, void* stream);
+
+/*
+ * vp_sparse_decode_attn -- the step's attention over the pruned context
+ * J_b = {vis_idx[b, 0 .. k[b])} U {text positions of b} (Sec. 4.1/4.2; the
+ * dropped visual tokens are absent from the softmax, which is renormalised
+ * over J_b at temperature 1):
+ *
+ *   out[b, h] = sum_{j in J_b} softmax_{J_b}(Z_{h, j}) V_{g(h), j}      [B, Hq, d]
+ *
+ * An empty J_b yields zeros. Kept indices outside [0, seq_len) or equal to -1
+ * are skipped. With flags & VP_ATTN_TEXT_FROM_WORKSPACE the text part is taken
+ * from the workspace filled by vp_visual_mass (V non-NULL, same inputs);
+ * otherwise this call reads the text K/V itself.
+ */
+vp_status vp_sparse_decode_attn(const vp_shape* shape, const vp_layout* layout, const vp_params* params,
+                                const void* q, const void* K, const void* V,
+                                const int32_t* vis_idx, const int32_t* k, void* out, int32_t flags,
+                                void* workspace, size_t workspace_bytes, void* stream);
+
+/* Host mirror of vp_budget's rule for one sequence (pure; for callers that keep
+ * the mass on the host). Returns -1 for invalid parameters. */
+int32_t vp_budget_host(double m_max, int32_t n_vis, const vp_params* params);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* VISIONPULSE_H */

@@ -1,0 +1,347 @@
+// C ABI of the VisionPulse decode-step path: argument validation, workspace
+// carving and kernel launches on the caller's stream (no allocation, no sync).
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+
+#include "vp_internal.h"
+
+namespace vp {
+namespace {
+
+thread_local std::string g_last_error;
+
+vp_status fail(vp_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+vp_status fail(vp_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+vp_status hip_fail(hipError_t e, const char* what) {
+  return fail(VP_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr int kMaxGroup = 16;
+constexpr int kMaxHq = 1024;
+constexpr int kMaxBatch = 65535;
+
+size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
+
+vp_status check_shape(const vp_shape* s) {
+  if (!s) return fail(VP_ERR_NULL, "shape is NULL");
+  if (s->dtype != VP_F32 && s->dtype != VP_BF16) return fail(VP_ERR_DTYPE, "dtype %d", s->dtype);
+  if (s->batch < 1 || s->batch > kMaxBatch) return fail(VP_ERR_SHAPE, "batch %d outside [1, %d]", s->batch, kMaxBatch);
+  if (s->n_q_heads < 1 || s->n_kv_heads < 1) return fail(VP_ERR_SHAPE, "head counts must be >= 1");
+  if (s->n_q_heads % s->n_kv_heads != 0)
+    return fail(VP_ERR_SHAPE, "n_q_heads %d not a multiple of n_kv_heads %d", s->n_q_heads, s->n_kv_heads);
+  if (s->n_q_heads / s->n_kv_heads > kMaxGroup)
+    return fail(VP_ERR_UNSUPPORTED, "query group %d > %d", s->n_q_heads / s->n_kv_heads, kMaxGroup);
+  if (s->n_q_heads > kMaxHq) return fail(VP_ERR_UNSUPPORTED, "n_q_heads %d > %d", s->n_q_heads, kMaxHq);
+  if (s->head_dim != 64 && s->head_dim != 128) return fail(VP_ERR_UNSUPPORTED, "head_dim %d (64 or 128)", s->head_dim);
+  if (s->max_seq_len < 1) return fail(VP_ERR_SHAPE, "max_seq_len %d < 1", s->max_seq_len);
+  if (s->max_vis < 1) return fail(VP_ERR_SHAPE, "max_vis %d < 1", s->max_vis);
+  if (s->max_segs < 0 || s->max_segs > 256) return fail(VP_ERR_UNSUPPORTED, "max_segs %d outside [0, 256]", s->max_segs);
+  if (s->k_cap < 1) return fail(VP_ERR_SHAPE, "k_cap %d < 1", s->k_cap);
+  if (s->reserved != 0) return fail(VP_ERR_SHAPE, "reserved field must be 0");
+  const int esz = s->dtype == VP_BF16 ? 2 : 4;
+  const int64_t align_elems = 16 / esz;
+  if (s->kv_stride_s < s->head_dim) return fail(VP_ERR_SHAPE, "kv_stride_s %lld < head_dim", (long long)s->kv_stride_s);
+  if (s->kv_stride_b < 0 || s->kv_stride_h < 0) return fail(VP_ERR_SHAPE, "negative KV stride");
+  if (s->kv_stride_s % align_elems || s->kv_stride_h % align_elems || s->kv_stride_b % align_elems)
+    return fail(VP_ERR_SHAPE, "KV strides must be multiples of %lld elements (16-byte rows)", (long long)align_elems);
+  return VP_OK;
+}
+
+vp_status check_params(const vp_params* p) {
+  if (!p) return fail(VP_ERR_NULL, "params is NULL");
+  if (!(p->tau_mass > 0.f) || !std::isfinite(p->tau_mass)) return fail(VP_ERR_RANGE, "tau_mass must be > 0");
+  if (!(p->tau_score > 0.f) || !std::isfinite(p->tau_score)) return fail(VP_ERR_RANGE, "tau_score must be > 0");
+  if (!std::isfinite(p->sm_scale)) return fail(VP_ERR_RANGE, "sm_scale not finite");
+  if (p->r_lo_bp < 0 || p->r_lo_bp > 10000 || p->r_hi_bp < 0 || p->r_hi_bp > 10000)
+    return fail(VP_ERR_RANGE, "retention bounds must lie in [0, 10000] basis points");
+  if (p->clamp != 0 && p->clamp != 1) return fail(VP_ERR_RANGE, "clamp must be 0 or 1");
+  return VP_OK;
+}
+
+vp_status check_layout(const vp_layout* l) {
+  if (!l) return fail(VP_ERR_NULL, "layout is NULL");
+  if (!l->seq_len || !l->vis_seg_off || !l->vis_seg)
+    return fail(VP_ERR_NULL, "layout seq_len / vis_seg_off / vis_seg is NULL");
+  return VP_OK;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+vp_status check_ws(const vp_shape* s, void* ws, size_t bytes, Plan& plan) {
+  plan = make_plan(*s);
+  if (!ws) return fail(VP_ERR_WORKSPACE, "workspace is NULL");
+  if ((reinterpret_cast<uintptr_t>(ws) & 255u) != 0) return fail(VP_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (bytes < plan.total) return fail(VP_ERR_WORKSPACE, "workspace %zu bytes < %zu needed", bytes, plan.total);
+  return VP_OK;
+}
+
+float zscale_of(const vp_shape* s, const vp_params* p) {
+  const float sm = p->sm_scale > 0.f ? p->sm_scale : 1.0f / std::sqrt(static_cast<float>(s->head_dim));
+  return sm * 1.4426950408889634f;  // log2(e)
+}
+
+int max_budget(const vp_shape* s, const vp_params* p) {
+  if (!p->clamp) return s->max_vis;
+  int hi = floor_bp(s->max_vis, p->r_hi_bp);
+  const int lo = ceil_bp(s->max_vis, p->r_lo_bp);
+  if (hi < lo) hi = lo;
+  return hi < s->max_vis ? hi : s->max_vis;
+}
+
+AttendArgs attend_args(const vp_shape* s, const vp_layout* l, const vp_params* p, const Plan& plan, char* ws,
+                       const void* q, const void* K, const void* V) {
+  AttendArgs a{};
+  a.q = q;
+  a.K = K;
+  a.V = V;
+  a.sb = s->kv_stride_b;
+  a.sh = s->kv_stride_h;
+  a.ss = s->kv_stride_s;
+  a.seq_len = l->seq_len;
+  a.seg_off = l->vis_seg_off;
+  a.seg = l->vis_seg;
+  a.B = s->batch;
+  a.Hq = s->n_q_heads;
+  a.Hkv = s->n_kv_heads;
+  a.G = s->n_q_heads / s->n_kv_heads;
+  a.max_seq_len = s->max_seq_len;
+  a.max_vis = s->max_vis;
+  a.zscale = zscale_of(s, p);
+  a.inv_tau_m = 1.0f / p->tau_mass;
+  a.inv_tau_s = 1.0f / p->tau_score;
+  a.chunk = plan.chunk;
+  a.nchunk = plan.nchunk;
+  a.zs = reinterpret_cast<float*>(ws + plan.zs);
+  a.stats = reinterpret_cast<float*>(ws + plan.stats);
+  a.acc = reinterpret_cast<float*>(ws + plan.acc);
+  a.k_cap = s->k_cap;
+  a.split = plan.split;
+  a.nsplit = plan.nsplit;
+  a.kstats = reinterpret_cast<float*>(ws + plan.kstats);
+  a.kacc = reinterpret_cast<float*>(ws + plan.kacc);
+  return a;
+}
+
+}  // namespace
+
+Plan make_plan(const vp_shape& s) {
+  Plan p{};
+  // Context pass: about 4096 one-wave work-groups (16 resident per CU on 256
+  // CUs), chunks of 64 .. 2048 positions in whole 32-row tiles.
+  const int64_t rows = static_cast<int64_t>(s.batch) * s.n_kv_heads * s.max_seq_len;
+  int64_t chunk = (rows + 4095) / 4096;
+  chunk = ((chunk + 31) / 32) * 32;
+  if (chunk < 64) chunk = 64;
+  if (chunk > 2048) chunk = 2048;
+  p.chunk = static_cast<int>(chunk);
+  p.nchunk = static_cast<int>((s.max_seq_len + chunk - 1) / chunk);
+  p.split = 64;
+  p.nsplit = (s.k_cap + p.split - 1) / p.split;
+  const size_t B = s.batch, Hq = s.n_q_heads, d = s.head_dim;
+  size_t off = 0;
+  p.zs = off;
+  off = align256(off + B * Hq * static_cast<size_t>(s.max_vis) * 4);
+  p.stats = off;
+  off = align256(off + B * Hq * p.nchunk * 8 * 4);
+  p.acc = off;
+  off = align256(off + B * Hq * p.nchunk * d * 4);
+  p.head = off;
+  off = align256(off + B * Hq * 2 * 4);
+  p.kstats = off;
+  off = align256(off + B * Hq * p.nsplit * 2 * 4);
+  p.kacc = off;
+  off = align256(off + B * Hq * p.nsplit * d * 4);
+  p.total = off;
+  return p;
+}
+
+}  // namespace vp
+
+using namespace vp;
+
+extern "C" {
+
+const char* vp_status_string(vp_status s) {
+  switch (s) {
+    case VP_OK: return "VP_OK";
+    case VP_ERR_NULL: return "VP_ERR_NULL";
+    case VP_ERR_SHAPE: return "VP_ERR_SHAPE";
+    case VP_ERR_RANGE: return "VP_ERR_RANGE";
+    case VP_ERR_DTYPE: return "VP_ERR_DTYPE";
+    case VP_ERR_UNSUPPORTED: return "VP_ERR_UNSUPPORTED";
+    case VP_ERR_WORKSPACE: return "VP_ERR_WORKSPACE";
+    case VP_ERR_HIP: return "VP_ERR_HIP";
+  }
+  return "VP_ERR_UNKNOWN";
+}
+
+const char* vp_last_error(void) { return g_last_error.c_str(); }
+
+vp_status vp_workspace_size(const vp_shape* shape, size_t* bytes) {
+  g_last_error.clear();
+  if (vp_status e = check_shape(shape)) return e;
+  if (!bytes) return fail(VP_ERR_NULL, "bytes is NULL");
+  *bytes = make_plan(*shape).total;
+  return VP_OK;
+}
+
+int32_t vp_budget_host(double m_max, int32_t n_vis, const vp_params* params) {
+  if (!params || check_params(params) != VP_OK || n_vis < 0) return -1;
+  return budget_rule(m_max, n_vis, params->r_lo_bp, params->r_hi_bp, params->clamp);
+}
+
+vp_status vp_visual_mass_timed(const vp_shape* shape, const vp_layout* layout, const vp_params* params,
+                               const void* q, const void* K, const void* V, float* mass_head, float* mass_seq,
+                               float* scores, void* workspace, size_t workspace_bytes, void* stream,
+                               void* ev_pass_begin, void* ev_pass_end) {
+  g_last_error.clear();
+  if (vp_status e = check_shape(shape)) return e;
+  if (vp_status e = check_layout(layout)) return e;
+  if (vp_status e = check_params(params)) return e;
+  if (!q || !K || !mass_head || !mass_seq || !scores) return fail(VP_ERR_NULL, "q, K, mass_head, mass_seq, scores required");
+  if (!aligned16(q) || !aligned16(K) || (V && !aligned16(V))) return fail(VP_ERR_SHAPE, "q, K, V must be 16-byte aligned");
+  Plan plan;
+  if (vp_status e = check_ws(shape, workspace, workspace_bytes, plan)) return e;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  AttendArgs a = attend_args(shape, layout, params, plan, ws, q, K, V);
+  if (ev_pass_begin)
+    if (hipError_t e = hipEventRecord(static_cast<hipEvent_t>(ev_pass_begin), st)) return hip_fail(e, "event record");
+  if (hipError_t e = launch_attend(a, V ? MODE_SCORE_TEXT : MODE_SCORE, shape->dtype, shape->head_dim, st))
+    return hip_fail(e, "context pass launch");
+  if (ev_pass_end)
+    if (hipError_t e = hipEventRecord(static_cast<hipEvent_t>(ev_pass_end), st)) return hip_fail(e, "event record");
+  MassArgs m{};
+  m.seq_len = layout->seq_len;
+  m.seg_off = layout->vis_seg_off;
+  m.seg = layout->vis_seg;
+  m.B = shape->batch;
+  m.Hq = shape->n_q_heads;
+  m.max_seq_len = shape->max_seq_len;
+  m.max_vis = shape->max_vis;
+  m.chunk = plan.chunk;
+  m.nchunk = plan.nchunk;
+  m.inv_tau_m = a.inv_tau_m;
+  m.inv_tau_s = a.inv_tau_s;
+  m.stats = a.stats;
+  m.zs = a.zs;
+  m.head = reinterpret_cast<float*>(ws + plan.head);
+  m.mass_head = mass_head;
+  m.mass_seq = mass_seq;
+  m.scores = scores;
+  if (hipError_t e = launch_mass_finalize(m, st)) return hip_fail(e, "mass finalize launch");
+  if (hipError_t e = launch_scores(m, st)) return hip_fail(e, "scores launch");
+  return VP_OK;
+}
+
+vp_status vp_visual_mass(const vp_shape* shape, const vp_layout* layout, const vp_params* params, const void* q,
+                         const void* K, const void* V, float* mass_head, float* mass_seq, float* scores,
+                         void* workspace, size_t workspace_bytes, void* stream) {
+  return vp_visual_mass_timed(shape, layout, params, q, K, V, mass_head, mass_seq, scores, workspace,
+                              workspace_bytes, stream, nullptr, nullptr);
+}
+
+vp_status vp_budget(const vp_shape* shape, const vp_layout* layout, const vp_params* params, const float* mass_seq,
+                    int32_t* k, void* stream) {
+  g_last_error.clear();
+  if (vp_status e = check_shape(shape)) return e;
+  if (vp_status e = check_layout(layout)) return e;
+  if (vp_status e = check_params(params)) return e;
+  if (!mass_seq || !k) return fail(VP_ERR_NULL, "mass_seq and k required");
+  if (shape->k_cap < max_budget(shape, params))
+    return fail(VP_ERR_SHAPE, "k_cap %d < largest budget %d for max_vis %d", shape->k_cap, max_budget(shape, params),
+                shape->max_vis);
+  BudgetArgs b{};
+  b.seq_len = layout->seq_len;
+  b.seg_off = layout->vis_seg_off;
+  b.seg = layout->vis_seg;
+  b.B = shape->batch;
+  b.max_seq_len = shape->max_seq_len;
+  b.r_lo_bp = params->r_lo_bp;
+  b.r_hi_bp = params->r_hi_bp;
+  b.clamp = params->clamp;
+  b.mass_seq = mass_seq;
+  b.k = k;
+  if (hipError_t e = launch_budget(b, static_cast<hipStream_t>(stream))) return hip_fail(e, "budget launch");
+  return VP_OK;
+}
+
+vp_status vp_select_topk(const vp_shape* shape, const vp_layout* layout, const float* scores, const int32_t* k,
+                         int32_t* vis_idx, void* stream) {
+  g_last_error.clear();
+  if (vp_status e = check_shape(shape)) return e;
+  if (vp_status e = check_layout(layout)) return e;
+  if (!scores || !k || !vis_idx) return fail(VP_ERR_NULL, "scores, k, vis_idx required");
+  TopkArgs t{};
+  t.seq_len = layout->seq_len;
+  t.seg_off = layout->vis_seg_off;
+  t.seg = layout->vis_seg;
+  t.B = shape->batch;
+  t.max_seq_len = shape->max_seq_len;
+  t.max_vis = shape->max_vis;
+  t.k_cap = shape->k_cap;
+  t.scores = scores;
+  t.k = k;
+  t.vis_idx = vis_idx;
+  if (hipError_t e = launch_topk(t, static_cast<hipStream_t>(stream))) return hip_fail(e, "top-k launch");
+  return VP_OK;
+}
+
+vp_status vp_sparse_decode_attn(const vp_shape* shape, const vp_layout* layout, const vp_params* params,
+                                const void* q, const void* K, const void* V, const int32_t* vis_idx,
+                                const int32_t* k, void* out, int32_t flags, void* workspace, size_t workspace_bytes,
+                                void* stream) {
+  g_last_error.clear();
+  if (vp_status e = check_shape(shape)) return e;
+  if (vp_status e = check_layout(layout)) return e;
+  if (vp_status e = check_params(params)) return e;
+  if (!q || !K || !V || !vis_idx || !k || !out) return fail(VP_ERR_NULL, "q, K, V, vis_idx, k, out required");
+  if (!aligned16(q) || !aligned16(K) || !aligned16(V)) return fail(VP_ERR_SHAPE, "q, K, V must be 16-byte aligned");
+  if (flags & ~VP_ATTN_TEXT_FROM_WORKSPACE) return fail(VP_ERR_RANGE, "unknown flags 0x%x", flags);
+  Plan plan;
+  if (vp_status e = check_ws(shape, workspace, workspace_bytes, plan)) return e;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  AttendArgs a = attend_args(shape, layout, params, plan, ws, q, K, V);
+  a.vis_idx = vis_idx;
+  a.kk = k;
+  if (!(flags & VP_ATTN_TEXT_FROM_WORKSPACE)) {
+    if (hipError_t e = launch_attend(a, MODE_TEXT, shape->dtype, shape->head_dim, st))
+      return hip_fail(e, "text pass launch");
+  }
+  if (hipError_t e = launch_attend(a, MODE_KEPT, shape->dtype, shape->head_dim, st))
+    return hip_fail(e, "kept pass launch");
+  MergeArgs m{};
+  m.seq_len = layout->seq_len;
+  m.kk = k;
+  m.B = shape->batch;
+  m.Hq = shape->n_q_heads;
+  m.max_seq_len = shape->max_seq_len;
+  m.k_cap = shape->k_cap;
+  m.chunk = plan.chunk;
+  m.nchunk = plan.nchunk;
+  m.split = plan.split;
+  m.nsplit = plan.nsplit;
+  m.dtype = shape->dtype;
+  m.stats = a.stats;
+  m.acc = a.acc;
+  m.kstats = a.kstats;
+  m.kacc = a.kacc;
+  m.out = out;
+  if (hipError_t e = launch_merge(m, shape->head_dim, st)) return hip_fail(e, "merge launch");
+  return VP_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,133 @@
+// Host/device interface between the C ABI (vp_api.hip) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "visionpulse.h"
+
+namespace vp {
+
+// Work decomposition and workspace carving, a pure function of the shape.
+struct Plan {
+  int chunk;    // cache positions per context-pass work-group (multiple of 32)
+  int nchunk;   // ceil(max_seq_len / chunk)
+  int split;    // kept rows per kept-pass work-group (multiple of 32)
+  int nsplit;   // ceil(k_cap / split)
+  size_t zs;      // float [B][Hq][max_vis]     visual logits (log2 domain)
+  size_t stats;   // float [B][Hq][nchunk][8]   per-chunk softmax statistics
+  size_t acc;     // float [B][Hq][nchunk][d]   per-chunk text value partials
+  size_t head;    // float [B][Hq][2]           merged (max, score normaliser)
+  size_t kstats;  // float [B][Hq][nsplit][2]   kept-row (max, sum)
+  size_t kacc;    // float [B][Hq][nsplit][d]   kept-row value partials
+  size_t total;
+};
+
+Plan make_plan(const vp_shape& s);
+
+enum Mode : int { MODE_SCORE = 1, MODE_TEXT = 2, MODE_SCORE_TEXT = 3, MODE_KEPT = 4 };
+
+struct AttendArgs {
+  const void* q;
+  const void* K;
+  const void* V;
+  int64_t sb, sh, ss;   // KV strides (elements)
+  const int32_t* seq_len;
+  const int32_t* seg_off;
+  const int32_t* seg;
+  int B, Hq, Hkv, G, max_seq_len, max_vis;
+  float zscale;         // sm_scale * log2(e)
+  float inv_tau_m;      // 1 / tau_mass
+  float inv_tau_s;      // 1 / tau_score
+  int chunk, nchunk;
+  float* zs;
+  float* stats;
+  float* acc;
+  const int32_t* vis_idx;
+  const int32_t* kk;
+  int k_cap, split, nsplit;
+  float* kstats;
+  float* kacc;
+};
+
+hipError_t launch_attend(const AttendArgs& a, int mode, int dtype, int head_dim, hipStream_t st);
+
+struct MassArgs {
+  const int32_t* seq_len;
+  const int32_t* seg_off;
+  const int32_t* seg;
+  int B, Hq, max_seq_len, max_vis, chunk, nchunk;
+  float inv_tau_m, inv_tau_s;
+  const float* stats;
+  const float* zs;
+  float* head;
+  float* mass_head;
+  float* mass_seq;
+  float* scores;
+};
+
+hipError_t launch_mass_finalize(const MassArgs& a, hipStream_t st);
+hipError_t launch_scores(const MassArgs& a, hipStream_t st);
+
+struct BudgetArgs {
+  const int32_t* seq_len;
+  const int32_t* seg_off;
+  const int32_t* seg;
+  int B, max_seq_len;
+  int r_lo_bp, r_hi_bp, clamp;
+  const float* mass_seq;
+  int32_t* k;
+};
+
+hipError_t launch_budget(const BudgetArgs& a, hipStream_t st);
+
+struct TopkArgs {
+  const int32_t* seq_len;
+  const int32_t* seg_off;
+  const int32_t* seg;
+  int B, max_seq_len, max_vis, k_cap;
+  const float* scores;
+  const int32_t* k;
+  int32_t* vis_idx;
+};
+
+hipError_t launch_topk(const TopkArgs& a, hipStream_t st);
+
+struct MergeArgs {
+  const int32_t* seq_len;
+  const int32_t* kk;
+  int B, Hq, max_seq_len, k_cap, chunk, nchunk, split, nsplit, dtype;
+  const float* stats;
+  const float* acc;
+  const float* kstats;
+  const float* kacc;
+  void* out;
+};
+
+hipError_t launch_merge(const MergeArgs& a, int head_dim, hipStream_t st);
+
+// kept-row budget helpers shared by host validation and the budget kernel
+__host__ __device__ inline int ceil_bp(long n, int bp) { return static_cast<int>((static_cast<long>(bp) * n + 9999) / 10000); }
+__host__ __device__ inline int floor_bp(long n, int bp) { return static_cast<int>((static_cast<long>(bp) * n) / 10000); }
+
+// Eq. (7) with the Sec. 5.2 clamp; m is the head-max visual mass
+__host__ __device__ inline int budget_rule(double m, int n_vis, int r_lo_bp, int r_hi_bp, int clamp) {
+  if (n_vis <= 0) return 0;
+  if (!(m >= 0.0)) m = 0.0;  // NaN or negative mass -> no visual mass
+  const double x = m * static_cast<double>(n_vis);
+  long k = x >= static_cast<double>(n_vis) ? n_vis : static_cast<long>(ceil(x));
+  if (clamp) {
+    const int lo = ceil_bp(n_vis, r_lo_bp);
+    int hi = floor_bp(n_vis, r_hi_bp);
+    if (hi < lo) hi = lo;
+    if (k < lo) k = lo;
+    if (k > hi) k = hi;
+  }
+  if (k > n_vis) k = n_vis;
+  if (k < 0) k = 0;
+  return static_cast<int>(k);
+}
+
+}  // namespace vp

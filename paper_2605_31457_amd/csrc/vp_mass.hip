@@ -1,0 +1,114 @@
+// Reductions after the context pass: Eq. (5)/(6) masses with the head mean and
+// head max (Sec. 4.3), Eq. (2) scores (Sec. 4.2), and the Eq. (7) budget with
+// the Sec. 5.2 clamp.
+#include "vp_common.h"
+#include "vp_internal.h"
+
+namespace vp {
+namespace {
+
+// One work-group per sequence. Merges the per-chunk statistics of every head
+// (max-shifted sums, combined in double), writes m^{vis}_{t,h}, the head mean
+// M_vis and head max M_vis,max, and the per-head (max, score normaliser) the
+// scores kernel needs.
+__global__ __launch_bounds__(256) void mass_finalize_kernel(const MassArgs a) {
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int L = clamp_len(a.seq_len[b], a.max_seq_len);
+  const int nv = (L + a.chunk - 1) / a.chunk;
+  double msum = 0.0;
+  double mmax = 0.0;
+  for (int h = tid; h < a.Hq; h += blockDim.x) {
+    const float* st = a.stats + (static_cast<size_t>(b) * a.Hq + h) * a.nchunk * 8;
+    float m = kNegInf;
+    for (int c = 0; c < nv; ++c) m = fmaxf(m, st[c * 8]);
+    double Ls = 0.0, Lm = 0.0, Vm = 0.0;
+    for (int c = 0; c < nv; ++c) {
+      const float mc = st[c * 8];
+      if (mc == kNegInf) continue;
+      const double fs = fast_exp2((mc - m) * a.inv_tau_s);
+      const double fm = fast_exp2((mc - m) * a.inv_tau_m);
+      Ls += fs * st[c * 8 + 1];
+      Lm += fm * st[c * 8 + 2];
+      Vm += fm * st[c * 8 + 3];
+    }
+    const double mass = Lm > 0.0 ? Vm / Lm : 0.0;
+    a.mass_head[static_cast<size_t>(b) * a.Hq + h] = static_cast<float>(mass);
+    a.head[(static_cast<size_t>(b) * a.Hq + h) * 2 + 0] = m;
+    a.head[(static_cast<size_t>(b) * a.Hq + h) * 2 + 1] = static_cast<float>(Ls);
+    msum += mass;
+    mmax = mass > mmax ? mass : mmax;
+  }
+  __shared__ double s_sum[256];
+  __shared__ double s_max[256];
+  s_sum[tid] = msum;
+  s_max[tid] = mmax;
+  __syncthreads();
+  for (int off = blockDim.x / 2; off > 0; off >>= 1) {
+    if (tid < off) {
+      s_sum[tid] += s_sum[tid + off];
+      s_max[tid] = s_max[tid] > s_max[tid + off] ? s_max[tid] : s_max[tid + off];
+    }
+    __syncthreads();
+  }
+  if (tid == 0) {
+    a.mass_seq[2 * b + 0] = static_cast<float>(s_sum[0] / a.Hq);
+    a.mass_seq[2 * b + 1] = static_cast<float>(s_max[0]);
+  }
+}
+
+// S_i = (1/Hq) sum_h 2^((z_{h,i} - m_h) / tau_score) / Ls_h for every visual rank i.
+// grid = (ceil(max_vis / 256), B); consecutive threads read consecutive ranks.
+__global__ __launch_bounds__(256) void scores_kernel(const MassArgs a) {
+  extern __shared__ float sh[];  // [Hq] max, [Hq] 1/Ls
+  float* s_m = sh;
+  float* s_inv = sh + a.Hq;
+  __shared__ int s_nv;
+  const int b = blockIdx.y;
+  const int tid = threadIdx.x;
+  if (tid == 0) {
+    const int L = clamp_len(a.seq_len[b], a.max_seq_len);
+    const int nv = count_visual(a.seg_off, a.seg, b, L);
+    s_nv = nv < a.max_vis ? nv : a.max_vis;
+  }
+  for (int h = tid; h < a.Hq; h += blockDim.x) {
+    const float* hs = a.head + (static_cast<size_t>(b) * a.Hq + h) * 2;
+    s_m[h] = hs[0];
+    s_inv[h] = hs[1] > 0.f ? 1.0f / hs[1] : 0.f;
+  }
+  __syncthreads();
+  const int i = blockIdx.x * blockDim.x + tid;
+  if (i >= s_nv) return;
+  const float* z = a.zs + static_cast<size_t>(b) * a.Hq * a.max_vis + i;
+  float s = 0.f;
+  for (int h = 0; h < a.Hq; ++h) s += fast_exp2((z[static_cast<size_t>(h) * a.max_vis] - s_m[h]) * a.inv_tau_s) * s_inv[h];
+  a.scores[static_cast<size_t>(b) * a.max_vis + i] = s / static_cast<float>(a.Hq);
+}
+
+__global__ __launch_bounds__(64) void budget_kernel(const BudgetArgs a) {
+  const int b = blockIdx.x * blockDim.x + threadIdx.x;
+  if (b >= a.B) return;
+  const int L = clamp_len(a.seq_len[b], a.max_seq_len);
+  const int nv = count_visual(a.seg_off, a.seg, b, L);
+  a.k[b] = budget_rule(static_cast<double>(a.mass_seq[2 * b + 1]), nv, a.r_lo_bp, a.r_hi_bp, a.clamp);
+}
+
+}  // namespace
+
+hipError_t launch_mass_finalize(const MassArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(mass_finalize_kernel, dim3(a.B), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_scores(const MassArgs& a, hipStream_t st) {
+  const dim3 grid((a.max_vis + 255) / 256, a.B);
+  hipLaunchKernelGGL(scores_kernel, grid, dim3(256), 2 * a.Hq * sizeof(float), st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_budget(const BudgetArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL(budget_kernel, dim3((a.B + 63) / 64), dim3(64), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace vp

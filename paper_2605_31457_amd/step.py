@@ -1,0 +1,95 @@
+"""Device buffers for one decode step and the four C-ABI calls in order.
+
+Marshalling only: uploads a ``workloads.Workload`` to the GPU (torch
+allocations), fills the ABI structs and calls vp_visual_mass -> vp_budget ->
+vp_select_topk -> vp_sparse_decode_attn through ``vp``. All arithmetic runs in
+libvisionpulse.so.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+from . import vp
+from .workloads import Workload, layout_arrays
+
+
+def _dev(a: np.ndarray, device) -> torch.Tensor:
+    if a.dtype == np.uint16:
+        return torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(device)
+    return torch.from_numpy(np.ascontiguousarray(a)).to(device)
+
+
+def make_params(w: Workload, sm_scale: float = 0.0) -> vp.vp_params:
+    return vp.vp_params(tau_mass=w.tau_mass, tau_score=w.tau_score, sm_scale=sm_scale,
+                        r_lo_bp=w.r_lo_bp, r_hi_bp=w.r_hi_bp, clamp=int(w.clamp))
+
+
+class DeviceStep:
+    """Device-resident inputs, outputs and workspace of one step of workload ``w``."""
+
+    def __init__(self, w: Workload, device="cuda:0", k_cap: int | None = None, max_vis: int | None = None,
+                 kv=None):
+        self.w = w
+        self.device = torch.device(device)
+        self.q = _dev(w.q, self.device)
+        if kv is None:
+            self.K = _dev(w.K, self.device)
+            self.V = _dev(w.V, self.device)
+        else:
+            self.K, self.V = kv
+        off, seg = layout_arrays(w.segments)
+        self.seq_len = torch.from_numpy(w.seq_len.astype(np.int32)).to(self.device)
+        self.seg_off = torch.from_numpy(off).to(self.device)
+        self.seg = torch.from_numpy(seg.reshape(-1) if seg.size else np.zeros(2, np.int32)).to(self.device)
+        B, Hq, d = w.B, w.Hq, w.d
+        self.max_vis = max_vis or w.max_vis
+        self.k_cap = k_cap or w.k_cap
+        st = self.K.stride()
+        self.shape = vp.vp_shape(batch=B, n_q_heads=Hq, n_kv_heads=w.Hkv, head_dim=d,
+                                 dtype=vp.VP_BF16 if w.dtype == "bf16" else vp.VP_F32,
+                                 max_seq_len=w.S_cap, max_vis=self.max_vis, max_segs=w.max_segs,
+                                 k_cap=self.k_cap, reserved=0, kv_stride_b=st[0], kv_stride_h=st[1],
+                                 kv_stride_s=st[2])
+        self.layout = vp.vp_layout(seq_len=self.seq_len.data_ptr(), vis_seg_off=self.seg_off.data_ptr(),
+                                   vis_seg=self.seg.data_ptr())
+        self.params = make_params(w)
+        f32 = dict(dtype=torch.float32, device=self.device)
+        i32 = dict(dtype=torch.int32, device=self.device)
+        self.mass_head = torch.zeros(B, Hq, **f32)
+        self.mass_seq = torch.zeros(B, 2, **f32)
+        self.scores = torch.zeros(B, self.max_vis, **f32)
+        self.k = torch.zeros(B, **i32)
+        self.vis_idx = torch.full((B, self.k_cap), -7, **i32)
+        self.out = torch.zeros(B, Hq, d, dtype=self.q.dtype, device=self.device)
+        self.ws_bytes = vp.vp_workspace_size(self.shape)
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
+
+    # the four calls ------------------------------------------------------
+    def visual_mass(self, fused=True, stream=None):
+        vp.vp_visual_mass(self.shape, self.layout, self.params, self.q, self.K, self.V if fused else None,
+                          self.mass_head, self.mass_seq, self.scores, self.ws, self.ws_bytes, stream)
+
+    def budget(self, stream=None):
+        vp.vp_budget(self.shape, self.layout, self.params, self.mass_seq, self.k, stream)
+
+    def select_topk(self, stream=None):
+        vp.vp_select_topk(self.shape, self.layout, self.scores, self.k, self.vis_idx, stream)
+
+    def sparse_decode_attn(self, fused=True, stream=None):
+        vp.vp_sparse_decode_attn(self.shape, self.layout, self.params, self.q, self.K, self.V, self.vis_idx,
+                                 self.k, self.out, vp.VP_ATTN_TEXT_FROM_WORKSPACE if fused else 0,
+                                 self.ws, self.ws_bytes, stream)
+
+    def run(self, fused=True, stream=None):
+        self.visual_mass(fused, stream)
+        self.budget(stream)
+        self.select_topk(stream)
+        self.sparse_decode_attn(fused, stream)
+
+    def results(self) -> dict:
+        torch.cuda.synchronize(self.device)
+        out = self.out.float().cpu().numpy()
+        return dict(mass_head=self.mass_head.cpu().numpy(), mass_seq=self.mass_seq.cpu().numpy(),
+                    scores=self.scores.cpu().numpy(), k=self.k.cpu().numpy(),
+                    vis_idx=self.vis_idx.cpu().numpy(), out=out)

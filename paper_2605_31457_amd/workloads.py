@@ -17,6 +17,7 @@ even from float32); the fp32 configuration stores ``float32``. KV caches are
 """
 from __future__ import annotations
 
+import os
 from dataclasses import dataclass, field
 
 import numpy as np
@@ -30,7 +31,11 @@ __all__ = ["Workload", "CONFIGS", "generate", "bf16_round", "bf16_to_f32",
 # --------------------------------------------------------------------------
 def bf16_round(x: np.ndarray) -> np.ndarray:
     """float32 -> bfloat16 bit patterns (uint16), round to nearest, ties to even."""
-    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    x = np.ascontiguousarray(x, dtype=np.float32)
+    if x.size >= (1 << 16):
+        import torch  # vectorised, multi-threaded RNE conversion for large tensors
+        return torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    u = x.view(np.uint32)
     r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
     return r.astype(np.uint16)
 
@@ -200,8 +205,10 @@ def generate(cfg: int, B: int | None = None, seqs=None, seed: int | None = None,
     V = np.zeros((Bn, Hkv, S_cap, d), dtype=st)
     kv_scale = 1.0 if cfg == 1 else 0.5
     frac = _spike_fraction(cfg)
-    offsets = []
-    for i, b in enumerate(idx):
+    offsets = [0.0] * Bn
+
+    def one(i):
+        b = idx[i]
         L = lens_all[b]
         segs = segs_all[b]
         qb = _normal(_rng(cfg, "q", b, seed), (Hq, d))
@@ -217,7 +224,7 @@ def generate(cfg: int, B: int | None = None, seqs=None, seed: int | None = None,
             ro = _rng(cfg, "offset", b, seed)
             s_b = float(ro.uniform(*CFG3_OFFSET_RANGE))
             Kb[:, vis, :] += np.float32(s_b) * dirs[:, None, :]
-            offsets.append(s_b)
+            offsets[i] = s_b
         if f32:
             q[i] = qb
             K[i, :, :L] = Kb
@@ -226,6 +233,13 @@ def generate(cfg: int, B: int | None = None, seqs=None, seed: int | None = None,
             q[i] = bf16_round(qb)
             K[i, :, :L] = bf16_round(Kb)
             V[i, :, :L] = bf16_round(Vb)
+
+    if Bn > 1:
+        from concurrent.futures import ThreadPoolExecutor
+        with ThreadPoolExecutor(max_workers=min(Bn, 8, os.cpu_count() or 1)) as ex:
+            list(ex.map(one, range(Bn)))
+    else:
+        one(0)
     w = Workload(name=c["name"], dtype=c["dtype"], B=Bn, Hq=Hq, Hkv=Hkv, d=d, S_cap=S_cap,
                  seq_len=np.array([lens_all[b] for b in idx], dtype=np.int32),
                  segments=[list(segs_all[b]) for b in idx], q=q, K=K, V=V,

@@ -1,0 +1,135 @@
+"""C ABI checks that need no GPU: the library loads, exports every declared
+entry point, and rejects bad arguments before launching anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2605_31457_amd import vp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "visionpulse.h")
+GOLDEN = os.path.join(ROOT, "tests", "golden")
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(vp.LIB_PATH):
+        from paper_2605_31457_amd import build
+        build.build()
+    return vp.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?[a-z_0-9]+\s*\*?\s*(vp_[a-z_0-9]+)\s*\(", text, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported(L):
+    names = declared_functions()
+    assert {"vp_visual_mass", "vp_budget", "vp_select_topk", "vp_sparse_decode_attn",
+            "vp_workspace_size", "vp_status_string", "vp_last_error", "vp_budget_host"} <= set(names)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def _shape(**kw):
+    s = dict(batch=2, n_q_heads=28, n_kv_heads=4, head_dim=128, dtype=vp.VP_BF16, max_seq_len=4096,
+             max_vis=1296, max_segs=1, k_cap=64, reserved=0, kv_stride_b=4 * 4096 * 128,
+             kv_stride_h=4096 * 128, kv_stride_s=128)
+    s.update(kw)
+    return vp.vp_shape(**s)
+
+
+def _params(**kw):
+    p = dict(tau_mass=0.1, tau_score=1.0, sm_scale=0.0, r_lo_bp=100, r_hi_bp=500, clamp=1)
+    p.update(kw)
+    return vp.vp_params(**p)
+
+
+def test_struct_layout_matches_header(L):
+    assert ctypes.sizeof(vp.vp_shape) == 64 and vp.vp_shape.kv_stride_b.offset == 40
+    assert ctypes.sizeof(vp.vp_params) == 24 and ctypes.sizeof(vp.vp_layout) == 24
+
+
+def test_workspace_size_is_pure_and_scales(L):
+    a = vp.vp_workspace_size(_shape())
+    b = vp.vp_workspace_size(_shape(batch=4))
+    assert a > 0 and b > a and a % 256 == 0
+    # visual logits (B*Hq*max_vis fp32) are the dominant piece
+    assert a >= 2 * 28 * 1296 * 4
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(dtype=7), "VP_ERR_DTYPE"),
+    (dict(n_q_heads=30), "VP_ERR_SHAPE"),
+    (dict(n_q_heads=68, n_kv_heads=4), "VP_ERR_UNSUPPORTED"),
+    (dict(head_dim=96), "VP_ERR_UNSUPPORTED"),
+    (dict(batch=0), "VP_ERR_SHAPE"),
+    (dict(max_vis=0), "VP_ERR_SHAPE"),
+    (dict(k_cap=0), "VP_ERR_SHAPE"),
+    (dict(kv_stride_s=64), "VP_ERR_SHAPE"),
+    (dict(kv_stride_s=130), "VP_ERR_SHAPE"),
+    (dict(reserved=1), "VP_ERR_SHAPE"),
+    (dict(max_segs=1000), "VP_ERR_UNSUPPORTED"),
+])
+def test_shape_validation(L, kw, status):
+    with pytest.raises(vp.VPError) as e:
+        vp.vp_workspace_size(_shape(**kw))
+    assert status in str(e.value)
+
+
+def _layout():
+    return vp.vp_layout(seq_len=0x1000, vis_seg_off=0x2000, vis_seg=0x3000)
+
+
+def test_calls_reject_nulls_and_bad_params_before_launch(L):
+    s, lay, p = _shape(), _layout(), _params()
+    ws_bytes = vp.vp_workspace_size(s)
+    fake = 0x10000  # never dereferenced: every case below fails validation first
+    with pytest.raises(vp.VPError, match="VP_ERR_NULL"):
+        vp.vp_visual_mass(s, lay, p, None, fake, None, fake, fake, fake, fake, ws_bytes, 0)
+    with pytest.raises(vp.VPError, match="VP_ERR_WORKSPACE"):
+        vp.vp_visual_mass(s, lay, p, fake, fake, None, fake, fake, fake, fake, ws_bytes - 1, 0)
+    with pytest.raises(vp.VPError, match="VP_ERR_WORKSPACE"):
+        vp.vp_visual_mass(s, lay, p, fake, fake, None, fake, fake, fake, fake + 16, ws_bytes, 0)
+    with pytest.raises(vp.VPError, match="VP_ERR_RANGE"):
+        vp.vp_visual_mass(s, lay, _params(tau_mass=0.0), fake, fake, None, fake, fake, fake, fake, ws_bytes, 0)
+    with pytest.raises(vp.VPError, match="VP_ERR_RANGE"):
+        vp.vp_budget(s, lay, _params(r_hi_bp=20000), fake, fake, 0)
+    with pytest.raises(vp.VPError, match="VP_ERR_SHAPE"):
+        vp.vp_budget(_shape(k_cap=10), lay, p, fake, fake, 0)  # 5% of 1296 needs 64 rows
+    with pytest.raises(vp.VPError, match="VP_ERR_NULL"):
+        vp.vp_select_topk(s, lay, fake, None, fake, 0)
+    with pytest.raises(vp.VPError, match="VP_ERR_NULL"):
+        vp.vp_select_topk(s, vp.vp_layout(seq_len=0x1000, vis_seg_off=None, vis_seg=0x3000), fake, fake, fake, 0)
+    with pytest.raises(vp.VPError, match="VP_ERR_RANGE"):
+        vp.vp_sparse_decode_attn(s, lay, p, fake, fake, fake, fake, fake, fake, 8, fake, ws_bytes, 0)
+    with pytest.raises(vp.VPError, match="VP_ERR_SHAPE"):
+        vp.vp_sparse_decode_attn(s, lay, p, fake + 2, fake, fake, fake, fake, fake, 0, fake, ws_bytes, 0)
+    assert "workspace" in L.vp_last_error().decode() or L.vp_last_error().decode() != ""
+
+
+def test_status_strings(L):
+    assert vp.vp_status_string(0) == "VP_OK" and vp.vp_status_string(7) == "VP_ERR_HIP"
+
+
+def _budget_rows():
+    rows = []
+    for line in open(os.path.join(GOLDEN, "budget_cases.txt")):
+        line = line.split("#")[0].strip()
+        if line:
+            m, n, lo, hi, c, k = line.split()
+            rows.append((float(m), int(n), int(lo), int(hi), int(c), int(k)))
+    return rows
+
+
+@pytest.mark.parametrize("m,n,lo,hi,c,k", _budget_rows())
+def test_budget_host_mirror_matches_table(L, m, n, lo, hi, c, k):
+    assert vp.vp_budget_host(m, n, _params(r_lo_bp=lo, r_hi_bp=hi, clamp=c)) == k
+
+
+def test_budget_host_rejects_bad_params(L):
+    assert vp.vp_budget_host(0.5, 100, _params(tau_mass=-1.0)) == -1

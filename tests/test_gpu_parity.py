@@ -1,0 +1,181 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 reference.
+
+Bars: masses and scores within 1e-5 relative; budgets exact; kept index sets
+bit-exact (inputs are planted so that the Eq. (3) cut has a >= 1e-3 relative
+score gap and the Eq. (7) rounding has a 1e-4 relative margin); outputs within
+bf16 atol 2e-2 / rtol 1e-2 (fp32: 1e-5 / 1e-5).
+"""
+import numpy as np
+import pytest
+import torch
+
+from _parity import check_sequence, small_workload, tile_batch
+from oracle import plant as P
+from oracle import vp_oracle as O
+from paper_2605_31457_amd import step as S
+from paper_2605_31457_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+
+def _log(msg):
+    print(msg, flush=True)
+
+
+def _run(w, fused=True, **kw):
+    ds = S.DeviceStep(w, **kw)
+    ds.run(fused=fused)
+    return ds, ds.results()
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_config_full(cfg):
+    w = W.generate(cfg)
+    ref, log = P.plant(w, P.params_of(w))
+    _log(f"cfg{cfg}: B={w.B} planted {sum(l['n_edits'] for l in log)} rows; k={[ref[b].k for b in range(w.B)]}")
+    for fused in (True, False):
+        _log(f"cfg{cfg}: GPU step fused={fused}")
+        _, g = _run(w, fused=fused)
+        for b in range(w.B):
+            check_sequence(f"cfg{cfg} fused={fused}", w, g, b, ref[b])
+
+
+def test_config4_full_batch():
+    """The 64 x 32k multi-image batch at full size, in the benchmark's launch
+    configuration. Four generated sequences are planted and checked by the
+    reference; the batch repeats them, so every one of the 64 outputs is checked."""
+    base = W.generate(4, seqs=[0, 1, 2, 3])
+    ref, log = P.plant(base, P.params_of(base))
+    w = tile_batch(base, 64)
+    _log(f"cfg4: B=64 x 32768, planted {[l['n_edits'] for l in log]}")
+    _, g = _run(w)
+    for b in range(64):
+        check_sequence("cfg4", w, g, b, ref[b % 4], b_src=b % 4)
+
+
+SMALL = {
+    "g4-d64-tails": dict(seed=1, B=3, Hq=8, Hkv=2, d=64, lens=[77, 200, 33],
+                         segs=[[(5, 40)], [(0, 64), (100, 50)], [(1, 31)]]),
+    "mha-d128": dict(seed=2, B=2, Hq=4, Hkv=4, d=128, lens=[129, 96], segs=[[(10, 100)], [(32, 32), (64, 16)]]),
+    "g16-all-visual": dict(seed=3, B=2, Hq=16, Hkv=1, d=128, lens=[300, 257], segs=[[(20, 200)], [(0, 257)]]),
+    "g7-many-segments": dict(seed=4, B=2, Hq=28, Hkv=4, d=128, lens=[500, 450],
+                             segs=[[(3, 50), (60, 40), (101, 7), (200, 100), (320, 90)],
+                                   [(10, 10), (20, 10), (30, 300)]]),
+    "f32-d128": dict(seed=5, dtype="f32", B=2, Hq=6, Hkv=2, d=128, lens=[100, 70], segs=[[(0, 60)], [(30, 40)]]),
+    "f32-d64-g4": dict(seed=9, dtype="f32", B=2, Hq=4, Hkv=1, d=64, lens=[200, 45], segs=[[(16, 150)], [(0, 40)]]),
+    "no-visual": dict(seed=6, B=2, Hq=8, Hkv=2, d=64, lens=[90, 40], segs=[[], [(0, 20)]]),
+    "unclamped-tau1": dict(seed=7, B=2, Hq=8, Hkv=2, d=128, lens=[150, 150], segs=[[(10, 100)], [(10, 100)]],
+                           tau_mass=1.0, clamp=False),
+    "short-seqs": dict(seed=8, B=3, Hq=4, Hkv=1, d=64, lens=[1, 5, 31], segs=[[], [(1, 3)], [(0, 31)]]),
+    "capacity-gt-len": dict(seed=10, B=2, Hq=8, Hkv=1, d=128, lens=[70, 130], segs=[[(2, 60)], [(64, 64)]],
+                            S_cap=200),
+}
+
+
+@pytest.mark.parametrize("name", sorted(SMALL))
+def test_small_shapes(name):
+    w = small_workload(**SMALL[name])
+    ref, _ = P.plant(w, P.params_of(w))
+    _log(f"small {name}: k={[ref[b].k for b in range(w.B)]} lens={list(w.seq_len)}")
+    for fused in (True, False):
+        _, g = _run(w, fused=fused)
+        for b in range(w.B):
+            check_sequence(f"{name} fused={fused}", w, g, b, ref[b])
+
+
+def test_fused_and_unfused_text_paths_agree_bitwise():
+    w = W.generate(2)
+    _, a = _run(w, fused=True)
+    _, b = _run(w, fused=False)
+    for key in ("mass_head", "mass_seq", "scores", "k", "vis_idx", "out"):
+        assert np.array_equal(a[key], b[key]), key
+
+
+def test_repeat_runs_are_bitwise_identical():
+    w = W.generate(3, B=4)
+    ds = S.DeviceStep(w)
+    ds.run()
+    first = ds.results()
+    for _ in range(3):
+        ds.run()
+        again = ds.results()
+        for key in first:
+            assert np.array_equal(first[key], again[key]), key
+
+
+def test_budget_kernel_matches_rule_exactly():
+    """vp_budget on given fp32 masses, including products that land exactly on
+    an integer, against Eq. (7) + clamp on the same fp32 values widened."""
+    n_vis = [256, 1296, 4096, 6400, 16384, 1, 0, 100]
+    lens = [max(n, 1) + 10 for n in n_vis]
+    segs = [[(5, n)] if n else [] for n in n_vis]
+    w = small_workload(seed=11, B=len(n_vis), Hq=4, Hkv=1, d=64, lens=lens, segs=segs, spike=0)
+    rng = np.random.default_rng(12)
+    for clamp in (True, False):
+        w.clamp = clamp
+        ds = S.DeviceStep(w, k_cap=max(n_vis))
+        for trial in range(20):
+            if trial == 0:
+                m = np.array([0.5, 0.25, 0.0, 1.0, 0.0625, 0.3, 0.7, 0.125], np.float32)  # exact products
+            elif trial == 1:
+                m = np.array([0.01, 0.05, 0.02, 0.03, 0.05, 0.01, 1.0, 0.5], np.float32)  # clamp edges
+            else:
+                m = rng.random(len(n_vis)).astype(np.float32) ** 3
+            ms = np.stack([m, m], axis=1)
+            ds.mass_seq.copy_(torch.from_numpy(ms))
+            ds.budget()
+            got = ds.k.cpu().numpy()
+            want = [O.budget(float(m[b]), n_vis[b], w.r_lo_bp, w.r_hi_bp, clamp) for b in range(len(n_vis))]
+            assert list(got) == want, (clamp, m, got, want)
+
+
+def test_topk_kernel_matches_sort_with_ties():
+    """vp_select_topk on given fp32 scores (many exact ties) against the
+    reference selection on the same values: ties go to the lower position."""
+    rng = np.random.default_rng(13)
+    n_vis = [16384, 4096, 1296, 37, 1, 300]
+    segs = [[(16 + 8188 * i, 4096) for i in range(4)], [(0, 4096)], [(14, 1296)], [(3, 10), (20, 27)],
+            [(0, 1)], [(0, 100), (150, 100), (300, 100)]]
+    lens = [32768, 5000, 3358, 50, 1, 400]
+    w = small_workload(seed=14, B=6, Hq=4, Hkv=1, d=64, lens=lens, segs=segs, spike=0)
+    ds = S.DeviceStep(w, k_cap=1000, max_vis=16384)
+    for trial in range(6):
+        sc = np.zeros((6, 16384), np.float32)
+        for b, n in enumerate(n_vis):
+            if trial % 3 == 0:
+                sc[b, :n] = rng.random(n).astype(np.float32)
+            elif trial % 3 == 1:
+                sc[b, :n] = (np.floor(rng.random(n) * 16) / 16).astype(np.float32)  # heavy ties
+            else:
+                sc[b, :n] = np.float32(1.0 / 7.0)                                   # all equal
+        ks = [rng.integers(0, min(n, 1000) + 1) for n in n_vis]
+        ks[0] = 819 if trial < 3 else 1000
+        ds.scores.copy_(torch.from_numpy(sc))
+        ds.k.copy_(torch.tensor(ks, dtype=torch.int32))
+        ds.select_topk()
+        got = ds.vis_idx.cpu().numpy()
+        for b, n in enumerate(n_vis):
+            vis = O.visual_positions(lens[b], segs[b])
+            k = min(ks[b], n, 1000)
+            want = O.select_top_k(sc[b, :n].astype(np.float64), vis, k)
+            assert np.array_equal(got[b, :k], want), (trial, b)
+            assert np.all(got[b, k:] == -1)
+
+
+def test_sparse_attention_on_given_selection():
+    """vp_sparse_decode_attn alone, on the reference's own selection, against
+    the reference pruned attention (also with k = N_v: dense attention)."""
+    w = W.generate(2)
+    p = P.params_of(w)
+    r = O.decode_step_sequence(w.q[0], w.K[0], w.V[0], int(w.seq_len[0]), w.segments[0], p)
+    ds = S.DeviceStep(w, k_cap=1296)
+    for k_use, sel in ((r.k, r.vis_idx), (1296, O.visual_positions(3358, w.segments[0]))):
+        idx = np.full((1, 1296), -1, np.int32)
+        idx[0, :k_use] = sel
+        ds.vis_idx.copy_(torch.from_numpy(idx))
+        ds.k.copy_(torch.tensor([k_use], dtype=torch.int32))
+        ds.sparse_decode_attn(fused=False)
+        got = ds.out.float().cpu().numpy()[0]
+        rr = O.decode_step_sequence(w.q[0], w.K[0], w.V[0], 3358, w.segments[0], p, k_override=k_use)
+        assert np.array_equal(rr.vis_idx, sel)
+        np.testing.assert_allclose(got, rr.out, atol=2e-2, rtol=1e-2)
