@@ -147,7 +147,9 @@ Plan make_plan(const vp_shape& s) {
   if (chunk > 2048) chunk = 2048;
   p.chunk = static_cast<int>(chunk);
   p.nchunk = static_cast<int>((s.max_seq_len + chunk - 1) / chunk);
-  p.split = 64;
+  // Kept pass: 64 rows (two tiles) per work-group, or 32 when that leaves
+  // fewer than 1024 work-groups.
+  p.split = static_cast<int64_t>(s.batch) * s.n_kv_heads * ((s.k_cap + 63) / 64) >= 1024 ? 64 : 32;
   p.nsplit = (s.k_cap + p.split - 1) / p.split;
   const size_t B = s.batch, Hq = s.n_q_heads, d = s.head_dim;
   size_t off = 0;

@@ -7,53 +7,67 @@
 namespace vp {
 namespace {
 
-// One work-group per sequence. Merges the per-chunk statistics of every head
-// (max-shifted sums, combined in double), writes m^{vis}_{t,h}, the head mean
-// M_vis and head max M_vis,max, and the per-head (max, score normaliser) the
-// scores kernel needs.
+// One work-group per sequence, one wave per head (lanes over chunks): merges
+// the per-chunk statistics of every head (max-shifted sums, combined in double
+// with fixed-order wave reductions), writes m^{vis}_{t,h}, the head mean M_vis
+// and head max M_vis,max, and the per-head (max, score normaliser) the scores
+// kernel needs.
 __global__ __launch_bounds__(256) void mass_finalize_kernel(const MassArgs a) {
+  constexpr int kWaves = 4;
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wid = tid >> 6;
   const int L = clamp_len(a.seq_len[b], a.max_seq_len);
   const int nv = (L + a.chunk - 1) / a.chunk;
   double msum = 0.0;
   double mmax = 0.0;
-  for (int h = tid; h < a.Hq; h += blockDim.x) {
-    const float* st = a.stats + (static_cast<size_t>(b) * a.Hq + h) * a.nchunk * 8;
+  for (int h = wid; h < a.Hq; h += kWaves) {
+    const float4* st = reinterpret_cast<const float4*>(a.stats + (static_cast<size_t>(b) * a.Hq + h) * a.nchunk * 8);
     float m = kNegInf;
-    for (int c = 0; c < nv; ++c) m = fmaxf(m, st[c * 8]);
+    for (int c = lane; c < nv; c += 64) m = fmaxf(m, st[2 * c].x);
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
     double Ls = 0.0, Lm = 0.0, Vm = 0.0;
-    for (int c = 0; c < nv; ++c) {
-      const float mc = st[c * 8];
-      if (mc == kNegInf) continue;
-      const double fs = fast_exp2((mc - m) * a.inv_tau_s);
-      const double fm = fast_exp2((mc - m) * a.inv_tau_m);
-      Ls += fs * st[c * 8 + 1];
-      Lm += fm * st[c * 8 + 2];
-      Vm += fm * st[c * 8 + 3];
+    for (int c = lane; c < nv; c += 64) {
+      const float4 s = st[2 * c];
+      if (s.x == kNegInf) continue;
+      const double fs = fast_exp2((s.x - m) * a.inv_tau_s);
+      const double fm = fast_exp2((s.x - m) * a.inv_tau_m);
+      Ls += fs * s.y;
+      Lm += fm * s.z;
+      Vm += fm * s.w;
+    }
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+      Ls += __shfl_xor(Ls, off);
+      Lm += __shfl_xor(Lm, off);
+      Vm += __shfl_xor(Vm, off);
     }
     const double mass = Lm > 0.0 ? Vm / Lm : 0.0;
-    a.mass_head[static_cast<size_t>(b) * a.Hq + h] = static_cast<float>(mass);
-    a.head[(static_cast<size_t>(b) * a.Hq + h) * 2 + 0] = m;
-    a.head[(static_cast<size_t>(b) * a.Hq + h) * 2 + 1] = static_cast<float>(Ls);
+    if (lane == 0) {
+      a.mass_head[static_cast<size_t>(b) * a.Hq + h] = static_cast<float>(mass);
+      *reinterpret_cast<float2*>(a.head + (static_cast<size_t>(b) * a.Hq + h) * 2) =
+          make_float2(m, static_cast<float>(Ls));
+    }
     msum += mass;
     mmax = mass > mmax ? mass : mmax;
   }
-  __shared__ double s_sum[256];
-  __shared__ double s_max[256];
-  s_sum[tid] = msum;
-  s_max[tid] = mmax;
-  __syncthreads();
-  for (int off = blockDim.x / 2; off > 0; off >>= 1) {
-    if (tid < off) {
-      s_sum[tid] += s_sum[tid + off];
-      s_max[tid] = s_max[tid] > s_max[tid + off] ? s_max[tid] : s_max[tid + off];
-    }
-    __syncthreads();
+  __shared__ double s_sum[kWaves];
+  __shared__ double s_max[kWaves];
+  if (lane == 0) {
+    s_sum[wid] = msum;
+    s_max[wid] = mmax;
   }
+  __syncthreads();
   if (tid == 0) {
-    a.mass_seq[2 * b + 0] = static_cast<float>(s_sum[0] / a.Hq);
-    a.mass_seq[2 * b + 1] = static_cast<float>(s_max[0]);
+    double t = 0.0, mx = 0.0;
+    for (int v = 0; v < kWaves; ++v) {
+      t += s_sum[v];
+      mx = s_max[v] > mx ? s_max[v] : mx;
+    }
+    a.mass_seq[2 * b + 0] = static_cast<float>(t / a.Hq);
+    a.mass_seq[2 * b + 1] = static_cast<float>(mx);
   }
 }
 

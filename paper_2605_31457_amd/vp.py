@@ -12,7 +12,8 @@ import ctypes
 import os
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(PKG, "libvisionpulse.so")
+# VP_LIB selects another build of the same library (e.g. a tuning variant)
+LIB_PATH = os.environ.get("VP_LIB") or os.path.join(PKG, "libvisionpulse.so")
 
 VP_F32, VP_BF16 = 0, 1
 VP_ATTN_TEXT_FROM_WORKSPACE = 1
