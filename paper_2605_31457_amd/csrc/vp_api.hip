@@ -1,5 +1,6 @@
 // C ABI of the VisionPulse decode-step path: argument validation, workspace
 // carving and kernel launches on the caller's stream (no allocation, no sync).
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -121,8 +122,13 @@ AttendArgs attend_args(const vp_shape* s, const vp_layout* l, const vp_params* p
   a.zscale = zscale_of(s, p);
   a.inv_tau_m = 1.0f / p->tau_mass;
   a.inv_tau_s = 1.0f / p->tau_score;
-  a.chunk = plan.chunk;
-  a.nchunk = plan.nchunk;
+  // lazy running maxima: a reference is raised only when a logit exceeds it by
+  // more than a margin that keeps every tempered weight below 2^64
+  a.thr_s = 64.0f / std::max(1.0f, std::max(a.inv_tau_m, a.inv_tau_s));
+  a.thr_t = a.thr_s;
+  a.tau_s_one = p->tau_score == 1.0f;
+  a.nparts = plan.nparts;
+  a.zs_stride = plan.zs_stride;
   a.zs = reinterpret_cast<float*>(ws + plan.zs);
   a.stats = reinterpret_cast<float*>(ws + plan.stats);
   a.acc = reinterpret_cast<float*>(ws + plan.acc);
@@ -136,29 +142,36 @@ AttendArgs attend_args(const vp_shape* s, const vp_layout* l, const vp_params* p
 
 }  // namespace
 
+#ifndef VP_TARGET_PARTS
+#define VP_TARGET_PARTS 4096
+#endif
+
 Plan make_plan(const vp_shape& s) {
   Plan p{};
-  // Context pass: about 4096 one-wave work-groups (16 resident per CU on 256
-  // CUs), chunks of 64 .. 2048 positions in whole 32-row tiles.
-  const int64_t rows = static_cast<int64_t>(s.batch) * s.n_kv_heads * s.max_seq_len;
-  int64_t chunk = (rows + 4095) / 4096;
-  chunk = ((chunk + 31) / 32) * 32;
-  if (chunk < 64) chunk = 64;
-  if (chunk > 2048) chunk = 2048;
-  p.chunk = static_cast<int>(chunk);
-  p.nchunk = static_cast<int>((s.max_seq_len + chunk - 1) / chunk);
+  // Context pass: about VP_TARGET_PARTS one-wave work-groups in all, each
+  // with at least two 32-row tiles. Tiles are dealt out cyclically, so every
+  // part sees the sequence's own mix of visual and text rows: consecutive
+  // work-groups land on different XCDs, and contiguous chunks would hand whole
+  // XCDs only visual (K) or only text (K + V) rows.
+  const int64_t pairs = static_cast<int64_t>(s.batch) * s.n_kv_heads;
+  const int64_t tiles = (s.max_seq_len + 31) / 32;
+  int64_t parts = (VP_TARGET_PARTS + pairs - 1) / pairs;
+  if (parts > (tiles + 1) / 2) parts = (tiles + 1) / 2;
+  if (parts < 1) parts = 1;
+  p.nparts = static_cast<int>(parts);
   // Kept pass: 64 rows (two tiles) per work-group, or 32 when that leaves
   // fewer than 1024 work-groups.
   p.split = static_cast<int64_t>(s.batch) * s.n_kv_heads * ((s.k_cap + 63) / 64) >= 1024 ? 64 : 32;
   p.nsplit = (s.k_cap + p.split - 1) / p.split;
   const size_t B = s.batch, Hq = s.n_q_heads, d = s.head_dim;
+  p.zs_stride = ((s.max_seq_len + 31) / 32) * 32;
   size_t off = 0;
   p.zs = off;
-  off = align256(off + B * Hq * static_cast<size_t>(s.max_vis) * 4);
+  off = align256(off + B * Hq * static_cast<size_t>(p.zs_stride) * 4);
   p.stats = off;
-  off = align256(off + B * Hq * p.nchunk * 8 * 4);
+  off = align256(off + B * Hq * p.nparts * 8 * 4);
   p.acc = off;
-  off = align256(off + B * Hq * p.nchunk * d * 4);
+  off = align256(off + B * Hq * p.nparts * d * 4);
   p.head = off;
   off = align256(off + B * Hq * 2 * 4);
   p.kstats = off;
@@ -221,8 +234,10 @@ vp_status vp_visual_mass_timed(const vp_shape* shape, const vp_layout* layout, c
   AttendArgs a = attend_args(shape, layout, params, plan, ws, q, K, V);
   if (ev_pass_begin)
     if (hipError_t e = hipEventRecord(static_cast<hipEvent_t>(ev_pass_begin), st)) return hip_fail(e, "event record");
-  if (hipError_t e = launch_attend(a, V ? MODE_SCORE_TEXT : MODE_SCORE, shape->dtype, shape->head_dim, st))
-    return hip_fail(e, "context pass launch");
+  if (hipError_t e = launch_attend(a, MODE_VIS, shape->dtype, shape->head_dim, st))
+    return hip_fail(e, "visual pass launch");
+  if (hipError_t e = launch_attend(a, V ? MODE_TEXT_BOTH : MODE_TEXT_STATS, shape->dtype, shape->head_dim, st))
+    return hip_fail(e, "text pass launch");
   if (ev_pass_end)
     if (hipError_t e = hipEventRecord(static_cast<hipEvent_t>(ev_pass_end), st)) return hip_fail(e, "event record");
   MassArgs m{};
@@ -233,8 +248,8 @@ vp_status vp_visual_mass_timed(const vp_shape* shape, const vp_layout* layout, c
   m.Hq = shape->n_q_heads;
   m.max_seq_len = shape->max_seq_len;
   m.max_vis = shape->max_vis;
-  m.chunk = plan.chunk;
-  m.nchunk = plan.nchunk;
+  m.nparts = plan.nparts;
+  m.zs_stride = plan.zs_stride;
   m.inv_tau_m = a.inv_tau_m;
   m.inv_tau_s = a.inv_tau_s;
   m.stats = a.stats;
@@ -320,7 +335,7 @@ vp_status vp_sparse_decode_attn(const vp_shape* shape, const vp_layout* layout, 
   a.vis_idx = vis_idx;
   a.kk = k;
   if (!(flags & VP_ATTN_TEXT_FROM_WORKSPACE)) {
-    if (hipError_t e = launch_attend(a, MODE_TEXT, shape->dtype, shape->head_dim, st))
+    if (hipError_t e = launch_attend(a, MODE_TEXT_ATTN, shape->dtype, shape->head_dim, st))
       return hip_fail(e, "text pass launch");
   }
   if (hipError_t e = launch_attend(a, MODE_KEPT, shape->dtype, shape->head_dim, st))
@@ -332,8 +347,7 @@ vp_status vp_sparse_decode_attn(const vp_shape* shape, const vp_layout* layout, 
   m.Hq = shape->n_q_heads;
   m.max_seq_len = shape->max_seq_len;
   m.k_cap = shape->k_cap;
-  m.chunk = plan.chunk;
-  m.nchunk = plan.nchunk;
+  m.nparts = plan.nparts;
   m.split = plan.split;
   m.nsplit = plan.nsplit;
   m.dtype = shape->dtype;

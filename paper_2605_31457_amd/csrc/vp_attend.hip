@@ -3,64 +3,96 @@
 // vp_sparse_decode_attn (Sec. 4.1/4.2).
 //
 // Work decomposition: one 64-lane wave per work-group; grid = (parts, Hkv, B).
-// A part is a chunk of `chunk` consecutive cache positions (context pass) or
-// `split` consecutive entries of the kept-index list (kept pass). The wave walks
-// its part in tiles of 64 rows (two 32-row sub-tiles) and issues all of a
-// tile's HBM reads at once: key rows into registers, value rows straight into
-// LDS with global_load_lds_dwordx4 (no registers held), so each wave keeps up
-// to 32 KB in flight.
+// In the context pass part p of `nparts` takes the 32-row tiles p, p + nparts,
+// p + 2 nparts, ... of the cache (a cyclic deal: every part, and so every XCD,
+// sees the sequence's own mix of visual and text rows); in the kept pass a part
+// is `split` consecutive entries of the kept-index list.
 //
-// Per tile the grouped query heads of this KV head (G <= 16, padded to 16) are
-// scored against the 32 key rows with matrix-core instructions:
+// Three roles share this kernel:
+//   visual pass  visual rows only: Eq. (5)/(6) and Eq. (2) statistics and the
+//                logit spill (the only large write of the step);
+//   text pass    text rows only: the same statistics and/or the attention
+//                partial over text K/V, with no large writes, so its reads
+//                stream without write traffic mixed in;
+//   kept pass    gathered kept visual rows: the attention partial.
+//
+// Memory path. Every K and V row of a tile is copied HBM -> LDS with
+// global_load_lds_dwordx4: one instruction moves whole rows (1 KB contiguous
+// per instruction for 256-byte rows), the access pattern that streams at full
+// HBM rate on gfx950 (the matrix-core operand layout, 16 rows x 64 B per load,
+// streams about 25% slower). All of a tile's copies are issued before any of
+// it is used, so no registers are held by data in flight. Inside LDS a row's
+// 16-byte pieces are XOR-swizzled by the row index (slot = piece ^ row), which
+// keeps the operand reads below free of bank conflicts.
+//
+// Per 32-row sub-tile the grouped query heads of this KV head (G <= 16, padded
+// to 16) are scored against the key rows on the matrix cores:
 //   C'[token][head] = K_tile[token][:] . q[head][:]
 // bf16: v_mfma_f32_16x16x32_bf16 (two 16-row halves x d/32 k-steps);
-// fp32: v_mfma_f32_16x16x4_f32. Key rows are loaded straight from HBM into the
-// A-operand registers (16 B per lane, 4 lanes cover 64 contiguous bytes of a
-// row). The output leaves lane l with head l%16 and tokens 16*half + 4*(l/16) + r.
+// fp32: v_mfma_f32_16x16x4_f32. Lane l then holds head l%16 for tokens
+// 16*half + 4*(l/16) + r.
 //
-// Statistics, all in the log2 domain z = Z * log2(e) with a running maximum
-// shared by the four lanes of a head:
+// Statistics, all in the log2 domain z = Z * log2(e), each over the rows of its
+// pass relative to a running maximum m (lane-local in the visual pass, shared
+// by the four lanes of a head in the text pass):
 //   Ls = sum_j 2^((z_j - m)/tau_score)   (normaliser of the Eq. (2) attention)
-//   Lm = sum_j 2^((z_j - m)/tau_mass)    (denominator of Eq. (6))
-//   Vm = sum_{j visual} 2^((z_j - m)/tau_mass)   (numerator of Eq. (5))
-// Visual logits are spilled to the workspace (rank order) for the scores,
-// which need the global (m, Ls) of every head.
+//   Lm = sum_j 2^((z_j - m)/tau_mass)    (Eq. (6) denominator; over the visual
+//                                         rows alone it is the Eq. (5) numerator)
+// A maximum is raised only when a logit exceeds it by more than a margin that
+// keeps every weight below 2^64, so rescaling is rare.
+// Visual logits are spilled to the workspace for the scores, which need the
+// global (m, Ls) of every head. The spill is indexed by cache position with
+// 128-byte aligned rows, and a full visual sub-tile is transposed through a
+// small LDS stage so that one store instruction writes one whole 128-byte line
+// per head: partial-line writes would compete with the streaming reads for the
+// L1's outstanding-request slots.
 //
 // Attention partial (text rows of the context pass, or the gathered kept rows):
 //   (m_t, l_t, acc[d]) with p_j = 2^(z_j - m_t), acc = sum_j p_j V_j.
 // The value product runs on the matrix cores as out^T[dim][head] += V^T P^T:
-// the V rows sit in LDS in groups of 1 KB (one DMA instruction each) padded to
-// 1152 bytes, so the four lane groups of the transposed read fall in different
-// bank windows; P comes straight from the score registers, so the accumulator
-// keeps lane l on head l%16 and the rescaling factor stays lane-local.
+// V is read transposed from LDS, P comes straight from the score registers, so
+// the accumulator keeps lane l on head l%16 and the rescaling factor is lane-local.
 #include "vp_common.h"
 #include "vp_internal.h"
 
 #ifndef VP_ATTEND_WAVES
-#define VP_ATTEND_WAVES 2
+#define VP_ATTEND_WAVES 2  // bf16 passes that read V
+#endif
+#ifndef VP_ATTEND_WAVES_LEAN
+#define VP_ATTEND_WAVES_LEAN 4  // bf16 passes that read only K
+#endif
+#ifndef VP_TILE_SUBS
+#define VP_TILE_SUBS 1
 #endif
 
 typedef __attribute__((address_space(1))) void global_void;
 typedef __attribute__((address_space(3))) void lds_void;
 
+// s_waitcnt immediates (gfx9 encoding: vmcnt [3:0]+[15:14], expcnt [6:4], lgkmcnt [11:8])
+constexpr int kWaitLgkm0 = 0xC07F;  // lgkmcnt(0), others unconstrained
+constexpr int kWaitVm0 = 0x0F70;    // vmcnt(0), others unconstrained
+
 namespace vp {
 namespace {
+
+// waves per SIMD the register allocation is sized for (one wave per work-group)
+constexpr int attend_waves(int dt, int mode) {
+  return dt != VP_BF16 ? 1 : ((mode == MODE_VIS || mode == MODE_TEXT_STATS) ? VP_ATTEND_WAVES_LEAN : VP_ATTEND_WAVES);
+}
 
 template <int DT, int D>
 struct Cfg {
   static constexpr bool BF = DT == VP_BF16;
   static constexpr int ESZ = BF ? 2 : 4;
   static constexpr int ROWB = D * ESZ;                      // bytes per K/V row
-  static constexpr int KLD_HALF = ROWB / 64;                // 16-byte K loads per lane per 16-row half
-  static constexpr int KLD = 2 * KLD_HALF;                  // per 32-row sub-tile
-  static constexpr int LANES_PER_ROW = ROWB / 16;           // 16-byte pieces per row
-  static constexpr int RPI = 64 / LANES_PER_ROW;            // rows per 1 KB LDS-DMA instruction
-  static constexpr int GSTR = 1024 + 128;                   // LDS bytes per DMA group (padded)
-  static constexpr int SUB_GROUPS = 32 / RPI;               // DMA instructions per sub-tile
-  static constexpr int SUB_BYTES = SUB_GROUPS * GSTR;       // LDS bytes per sub-tile
+  static constexpr int PIECES = ROWB / 16;                  // 16-byte pieces per row
+  static constexpr int RPI = 64 / PIECES;                   // rows per 1 KB copy instruction
+  static constexpr int SUB_ROWS_BYTES = 32 * ROWB;          // one 32-row block of K or V
+  static constexpr int STAGE_BYTES = 16 * 32 * 4;           // logits of 16 heads x 32 rows
+  static constexpr int COPIES = 32 / RPI;                   // copy instructions per block
   static constexpr int ACC_N = BF ? (D / 64) * 4 : D / 16;  // f32x4 accumulators
-  // LDS offset of row r of a sub-tile
-  static __device__ __forceinline__ int row_off(int r) { return (r / RPI) * GSTR + (r % RPI) * ROWB; }
+  // LDS byte offset of 16-byte piece p of row r inside a block
+  static __device__ __forceinline__ int at(int r, int p) { return r * ROWB + 16 * (p ^ (r & (PIECES - 1))); }
 };
 
 template <int DT, int D>
@@ -99,31 +131,31 @@ __device__ __forceinline__ void load_q(QFrag<DT, D>& f, const void* qrow, bool v
   }
 }
 
-// 16-byte piece j of this lane's share of a key row (same dim mapping as load_q)
+// C'[token n16 of 16-row half hf][head] from the key block in LDS (same dim
+// mapping as load_q)
 template <int DT, int D>
-__device__ __forceinline__ int kpiece(int a4, int j) {
-  if constexpr (DT == VP_BF16)
-    return 4 * j + a4;
-  else
-    return (D / 16) * a4 + j;
-}
-
-// C'[token n16 of a 16-row half][head] from the lane's preloaded key pieces
-template <int DT, int D>
-__device__ __forceinline__ f32x4 score_half(const uint4* kr, const QFrag<DT, D>& q) {
+__device__ __forceinline__ f32x4 score_half(const unsigned char* kb, int hf, const QFrag<DT, D>& q, int a4,
+                                            int n16) {
+  using C = Cfg<DT, D>;
+  const int r = 16 * hf + n16;
   f32x4 c = {0.f, 0.f, 0.f, 0.f};
   if constexpr (DT == VP_BF16) {
+    uint4 k[D / 32];
+#pragma unroll
+    for (int s = 0; s < D / 32; ++s) k[s] = *reinterpret_cast<const uint4*>(kb + C::at(r, 4 * s + a4));
 #pragma unroll
     for (int s = 0; s < D / 32; ++s)
-      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, kr[s]), q.v[s], c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, k[s]), q.v[s], c, 0, 0, 0);
   } else {
+    float4 k[D / 16];
+#pragma unroll
+    for (int s4 = 0; s4 < D / 16; ++s4) k[s4] = *reinterpret_cast<const float4*>(kb + C::at(r, (D / 16) * a4 + s4));
 #pragma unroll
     for (int s4 = 0; s4 < D / 16; ++s4) {
-      const float4 u = __builtin_bit_cast(float4, kr[s4]);
-      c = __builtin_amdgcn_mfma_f32_16x16x4f32(u.x, q.v[4 * s4 + 0], c, 0, 0, 0);
-      c = __builtin_amdgcn_mfma_f32_16x16x4f32(u.y, q.v[4 * s4 + 1], c, 0, 0, 0);
-      c = __builtin_amdgcn_mfma_f32_16x16x4f32(u.z, q.v[4 * s4 + 2], c, 0, 0, 0);
-      c = __builtin_amdgcn_mfma_f32_16x16x4f32(u.w, q.v[4 * s4 + 3], c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_16x16x4f32(k[s4].x, q.v[4 * s4 + 0], c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_16x16x4f32(k[s4].y, q.v[4 * s4 + 1], c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_16x16x4f32(k[s4].z, q.v[4 * s4 + 2], c, 0, 0, 0);
+      c = __builtin_amdgcn_mfma_f32_16x16x4f32(k[s4].w, q.v[4 * s4 + 3], c, 0, 0, 0);
     }
   }
   return c;
@@ -134,7 +166,7 @@ __device__ __forceinline__ f32x4 score_half(const uint4* kr, const QFrag<DT, D>&
 __device__ __forceinline__ int pv_token(int a4, int i) { return i < 4 ? 4 * a4 + i : 16 + 4 * a4 + (i - 4); }
 
 template <int DT, int D, int N>
-__device__ __forceinline__ void value_product(f32x4 (&acc)[N], const unsigned char* vlds, const float (&p)[8],
+__device__ __forceinline__ void value_product(f32x4 (&acc)[N], const unsigned char* vb, const float (&p)[8],
                                               int a4, int n16) {
   using C = Cfg<DT, D>;
   if constexpr (DT == VP_BF16) {
@@ -144,10 +176,11 @@ __device__ __forceinline__ void value_product(f32x4 (&acc)[N], const unsigned ch
     for (int i = 0; i < 8; ++i) pf[i] = static_cast<__bf16>(p[i]);
 #pragma unroll
     for (int u = 0; u < D / 64; ++u) {
+      // lane n16 takes dims 64u + 4*n16 .. +3 = 8 bytes in piece 8u + n16/2
       uint2 w[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i)
-        w[i] = *reinterpret_cast<const uint2*>(vlds + C::row_off(pv_token(a4, i)) + 128 * u + 8 * n16);
+        w[i] = *reinterpret_cast<const uint2*>(vb + C::at(pv_token(a4, i), 8 * u + (n16 >> 1)) + 8 * (n16 & 1));
       // A operand of MFMA (u, e): row n16 <-> dim 64u + 4*n16 + e, slot i <-> token pv_token(a4, i)
       uint32_t lo0[4], hi0[4], lo1[4], hi1[4];
 #pragma unroll
@@ -170,10 +203,11 @@ __device__ __forceinline__ void value_product(f32x4 (&acc)[N], const unsigned ch
     // k-step s covers tokens pv_token(a4, s) (one per lane group); row n16 <-> dim 16*dt + n16
 #pragma unroll
     for (int s = 0; s < 8; ++s) {
-      const unsigned char* row = vlds + C::row_off(pv_token(a4, s));
+      const int t = pv_token(a4, s);
 #pragma unroll
       for (int dt = 0; dt < D / 16; ++dt) {
-        const float v = *reinterpret_cast<const float*>(row + 4 * (16 * dt + n16));
+        const int dim = 16 * dt + n16;
+        const float v = *reinterpret_cast<const float*>(vb + C::at(t, dim >> 2) + 4 * (dim & 3));
         acc[dt] = __builtin_amdgcn_mfma_f32_16x16x4f32(v, p[s], acc[dt], 0, 0, 0);
       }
     }
@@ -214,30 +248,33 @@ struct Sub {
   SegWalker w;  // segment walker positioned at t0 (context pass)
 };
 
-// All per-wave state of one part; the member functions are force-inlined so the
-// key registers never leave the register file.
+// All per-wave state of one part; member functions are force-inlined.
 template <int DT, int D, int MODE>
 struct Pass {
   using C = Cfg<DT, D>;
   static constexpr bool KEPT = MODE == MODE_KEPT;
-  static constexpr bool SCORE = (MODE & MODE_SCORE) != 0 && !KEPT;
-  static constexpr bool ATTN = KEPT || (MODE & MODE_TEXT) != 0;
-  static constexpr bool SKIP_VIS = MODE == MODE_TEXT;  // text-only pass never touches visual rows
+  static constexpr bool VIS = MODE == MODE_VIS;                  // visual rows: statistics + spill
+  static constexpr bool TSTATS = (MODE & MODE_TEXT_STATS) != 0;  // text rows: statistics
+  static constexpr bool ATTN = KEPT || (MODE & MODE_TEXT_ATTN) != 0;
+  static constexpr bool TEXT = !KEPT && !VIS;                    // a text-row pass
 
   const AttendArgs& a;
-  unsigned char* vlds;
-  int lane, n16, a4, L, r0, r1, h;
+  int lane, n16, a4, L, r0, r1, step, h;  // rows [r0, r1) in tiles `step` apart
   bool hv;
   const int32_t* kept;
   const char* Kb;
   const char* Vb;
   size_t rstride;
-  float* zrow;
+  float* zrow;   // spill row of this lane's head
+  float* zbase;  // spill row of the first head of this KV group
   QFrag<DT, D> qf;
-  float m_all, Ls, Lm, Vm, m_t, l_t;
+  // visual pass: lane-local reference and sums (merged over a head's 4 lanes at the end)
+  float m_v, Ls_v, Lm_v;
+  // text / kept pass: reference shared by a head's 4 lanes, sums and value partial
+  float m_t, l_t, Lm_t, Ls_t;
   f32x4 acc[C::ACC_N];
 
-  __device__ __forceinline__ Pass(const AttendArgs& a_, unsigned char* vlds_) : a(a_), vlds(vlds_) {}
+  __device__ __forceinline__ explicit Pass(const AttendArgs& a_) : a(a_) {}
 
   // cache position of part row t (clamped to a readable row; validity is tracked separately)
   __device__ __forceinline__ int row_pos(int t) const {
@@ -249,10 +286,14 @@ struct Pass {
     }
   }
 
+  // does this pass have rows in sub-tile s
   __device__ __forceinline__ bool active(const Sub& s) const {
-    return s.t0 < r1 && !(SKIP_VIS && s.cls == TILE_VIS);
+    if (s.t0 >= r1) return false;
+    if constexpr (VIS) return s.cls != TILE_TEXT;
+    if constexpr (TEXT) return s.cls != TILE_VIS;
+    return true;
   }
-  __device__ __forceinline__ bool needs_v(const Sub& s) const { return ATTN && (KEPT || s.cls != TILE_VIS); }
+  __device__ __forceinline__ bool needs_v(const Sub& s) const { return ATTN; }
 
   __device__ __forceinline__ Sub sub_at(const Sub& prev, int t0) const {
     Sub n = prev;
@@ -267,63 +308,53 @@ struct Pass {
     return n;
   }
 
-  // this lane's key pieces of sub-tile s, into registers
-  __device__ __forceinline__ void load_k(uint4 (&kr)[C::KLD], const Sub& s) const {
+  // the 32 rows of sub-tile s from `src` (K or V of this head) into an LDS block:
+  // lane l of copy j carries row j*RPI + l/PIECES, swizzled slot l%PIECES
+  __device__ __forceinline__ void copy_rows(const char* src, const Sub& s, unsigned char* block) const {
+    const int rr = lane / C::PIECES;
+    const int slot = lane % C::PIECES;
 #pragma unroll
-    for (int hf = 0; hf < 2; ++hf) {
-      const uint4* row = reinterpret_cast<const uint4*>(Kb + row_pos(s.t0 + 16 * hf + n16) * rstride);
-#pragma unroll
-      for (int j = 0; j < C::KLD_HALF; ++j) kr[hf * C::KLD_HALF + j] = row[kpiece<DT, D>(a4, j)];
-    }
-  }
-  // the 32 value rows of sub-tile s, HBM -> LDS directly (lane l of DMA group j
-  // carries 16 bytes of row j*RPI + l/LANES_PER_ROW)
-  __device__ __forceinline__ void dma_v(const Sub& s, unsigned char* lbase) const {
-    const int rr = lane / C::LANES_PER_ROW;
-    const int col = lane % C::LANES_PER_ROW;
-#pragma unroll
-    for (int j = 0; j < C::SUB_GROUPS; ++j) {
-      const char* src = Vb + row_pos(s.t0 + j * C::RPI + rr) * rstride + 16 * col;
-      __builtin_amdgcn_global_load_lds((global_void*)(src), (lds_void*)(lbase + j * C::GSTR), 16, 0, 0);
+    for (int j = 0; j < C::COPIES; ++j) {
+      const int r = j * C::RPI + rr;
+      const int piece = slot ^ (r & (C::PIECES - 1));
+      const char* g = src + row_pos(s.t0 + r) * rstride + 16 * piece;
+      __builtin_amdgcn_global_load_lds((global_void*)(g), (lds_void*)(block + 1024 * j), 16, 0, 0);
     }
   }
 
-  __device__ __forceinline__ void process(const Sub& tile, const uint4 (&kr)[C::KLD], const unsigned char* vsub) {
+  __device__ __forceinline__ void process(const Sub& tile, const unsigned char* kblk, const unsigned char* vblk,
+                                         float* stage) {
     const int t0 = tile.t0;
     const int cls = tile.cls;
     const int t_end = min(t0 + 32, r1);
     // ---- scores of the 32 rows against the query group ----
-    const f32x4 c0 = score_half<DT, D>(kr, qf);
-    const f32x4 c1 = score_half<DT, D>(kr + C::KLD_HALF, qf);
-
+    const f32x4 c0 = score_half<DT, D>(kblk, 0, qf, a4, n16);
+    const f32x4 c1 = score_half<DT, D>(kblk, 1, qf, a4, n16);
     float z[8];
-    bool valid[8], vis[8];
-    int rank[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int tt = 16 * (i >> 2) + 4 * a4 + (i & 3);
-      z[i] = (i < 4 ? c0[i & 3] : c1[i & 3]) * a.zscale;
-      vis[i] = false;
-      rank[i] = 0;
-      if constexpr (KEPT) {
-        const int t = t0 + tt;
+    for (int i = 0; i < 8; ++i) z[i] = (i < 4 ? c0[i & 3] : c1[i & 3]) * a.zscale;
+
+    // value i of this lane is row t0 + 16*(i/4) + 4*a4 + i%4; bit i of the masks
+    unsigned valid = 0xffu, vis = 0u;
+    if constexpr (KEPT) {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int t = t0 + 16 * (i >> 2) + 4 * a4 + (i & 3);
         bool ok = t < r1;
         if (ok) {
           const int p = kept[t];
           ok = p >= 0 && p < L;
         }
-        valid[i] = ok;
-      } else {
-        valid[i] = t0 + tt < t_end;
+        valid &= ok ? 0xffu : ~(1u << i);
       }
-    }
-    if constexpr (!KEPT) {
-      if (cls == TILE_VIS) {
+    } else {
+      if (t_end - t0 < 32) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          vis[i] = true;
-          rank[i] = tile.w.rank + (t0 + 16 * (i >> 2) + 4 * a4 + (i & 3) - tile.w.st);
-        }
+        for (int i = 0; i < 8; ++i)
+          if (t0 + 16 * (i >> 2) + 4 * a4 + (i & 3) >= t_end) valid &= ~(1u << i);
+      }
+      if (cls == TILE_VIS) {
+        vis = valid;
       } else if (cls == TILE_MIXED) {
         SegWalker lw = tile.w;
 #pragma unroll
@@ -331,88 +362,116 @@ struct Pass {
           const int p = t0 + 16 * (i >> 2) + 4 * a4 + (i & 3);
           if (p < t_end) {
             lw.seek(p);
-            vis[i] = lw.contains(p);
-            rank[i] = lw.rank + (p - lw.st);
+            if (lw.contains(p)) vis |= 1u << i;
           }
         }
       }
     }
 
-    // ---- Eq. (5)/(6) and Eq. (2) statistics ----
-    if constexpr (SCORE) {
-      float tmax = kNegInf;
+    if constexpr (VIS) {
+      // ---- Eq. (5)/(6) and Eq. (2) statistics over visual rows ----
+      float lmax = kNegInf;
 #pragma unroll
       for (int i = 0; i < 8; ++i)
-        if (valid[i]) tmax = fmaxf(tmax, z[i]);
-      tmax = max_over_quads(tmax);
-      const float mn = fmaxf(m_all, tmax);
-      const float als = fast_exp2((m_all - mn) * a.inv_tau_s);
-      const float alm = fast_exp2((m_all - mn) * a.inv_tau_m);
-      float ts = 0.f, tm = 0.f, tv = 0.f;
+        if (vis & (1u << i)) lmax = fmaxf(lmax, z[i]);
+      const bool up = lmax > m_v + a.thr_s;  // per lane; rare after the first tile
+      if (__builtin_amdgcn_ballot_w64(up)) {
+        Ls_v *= up ? fast_exp2((m_v - lmax) * a.inv_tau_s) : 1.f;
+        Lm_v *= up ? fast_exp2((m_v - lmax) * a.inv_tau_m) : 1.f;
+        m_v = up ? lmax : m_v;
+      }
+      float ts = 0.f, tm = 0.f;
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
-        const float d = valid[i] ? z[i] - mn : kNegInf;
-        const float es = fast_exp2(d * a.inv_tau_s);
-        const float em = fast_exp2(d * a.inv_tau_m);
-        ts += es;
-        tm += em;
-        tv += vis[i] ? em : 0.f;
+        const float d = (vis & (1u << i)) ? z[i] - m_v : kNegInf;
+        ts += fast_exp2(d * a.inv_tau_s);
+        tm += fast_exp2(d * a.inv_tau_m);
       }
-      Ls = Ls * als + ts;
-      Lm = Lm * alm + tm;
-      Vm = Vm * alm + tv;
-      m_all = mn;
-      if (hv) {
+      Ls_v += ts;
+      Lm_v += tm;
+      // visual logits, position order
+      if (cls == TILE_VIS && t_end - t0 == 32) {
+        // transpose through the stage: lane (a4, n16) holds head n16, rows
+        // 16*hf + 4*a4 .. +3; lane l then stores 16 bytes of head l/8's line
+        *reinterpret_cast<float4*>(stage + n16 * 32 + 4 * a4) = make_float4(z[0], z[1], z[2], z[3]);
+        *reinterpret_cast<float4*>(stage + n16 * 32 + 16 + 4 * a4) = make_float4(z[4], z[5], z[6], z[7]);
+#pragma unroll
+        for (int round = 0; round < 2; ++round) {
+          const int hh = 8 * round + (lane >> 3);
+          if (round == 0 || a.G > 8) {
+            const float4 v = *reinterpret_cast<const float4*>(stage + hh * 32 + 4 * (lane & 7));
+            if (hh < a.G)
+              *reinterpret_cast<float4*>(zbase + static_cast<size_t>(hh) * a.zs_stride + t0 + 4 * (lane & 7)) = v;
+          }
+        }
+      } else if (hv && vis) {
 #pragma unroll
         for (int i = 0; i < 8; ++i)
-          if (valid[i] && vis[i] && rank[i] < a.max_vis) zrow[rank[i]] = z[i];
+          if (vis & (1u << i)) zrow[t0 + 16 * (i >> 2) + 4 * a4 + (i & 3)] = z[i];
       }
-    }
-
-    // ---- attention partial over text rows (context pass) or kept rows ----
-    if constexpr (ATTN) {
-      if (needs_v(tile)) {
-        float zt[8];
-        float tmax = kNegInf;
+    } else {
+      // ---- text rows (or kept rows): attention weights, statistics, value product ----
+      const unsigned att = valid & ~vis;
+      float lmax = kNegInf;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          zt[i] = (valid[i] && !vis[i]) ? z[i] : kNegInf;
-          tmax = fmaxf(tmax, zt[i]);
+      for (int i = 0; i < 8; ++i)
+        if (att & (1u << i)) lmax = fmaxf(lmax, z[i]);
+      if (__builtin_amdgcn_ballot_w64(lmax > m_t + a.thr_t)) {
+        // the four lanes of a head share the reference (their weights meet in one MFMA)
+        const float tm = max_over_quads(lmax);
+        const bool up = tm > m_t + a.thr_t;
+        const float d = m_t - tm;
+        const float al = up ? fast_exp2(d) : 1.f;
+        l_t *= al;
+        if constexpr (TSTATS) {
+          Lm_t *= up ? fast_exp2(d * a.inv_tau_m) : 1.f;
+          Ls_t *= up ? fast_exp2(d * a.inv_tau_s) : 1.f;
         }
-        tmax = max_over_quads(tmax);
-        if (tmax != kNegInf) {
-          const float mn = fmaxf(m_t, tmax);
-          const float al = fast_exp2(m_t - mn);
-          float p[8];
-          float ps = 0.f;
-#pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            p[i] = fast_exp2(zt[i] - mn);
-            ps += p[i];
-          }
-          l_t = l_t * al + ps;
-          m_t = mn;
+        if constexpr (ATTN) {
 #pragma unroll
           for (int i = 0; i < C::ACC_N; ++i) acc[i] *= al;
-          // the value rows were written to LDS by the DMA: wait for every
-          // outstanding vector-memory operation, then read them transposed
-          __builtin_amdgcn_s_waitcnt(0);
-          __syncthreads();
-          value_product<DT, D, C::ACC_N>(acc, vsub, p, a4, n16);
         }
+        m_t = up ? tm : m_t;
+      }
+      float p[8];
+      float ps = 0.f;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        p[i] = (att & (1u << i)) ? fast_exp2(z[i] - m_t) : 0.f;
+        ps += p[i];
+      }
+      l_t += ps;
+      if constexpr (TSTATS) {
+        float tm = 0.f, ts = 0.f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const float d = (att & (1u << i)) ? z[i] - m_t : kNegInf;
+          tm += fast_exp2(d * a.inv_tau_m);
+          if (!a.tau_s_one) ts += fast_exp2(d * a.inv_tau_s);
+        }
+        Lm_t += tm;
+        Ls_t += ts;
+      }
+      if constexpr (ATTN) {
+        if (__builtin_amdgcn_ballot_w64(att != 0u)) value_product<DT, D, C::ACC_N>(acc, vblk, p, a4, n16);
       }
     }
   }
 };
 
 template <int DT, int D, int MODE>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(VP_ATTEND_WAVES))) void attend_kernel(
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(attend_waves(DT, MODE)))) void attend_kernel(
     const AttendArgs a) {
   using C = Cfg<DT, D>;
   using P = Pass<DT, D, MODE>;
-  __shared__ __attribute__((aligned(16))) unsigned char vlds[P::ATTN ? 2 * C::SUB_BYTES : 16];
+  constexpr int NSUB = VP_TILE_SUBS;
+  // per sub-tile: K block, V block (passes that read V), logit stage (visual pass)
+  constexpr int VB = P::ATTN ? C::SUB_ROWS_BYTES : 0;
+  constexpr int SB = P::VIS ? C::STAGE_BYTES : 0;
+  constexpr int SUB = C::SUB_ROWS_BYTES + VB + SB;
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[NSUB * SUB];
 
-  P s(a, vlds);
+  P s(a);
   s.lane = threadIdx.x;
   s.n16 = s.lane & 15;
   s.a4 = s.lane >> 4;
@@ -427,10 +486,12 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(VP_ATTEND_WA
     kb = kb < 0 ? 0 : (kb > a.k_cap ? a.k_cap : kb);
     s.r0 = part * a.split;
     s.r1 = min(s.r0 + a.split, kb);
+    s.step = 32;
     s.kept = a.vis_idx + static_cast<size_t>(b) * a.k_cap;
   } else {
-    s.r0 = part * a.chunk;
-    s.r1 = min(s.r0 + a.chunk, s.L);
+    s.r0 = 32 * part;
+    s.r1 = s.L;
+    s.step = 32 * a.nparts;
   }
   if (s.r0 >= s.r1) return;
 
@@ -444,83 +505,108 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(VP_ATTEND_WA
   load_q<DT, D>(s.qf,
                 static_cast<const char*>(a.q) + (static_cast<size_t>(b) * a.Hq + (s.hv ? s.h : 0)) * C::ROWB,
                 s.hv, s.a4);
-  s.m_all = kNegInf;
-  s.Ls = s.Lm = s.Vm = 0.f;
+  s.m_v = kNegInf;
+  s.Ls_v = s.Lm_v = 0.f;
   s.m_t = kNegInf;
-  s.l_t = 0.f;
+  s.l_t = s.Lm_t = s.Ls_t = 0.f;
 #pragma unroll
   for (int i = 0; i < C::ACC_N; ++i) s.acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  s.zrow = P::SCORE ? a.zs + (static_cast<size_t>(b) * a.Hq + (s.hv ? s.h : 0)) * a.max_vis : nullptr;
+  s.zbase = P::VIS ? a.zs + (static_cast<size_t>(b) * a.Hq + static_cast<size_t>(g) * a.G) * a.zs_stride : nullptr;
+  s.zrow = P::VIS ? s.zbase + static_cast<size_t>(s.hv ? s.n16 : 0) * a.zs_stride : nullptr;
 
-  Sub s0;
-  s0.t0 = s.r0;
-  s0.cls = TILE_TEXT;
+  Sub cur;
+  cur.t0 = s.r0;
+  cur.cls = TILE_TEXT;
   if constexpr (!P::KEPT) {
     const int o0 = a.seg_off[b];
-    s0.w.start(a.seg + 2 * static_cast<long>(o0), a.seg_off[b + 1] - o0, s.L);
+    cur.w.start(a.seg + 2 * static_cast<long>(o0), a.seg_off[b + 1] - o0, s.L);
   }
-  s0 = s.sub_at(s0, s.r0);
+  cur = s.sub_at(cur, s.r0);
 
-  uint4 k0[C::KLD], k1[C::KLD];
-  unsigned char* v0 = vlds;
-  unsigned char* v1 = vlds + C::SUB_BYTES;
-  // 64-row tiles: every read of the tile is issued before any of it is used
-  while (s0.t0 < s.r1) {
-    const Sub s1 = s.sub_at(s0, s0.t0 + 32);
-    const bool act0 = s.active(s0), act1 = s.active(s1);
-    if constexpr (P::ATTN) __syncthreads();  // the previous tile's LDS reads are done
-    if (act0) s.load_k(k0, s0);
-    if (act1) s.load_k(k1, s1);
-    if constexpr (P::ATTN) {
-      if (act0 && s.needs_v(s0)) s.dma_v(s0, v0);
-      if (act1 && s.needs_v(s1)) s.dma_v(s1, v1);
+  // tiles of NSUB sub-tiles: all copies of a tile are issued before any of it is used
+  while (cur.t0 < s.r1) {
+    Sub sub[NSUB];
+    bool act[NSUB];
+    sub[0] = cur;
+#pragma unroll
+    for (int i = 1; i < NSUB; ++i) sub[i] = s.sub_at(sub[i - 1], sub[i - 1].t0 + s.step);
+#pragma unroll
+    for (int i = 0; i < NSUB; ++i) act[i] = s.active(sub[i]);
+    // The work-group is a single wave, so ordering needs counters, not barriers
+    // (a barrier's release fence would also wait for the logit stores of the
+    // previous tile). LDS reads of the previous tile must have returned before
+    // the copies overwrite it:
+    __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+#pragma unroll
+    for (int i = 0; i < NSUB; ++i) {
+      if (act[i]) {
+        unsigned char* blk = lds + i * SUB;
+        s.copy_rows(s.Kb, sub[i], blk);
+        if (s.needs_v(sub[i])) s.copy_rows(s.Vb, sub[i], blk + C::SUB_ROWS_BYTES);
+      }
     }
-    if (act0) s.process(s0, k0, v0);
-    if (act1) s.process(s1, k1, v1);
-    s0 = s.sub_at(s1, s1.t0 + 32);
+    // the copies have landed in LDS once the vector-memory counter drains
+    __builtin_amdgcn_s_waitcnt(kWaitVm0);
+#pragma unroll
+    for (int i = 0; i < NSUB; ++i)
+      if (act[i])
+        s.process(sub[i], lds + i * SUB, lds + i * SUB + C::SUB_ROWS_BYTES,
+                  reinterpret_cast<float*>(lds + i * SUB + C::SUB_ROWS_BYTES + VB));
+    cur = s.sub_at(sub[NSUB - 1], sub[NSUB - 1].t0 + s.step);
   }
 
   // ---- write this part's partials ----
-  if constexpr (P::SCORE) {
-    const float s_ls = sum_over_quads(s.Ls);
-    const float s_lm = sum_over_quads(s.Lm);
-    const float s_vm = sum_over_quads(s.Vm);
+  if constexpr (P::VIS) {
+    // merge the four lanes' statistics onto their common maximum
+    const float M = max_over_quads(s.m_v);
+    const bool any = s.m_v != kNegInf;
+    const float fs = any ? fast_exp2((s.m_v - M) * a.inv_tau_s) : 0.f;
+    const float fm = any ? fast_exp2((s.m_v - M) * a.inv_tau_m) : 0.f;
+    const float s_ls = sum_over_quads(s.Ls_v * fs);
+    const float s_lm = sum_over_quads(s.Lm_v * fm);
     if (s.hv && s.a4 == 0) {
-      float* st = a.stats + ((static_cast<size_t>(b) * a.Hq + s.h) * a.nchunk + part) * 8;
-      *reinterpret_cast<float4*>(st) = make_float4(s.m_all, s_ls, s_lm, s_vm);
+      float* st = a.stats + ((static_cast<size_t>(b) * a.Hq + s.h) * a.nparts + part) * 8;
+      *reinterpret_cast<float4*>(st) = make_float4(M, s_ls, s_lm, 0.f);
     }
-  }
-  if constexpr (P::ATTN) {
+  } else {
     const float s_lt = sum_over_quads(s.l_t);
+    const float s_lm = P::TSTATS ? sum_over_quads(s.Lm_t) : 0.f;
+    const float s_ls = P::TSTATS ? (a.tau_s_one ? s_lt : sum_over_quads(s.Ls_t)) : 0.f;
     if (s.hv) {
-      float* dst;
       if constexpr (P::KEPT) {
         const size_t row = (static_cast<size_t>(b) * a.Hq + s.h) * a.nsplit + part;
-        dst = a.kacc + row * D;
         if (s.a4 == 0) *reinterpret_cast<float2*>(a.kstats + row * 2) = make_float2(s.m_t, s_lt);
+        store_acc<DT, D, C::ACC_N>(a.kacc + row * D, s.acc, s.a4);
       } else {
-        const size_t row = (static_cast<size_t>(b) * a.Hq + s.h) * a.nchunk + part;
-        dst = a.acc + row * D;
-        if (s.a4 == 0) *reinterpret_cast<float2*>(a.stats + row * 8 + 4) = make_float2(s.m_t, s_lt);
+        const size_t row = (static_cast<size_t>(b) * a.Hq + s.h) * a.nparts + part;
+        if (s.a4 == 0) {
+          if constexpr (P::TSTATS)
+            *reinterpret_cast<float4*>(a.stats + row * 8 + 4) = make_float4(s.m_t, s_lt, s_lm, s_ls);
+          else
+            *reinterpret_cast<float2*>(a.stats + row * 8 + 4) = make_float2(s.m_t, s_lt);
+        }
+        if constexpr (P::ATTN) store_acc<DT, D, C::ACC_N>(a.acc + row * D, s.acc, s.a4);
       }
-      store_acc<DT, D, C::ACC_N>(dst, s.acc, s.a4);
     }
   }
 }
 
 template <int DT, int D>
 hipError_t launch_dd(const AttendArgs& a, int mode, hipStream_t st) {
-  const dim3 grid(mode == MODE_KEPT ? a.nsplit : a.nchunk, a.Hkv, a.B);
+  const dim3 grid(mode == MODE_KEPT ? a.nsplit : a.nparts, a.Hkv, a.B);
   const dim3 block(64);
   switch (mode) {
-    case MODE_SCORE:
-      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_SCORE>), grid, block, 0, st, a);
+    case MODE_VIS:
+      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_VIS>), grid, block, 0, st, a);
       break;
-    case MODE_TEXT:
-      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_TEXT>), grid, block, 0, st, a);
+    case MODE_TEXT_STATS:
+      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_TEXT_STATS>), grid, block, 0, st, a);
       break;
-    case MODE_SCORE_TEXT:
-      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_SCORE_TEXT>), grid, block, 0, st, a);
+    case MODE_TEXT_ATTN:
+      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_TEXT_ATTN>), grid, block, 0, st, a);
+      break;
+    case MODE_TEXT_BOTH:
+      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_TEXT_BOTH>), grid, block, 0, st, a);
       break;
     case MODE_KEPT:
       hipLaunchKernelGGL((attend_kernel<DT, D, MODE_KEPT>), grid, block, 0, st, a);

@@ -12,13 +12,15 @@ namespace vp {
 
 // Work decomposition and workspace carving, a pure function of the shape.
 struct Plan {
-  int chunk;    // cache positions per context-pass work-group (multiple of 32)
-  int nchunk;   // ceil(max_seq_len / chunk)
+  int nparts;   // context-pass work-groups per (sequence, KV head); part p takes
+                // the 32-row tiles p, p + nparts, p + 2 nparts, ...
   int split;    // kept rows per kept-pass work-group (multiple of 32)
   int nsplit;   // ceil(k_cap / split)
-  size_t zs;      // float [B][Hq][max_vis]     visual logits (log2 domain)
-  size_t stats;   // float [B][Hq][nchunk][8]   per-chunk softmax statistics
-  size_t acc;     // float [B][Hq][nchunk][d]   per-chunk text value partials
+  int zs_stride;  // floats per spill row: max_seq_len rounded up to 32 (128-byte rows)
+  size_t zs;      // float [B][Hq][zs_stride]   visual logits (log2 domain), by cache position
+  size_t stats;   // float [B][Hq][nparts][8]   per-part statistics: visual rows
+                  //   {m_v, Ls_v, Lm_v, -}, text rows {m_t, l_t, Lm_t, Ls_t}
+  size_t acc;     // float [B][Hq][nparts][d]   per-part text value partials
   size_t head;    // float [B][Hq][2]           merged (max, score normaliser)
   size_t kstats;  // float [B][Hq][nsplit][2]   kept-row (max, sum)
   size_t kacc;    // float [B][Hq][nsplit][d]   kept-row value partials
@@ -27,7 +29,16 @@ struct Plan {
 
 Plan make_plan(const vp_shape& s);
 
-enum Mode : int { MODE_SCORE = 1, MODE_TEXT = 2, MODE_SCORE_TEXT = 3, MODE_KEPT = 4 };
+// Passes over the cache. The visual pass is the only one that writes a large
+// output (the logit spill); keeping it apart from the text pass keeps writes out
+// of the text pass's read stream.
+enum Mode : int {
+  MODE_VIS = 1,         // visual rows: Eq. (5)/(6) statistics + logit spill
+  MODE_TEXT_STATS = 2,  // text rows: Eq. (6)/(2) normaliser statistics
+  MODE_TEXT_ATTN = 4,   // text rows: attention partial (reads V)
+  MODE_TEXT_BOTH = 6,
+  MODE_KEPT = 8         // kept visual rows: attention partial
+};
 
 struct AttendArgs {
   const void* q;
@@ -41,7 +52,11 @@ struct AttendArgs {
   float zscale;         // sm_scale * log2(e)
   float inv_tau_m;      // 1 / tau_mass
   float inv_tau_s;      // 1 / tau_score
-  int chunk, nchunk;
+  float thr_s;          // raise a running maximum of the statistics only past this margin (log2 units)
+  float thr_t;          // same for the attention partial
+  int tau_s_one;        // tau_score == 1: the attention weight doubles as the score weight
+  int nparts;
+  int zs_stride;
   float* zs;
   float* stats;
   float* acc;
@@ -52,13 +67,19 @@ struct AttendArgs {
   float* kacc;
 };
 
+// context-pass parts that hold at least one tile of a sequence of length L
+__host__ __device__ inline int parts_used(int L, int nparts) {
+  const int tiles = (L + 31) / 32;
+  return tiles < nparts ? tiles : nparts;
+}
+
 hipError_t launch_attend(const AttendArgs& a, int mode, int dtype, int head_dim, hipStream_t st);
 
 struct MassArgs {
   const int32_t* seq_len;
   const int32_t* seg_off;
   const int32_t* seg;
-  int B, Hq, max_seq_len, max_vis, chunk, nchunk;
+  int B, Hq, max_seq_len, max_vis, nparts, zs_stride;
   float inv_tau_m, inv_tau_s;
   const float* stats;
   const float* zs;
@@ -98,7 +119,7 @@ hipError_t launch_topk(const TopkArgs& a, hipStream_t st);
 struct MergeArgs {
   const int32_t* seq_len;
   const int32_t* kk;
-  int B, Hq, max_seq_len, k_cap, chunk, nchunk, split, nsplit, dtype;
+  int B, Hq, max_seq_len, k_cap, nparts, split, nsplit, dtype;
   const float* stats;
   const float* acc;
   const float* kstats;

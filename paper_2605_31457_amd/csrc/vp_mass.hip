@@ -7,10 +7,11 @@
 namespace vp {
 namespace {
 
-// One work-group per sequence, one wave per head (lanes over chunks): merges
-// the per-chunk statistics of every head (max-shifted sums, combined in double
-// with fixed-order wave reductions), writes m^{vis}_{t,h}, the head mean M_vis
-// and head max M_vis,max, and the per-head (max, score normaliser) the scores
+// One work-group per sequence, one wave per head (lanes over parts): merges
+// the per-part statistics of every head (visual rows and text rows are kept
+// apart by the context pass; max-shifted sums, combined in double with
+// fixed-order wave reductions), writes m^{vis}_{t,h}, the head mean M_vis and
+// head max M_vis,max, and the per-head (max, score normaliser) the scores
 // kernel needs.
 __global__ __launch_bounds__(256) void mass_finalize_kernel(const MassArgs a) {
   constexpr int kWaves = 4;
@@ -19,24 +20,30 @@ __global__ __launch_bounds__(256) void mass_finalize_kernel(const MassArgs a) {
   const int lane = tid & 63;
   const int wid = tid >> 6;
   const int L = clamp_len(a.seq_len[b], a.max_seq_len);
-  const int nv = (L + a.chunk - 1) / a.chunk;
+  const int nv = parts_used(L, a.nparts);
   double msum = 0.0;
   double mmax = 0.0;
   for (int h = wid; h < a.Hq; h += kWaves) {
-    const float4* st = reinterpret_cast<const float4*>(a.stats + (static_cast<size_t>(b) * a.Hq + h) * a.nchunk * 8);
+    // per part: [0] visual {m, Ls, Lm, -}, [1] text {m, l, Lm, Ls}
+    const float4* st = reinterpret_cast<const float4*>(a.stats + (static_cast<size_t>(b) * a.Hq + h) * a.nparts * 8);
     float m = kNegInf;
-    for (int c = lane; c < nv; c += 64) m = fmaxf(m, st[2 * c].x);
+    for (int c = lane; c < nv; c += 64) m = fmaxf(m, fmaxf(st[2 * c].x, st[2 * c + 1].x));
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
     double Ls = 0.0, Lm = 0.0, Vm = 0.0;
     for (int c = lane; c < nv; c += 64) {
-      const float4 s = st[2 * c];
-      if (s.x == kNegInf) continue;
-      const double fs = fast_exp2((s.x - m) * a.inv_tau_s);
-      const double fm = fast_exp2((s.x - m) * a.inv_tau_m);
-      Ls += fs * s.y;
-      Lm += fm * s.z;
-      Vm += fm * s.w;
+      const float4 v = st[2 * c];
+      const float4 t = st[2 * c + 1];
+      if (v.x != kNegInf) {
+        const double fm = fast_exp2((v.x - m) * a.inv_tau_m);
+        Ls += static_cast<double>(fast_exp2((v.x - m) * a.inv_tau_s)) * v.y;
+        Lm += fm * v.z;
+        Vm += fm * v.z;
+      }
+      if (t.x != kNegInf) {
+        Ls += static_cast<double>(fast_exp2((t.x - m) * a.inv_tau_s)) * t.w;
+        Lm += static_cast<double>(fast_exp2((t.x - m) * a.inv_tau_m)) * t.z;
+      }
     }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
@@ -72,18 +79,27 @@ __global__ __launch_bounds__(256) void mass_finalize_kernel(const MassArgs a) {
 }
 
 // S_i = (1/Hq) sum_h 2^((z_{h,i} - m_h) / tau_score) / Ls_h for every visual rank i.
-// grid = (ceil(max_vis / 256), B); consecutive threads read consecutive ranks.
+// grid = (ceil(max_vis / 256), B); consecutive threads take consecutive ranks,
+// whose logits sit at consecutive cache positions inside a segment.
 __global__ __launch_bounds__(256) void scores_kernel(const MassArgs a) {
   extern __shared__ float sh[];  // [Hq] max, [Hq] 1/Ls
   float* s_m = sh;
   float* s_inv = sh + a.Hq;
   __shared__ int s_nv;
+  __shared__ SegWalker s_w;  // walker at the segment holding this block's first rank
   const int b = blockIdx.y;
   const int tid = threadIdx.x;
+  const int rank0 = blockIdx.x * blockDim.x;
   if (tid == 0) {
     const int L = clamp_len(a.seq_len[b], a.max_seq_len);
-    const int nv = count_visual(a.seg_off, a.seg, b, L);
+    const int o0 = a.seg_off[b];
+    SegWalker w;
+    w.start(a.seg + 2 * static_cast<long>(o0), a.seg_off[b + 1] - o0, L);
+    SegWalker t = w;
+    const int nv = t.total();
     s_nv = nv < a.max_vis ? nv : a.max_vis;
+    while (w.s < w.nseg && w.rank + (w.en - w.st) <= rank0) w.next();
+    s_w = w;
   }
   for (int h = tid; h < a.Hq; h += blockDim.x) {
     const float* hs = a.head + (static_cast<size_t>(b) * a.Hq + h) * 2;
@@ -91,11 +107,15 @@ __global__ __launch_bounds__(256) void scores_kernel(const MassArgs a) {
     s_inv[h] = hs[1] > 0.f ? 1.0f / hs[1] : 0.f;
   }
   __syncthreads();
-  const int i = blockIdx.x * blockDim.x + tid;
+  const int i = rank0 + tid;
   if (i >= s_nv) return;
-  const float* z = a.zs + static_cast<size_t>(b) * a.Hq * a.max_vis + i;
+  SegWalker w = s_w;
+  while (w.s < w.nseg && w.rank + (w.en - w.st) <= i) w.next();
+  const int pos = w.st + (i - w.rank);
+  const float* z = a.zs + static_cast<size_t>(b) * a.Hq * a.zs_stride + pos;
   float s = 0.f;
-  for (int h = 0; h < a.Hq; ++h) s += fast_exp2((z[static_cast<size_t>(h) * a.max_vis] - s_m[h]) * a.inv_tau_s) * s_inv[h];
+  for (int h = 0; h < a.Hq; ++h)
+    s += fast_exp2((z[static_cast<size_t>(h) * a.zs_stride] - s_m[h]) * a.inv_tau_s) * s_inv[h];
   a.scores[static_cast<size_t>(b) * a.max_vis + i] = s / static_cast<float>(a.Hq);
 }
 

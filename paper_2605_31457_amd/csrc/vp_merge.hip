@@ -1,43 +1,52 @@
 // Split-K reduction of the pruned attention (Sec. 4.1/4.2): merges the text
-// partials of the context pass (one per cache chunk) and the kept-row partials
+// partials of the context pass (one per context-pass part) and the kept-row partials
 // (one per split of the kept list) of every (sequence, query head):
 //   out = sum_i 2^(m_i - M) acc_i / sum_i 2^(m_i - M) l_i,  M = max_i m_i,
 // over the partials with l_i > 0; an empty context gives zeros.
-// grid = (Hq, B), one thread per output dimension.
+// grid = (Hq, B); 256 threads = (D/4 float4 columns) x R partial lanes, so the
+// partials are read in parallel (R at a time, each row as coalesced float4s)
+// rather than one after another.
 #include "vp_common.h"
 #include "vp_internal.h"
 
 namespace vp {
 namespace {
 
+constexpr int kMergeThreads = 256;
+
 template <int D>
-__global__ __launch_bounds__(D) void merge_kernel(const MergeArgs a) {
-  __shared__ float s_w[D];   // weight 2^(m_i - M) of each partial of the current block
-  __shared__ float s_red[D / 64];
+__global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a) {
+  constexpr int COLS = D / 4;                // float4 columns of a partial
+  constexpr int R = kMergeThreads / COLS;    // partials in flight per step
+  __shared__ float s_red[kMergeThreads / 64];
+  __shared__ float4 s_num[R][COLS];
+  __shared__ float s_den[R];
   const int h = blockIdx.x;
   const int b = blockIdx.y;
-  const int dim = threadIdx.x;
-  const int lane = dim & 63;
-  const int wid = dim >> 6;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wid = tid >> 6;
+  const int col = tid % COLS;
+  const int r = tid / COLS;
   const int L = clamp_len(a.seq_len[b], a.max_seq_len);
-  const int nc = (L + a.chunk - 1) / a.chunk;
+  const int nc = parts_used(L, a.nparts);
   int kb = a.kk[b];
   kb = kb < 0 ? 0 : (kb > a.k_cap ? a.k_cap : kb);
   const int ns = L > 0 ? (kb + a.split - 1) / a.split : 0;
   const int np = nc + ns;
   const size_t bh = static_cast<size_t>(b) * a.Hq + h;
-  const float* st = a.stats + bh * a.nchunk * 8;
+  const float* st = a.stats + bh * a.nparts * 8;
   const float* ks = a.kstats + bh * a.nsplit * 2;
-  const float* ac = a.acc + bh * a.nchunk * D + dim;
-  const float* ka = a.kacc + bh * a.nsplit * D + dim;
-  // (max, sum) of partial i: text chunk i < nc, else kept split i - nc
+  const float4* ac = reinterpret_cast<const float4*>(a.acc + bh * a.nparts * D) + col;
+  const float4* ka = reinterpret_cast<const float4*>(a.kacc + bh * a.nsplit * D) + col;
+  // (max, sum) of partial i: text part i < nc, else kept split i - nc
   auto ml = [&](int i) -> float2 {
     return i < nc ? *reinterpret_cast<const float2*>(st + i * 8 + 4)
                   : *reinterpret_cast<const float2*>(ks + (i - nc) * 2);
   };
 
   float M = kNegInf;
-  for (int i = dim; i < np; i += D) {
+  for (int i = tid; i < np; i += kMergeThreads) {
     const float2 v = ml(i);
     if (v.y > 0.f) M = fmaxf(M, v.x);
   }
@@ -47,37 +56,50 @@ __global__ __launch_bounds__(D) void merge_kernel(const MergeArgs a) {
   __syncthreads();
   M = s_red[0];
 #pragma unroll
-  for (int v = 1; v < D / 64; ++v) M = fmaxf(M, s_red[v]);
+  for (int v = 1; v < kMergeThreads / 64; ++v) M = fmaxf(M, s_red[v]);
 
-  float num = 0.f, den = 0.f;
-  for (int base = 0; base < np; base += D) {
-    __syncthreads();
-    {
-      const int i = base + dim;
-      float wgt = 0.f;
-      if (i < np) {
-        const float2 v = ml(i);
-        wgt = v.y > 0.f ? fast_exp2(v.x - M) : 0.f;
-      }
-      s_w[dim] = wgt;
+  float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+  float den = 0.f;
+#pragma unroll 4
+  for (int i = r; i < np; i += R) {
+    const float2 v = ml(i);
+    const float w = v.y > 0.f ? fast_exp2(v.x - M) : 0.f;
+    const float4 x = i < nc ? ac[static_cast<size_t>(i) * COLS] : ka[static_cast<size_t>(i - nc) * COLS];
+    den += w * v.y;
+    num.x += w * x.x;
+    num.y += w * x.y;
+    num.z += w * x.z;
+    num.w += w * x.w;
+  }
+  s_num[r][col] = num;
+  if (col == 0) s_den[r] = den;
+  __syncthreads();
+  if (r == 0) {
+    float dd = 0.f;
+    float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      const float4 x = s_num[j][col];
+      o.x += x.x;
+      o.y += x.y;
+      o.z += x.z;
+      o.w += x.w;
+      dd += s_den[j];
     }
-    __syncthreads();
-    const int cnt = min(D, np - base);
-    for (int j = 0; j < cnt; ++j) {
-      const float wgt = s_w[j];
-      if (wgt == 0.f) continue;
-      const int i = base + j;
-      const float l = i < nc ? st[i * 8 + 5] : ks[(i - nc) * 2 + 1];
-      const float v = i < nc ? ac[static_cast<size_t>(i) * D] : ka[static_cast<size_t>(i - nc) * D];
-      den += wgt * l;
-      num += wgt * v;
+    const float inv = dd > 0.f ? 1.0f / dd : 0.f;
+    o.x *= inv;
+    o.y *= inv;
+    o.z *= inv;
+    o.w *= inv;
+    if (a.dtype == VP_BF16) {
+      uint2 packed;
+      packed.x = f32_to_bf16_bits(o.x) | (static_cast<uint32_t>(f32_to_bf16_bits(o.y)) << 16);
+      packed.y = f32_to_bf16_bits(o.z) | (static_cast<uint32_t>(f32_to_bf16_bits(o.w)) << 16);
+      reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + bh * D)[col] = packed;
+    } else {
+      reinterpret_cast<float4*>(static_cast<float*>(a.out) + bh * D)[col] = o;
     }
   }
-  const float o = den > 0.f ? num / den : 0.f;
-  if (a.dtype == VP_BF16)
-    static_cast<uint16_t*>(a.out)[bh * D + dim] = f32_to_bf16_bits(o);
-  else
-    static_cast<float*>(a.out)[bh * D + dim] = o;
 }
 
 }  // namespace
@@ -85,9 +107,9 @@ __global__ __launch_bounds__(D) void merge_kernel(const MergeArgs a) {
 hipError_t launch_merge(const MergeArgs& a, int head_dim, hipStream_t st) {
   const dim3 grid(a.Hq, a.B);
   if (head_dim == 128)
-    hipLaunchKernelGGL(merge_kernel<128>, grid, dim3(128), 0, st, a);
+    hipLaunchKernelGGL(merge_kernel<128>, grid, dim3(kMergeThreads), 0, st, a);
   else if (head_dim == 64)
-    hipLaunchKernelGGL(merge_kernel<64>, grid, dim3(64), 0, st, a);
+    hipLaunchKernelGGL(merge_kernel<64>, grid, dim3(kMergeThreads), 0, st, a);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
