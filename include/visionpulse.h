@@ -139,17 +139,22 @@ vp_status vp_visual_mass(const vp_shape* shape, const vp_layout* layout, const v
                          void* workspace, size_t workspace_bytes, void* stream);
 
 /*
- * vp_visual_mass_timed -- vp_visual_mass that also records two caller-created
- * HIP events (hipEvent_t, may be NULL) on `stream` immediately before and
- * after the launch of its streaming pass over the cache, so a profiler or
- * benchmark can time that kernel alone with hipEventElapsedTime. Results are
- * identical to vp_visual_mass.
+ * vp_visual_mass_timed -- vp_visual_mass that also records caller-created HIP
+ * events (hipEvent_t) on `stream` between its kernel launches, so a profiler or
+ * benchmark can time each kernel alone with hipEventElapsedTime. events[i],
+ * i < n_events (at most VP_MASS_EVENTS; NULL entries are skipped), is recorded
+ *   [0] before the visual pass      [1] after it, before the text pass
+ *   [2] after the text pass         [3] after the mass reduction
+ *   [4] after the scores kernel.
+ * events may be NULL when n_events is 0. Results are identical to
+ * vp_visual_mass. VP_ERR_RANGE if n_events is outside [0, VP_MASS_EVENTS].
  */
+#define VP_MASS_EVENTS 5
 vp_status vp_visual_mass_timed(const vp_shape* shape, const vp_layout* layout, const vp_params* params,
                                const void* q, const void* K, const void* V,
                                float* mass_head, float* mass_seq, float* scores,
                                void* workspace, size_t workspace_bytes, void* stream,
-                               void* ev_pass_begin, void* ev_pass_end);
+                               void* const* events, int32_t n_events);
 
 /*
  * vp_budget -- Eq. (7): K_t = M_vis,max * N_v rounded up, clamped to

@@ -220,8 +220,10 @@ int32_t vp_budget_host(double m_max, int32_t n_vis, const vp_params* params) {
 vp_status vp_visual_mass_timed(const vp_shape* shape, const vp_layout* layout, const vp_params* params,
                                const void* q, const void* K, const void* V, float* mass_head, float* mass_seq,
                                float* scores, void* workspace, size_t workspace_bytes, void* stream,
-                               void* ev_pass_begin, void* ev_pass_end) {
+                               void* const* events, int32_t n_events) {
   g_last_error.clear();
+  if (n_events < 0 || n_events > VP_MASS_EVENTS) return fail(VP_ERR_RANGE, "n_events %d outside [0, %d]", n_events, VP_MASS_EVENTS);
+  if (n_events > 0 && !events) return fail(VP_ERR_NULL, "events is NULL with n_events %d", n_events);
   if (vp_status e = check_shape(shape)) return e;
   if (vp_status e = check_layout(layout)) return e;
   if (vp_status e = check_params(params)) return e;
@@ -232,14 +234,16 @@ vp_status vp_visual_mass_timed(const vp_shape* shape, const vp_layout* layout, c
   hipStream_t st = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
   AttendArgs a = attend_args(shape, layout, params, plan, ws, q, K, V);
-  if (ev_pass_begin)
-    if (hipError_t e = hipEventRecord(static_cast<hipEvent_t>(ev_pass_begin), st)) return hip_fail(e, "event record");
+  auto mark = [&](int i) -> hipError_t {
+    return (i < n_events && events[i]) ? hipEventRecord(static_cast<hipEvent_t>(events[i]), st) : hipSuccess;
+  };
+  if (hipError_t e = mark(0)) return hip_fail(e, "event record");
   if (hipError_t e = launch_attend(a, MODE_VIS, shape->dtype, shape->head_dim, st))
     return hip_fail(e, "visual pass launch");
+  if (hipError_t e = mark(1)) return hip_fail(e, "event record");
   if (hipError_t e = launch_attend(a, V ? MODE_TEXT_BOTH : MODE_TEXT_STATS, shape->dtype, shape->head_dim, st))
     return hip_fail(e, "text pass launch");
-  if (ev_pass_end)
-    if (hipError_t e = hipEventRecord(static_cast<hipEvent_t>(ev_pass_end), st)) return hip_fail(e, "event record");
+  if (hipError_t e = mark(2)) return hip_fail(e, "event record");
   MassArgs m{};
   m.seq_len = layout->seq_len;
   m.seg_off = layout->vis_seg_off;
@@ -259,7 +263,9 @@ vp_status vp_visual_mass_timed(const vp_shape* shape, const vp_layout* layout, c
   m.mass_seq = mass_seq;
   m.scores = scores;
   if (hipError_t e = launch_mass_finalize(m, st)) return hip_fail(e, "mass finalize launch");
+  if (hipError_t e = mark(3)) return hip_fail(e, "event record");
   if (hipError_t e = launch_scores(m, st)) return hip_fail(e, "scores launch");
+  if (hipError_t e = mark(4)) return hip_fail(e, "event record");
   return VP_OK;
 }
 
@@ -267,7 +273,7 @@ vp_status vp_visual_mass(const vp_shape* shape, const vp_layout* layout, const v
                          const void* K, const void* V, float* mass_head, float* mass_seq, float* scores,
                          void* workspace, size_t workspace_bytes, void* stream) {
   return vp_visual_mass_timed(shape, layout, params, q, K, V, mass_head, mass_seq, scores, workspace,
-                              workspace_bytes, stream, nullptr, nullptr);
+                              workspace_bytes, stream, nullptr, 0);
 }
 
 vp_status vp_budget(const vp_shape* shape, const vp_layout* layout, const vp_params* params, const float* mass_seq,

@@ -60,8 +60,8 @@ def lib() -> ctypes.CDLL:
             "vp_last_error": ([], ctypes.c_char_p),
             "vp_workspace_size": ([P(vp_shape), P(S)], ctypes.c_int),
             "vp_visual_mass": ([P(vp_shape), P(vp_layout), P(vp_params), V, V, V, V, V, V, V, S, V], ctypes.c_int),
-            "vp_visual_mass_timed": ([P(vp_shape), P(vp_layout), P(vp_params), V, V, V, V, V, V, V, S, V, V, V],
-                                     ctypes.c_int),
+            "vp_visual_mass_timed": ([P(vp_shape), P(vp_layout), P(vp_params), V, V, V, V, V, V, V, S, V,
+                                      ctypes.POINTER(V), ctypes.c_int32], ctypes.c_int),
             "vp_budget": ([P(vp_shape), P(vp_layout), P(vp_params), V, V, V], ctypes.c_int),
             "vp_select_topk": ([P(vp_shape), P(vp_layout), V, V, V, V], ctypes.c_int),
             "vp_sparse_decode_attn": ([P(vp_shape), P(vp_layout), P(vp_params), V, V, V, V, V, V,
@@ -114,13 +114,20 @@ def vp_visual_mass(shape, layout, params, q, K, V, mass_head, mass_seq, scores, 
         _p(mass_head), _p(mass_seq), _p(scores), _p(workspace), nbytes, _stream(stream)))
 
 
+VP_MASS_EVENTS = 5
+
+
 def vp_visual_mass_timed(shape, layout, params, q, K, V, mass_head, mass_seq, scores, workspace,
-                         workspace_bytes=None, stream=None, ev_pass_begin=None, ev_pass_end=None):
+                         workspace_bytes=None, stream=None, events=()):
+    """events: up to VP_MASS_EVENTS hipEvent_t handles (None entries skipped),
+    recorded before/between/after the call's kernel launches."""
     nbytes = workspace.numel() * workspace.element_size() if workspace_bytes is None else workspace_bytes
+    n = len(events)
+    arr = (ctypes.c_void_p * max(n, 1))(*[e for e in events]) if n else None
     _check("vp_visual_mass_timed", lib().vp_visual_mass_timed(
         ctypes.byref(shape), ctypes.byref(layout), ctypes.byref(params), _p(q), _p(K), _p(V),
         _p(mass_head), _p(mass_seq), _p(scores), _p(workspace), nbytes, _stream(stream),
-        ev_pass_begin, ev_pass_end))
+        arr, n))
 
 
 def vp_budget(shape, layout, params, mass_seq, k, stream=None):

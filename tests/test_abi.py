@@ -109,7 +109,20 @@ def test_calls_reject_nulls_and_bad_params_before_launch(L):
         vp.vp_sparse_decode_attn(s, lay, p, fake, fake, fake, fake, fake, fake, 8, fake, ws_bytes, 0)
     with pytest.raises(vp.VPError, match="VP_ERR_SHAPE"):
         vp.vp_sparse_decode_attn(s, lay, p, fake + 2, fake, fake, fake, fake, fake, 0, fake, ws_bytes, 0)
+    with pytest.raises(vp.VPError, match="VP_ERR_RANGE"):
+        vp.vp_visual_mass_timed(s, lay, p, fake, fake, None, fake, fake, fake, fake, ws_bytes, 0,
+                                events=[None] * (vp.VP_MASS_EVENTS + 1))
+    rc = L.vp_visual_mass_timed(ctypes.byref(s), ctypes.byref(lay), ctypes.byref(p), fake, fake, None, fake, fake,
+                                fake, fake, ws_bytes, None, None, 2)
+    assert L.vp_status_string(rc) == b"VP_ERR_NULL"
     assert "workspace" in L.vp_last_error().decode() or L.vp_last_error().decode() != ""
+
+
+def test_header_constants_match_binding():
+    text = open(HEADER).read()
+    consts = dict(re.findall(r"#define\s+(VP_[A-Z_]+)\s+(\d+)", text))
+    assert int(consts["VP_MASS_EVENTS"]) == vp.VP_MASS_EVENTS
+    assert int(consts["VP_ATTN_TEXT_FROM_WORKSPACE"]) == vp.VP_ATTN_TEXT_FROM_WORKSPACE
 
 
 def test_status_strings(L):
