@@ -161,7 +161,11 @@ Plan make_plan(const vp_shape& s) {
   p.nparts = static_cast<int>(parts);
   // Kept pass: 64 rows (two tiles) per work-group, or 32 when that leaves
   // fewer than 1024 work-groups.
+#ifdef VP_KEPT_SPLIT
+  p.split = VP_KEPT_SPLIT;
+#else
   p.split = static_cast<int64_t>(s.batch) * s.n_kv_heads * ((s.k_cap + 63) / 64) >= 1024 ? 64 : 32;
+#endif
   p.nsplit = (s.k_cap + p.split - 1) / p.split;
   const size_t B = s.batch, Hq = s.n_q_heads, d = s.head_dim;
   p.zs_stride = ((s.max_seq_len + 31) / 32) * 32;

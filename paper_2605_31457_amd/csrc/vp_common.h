@@ -53,7 +53,7 @@ struct SegWalker {
 
   __device__ __forceinline__ void start(const int32_t* seg_, int nseg_, int L_) {
     seg = seg_;
-    nseg = nseg_ < 0 ? 0 : nseg_;
+    nseg = nseg_ < 0 ? 0 : (nseg_ > 256 ? 256 : nseg_);  // at most 256 segments are read
     L = L_;
     s = -1;
     st = 0;
@@ -92,6 +92,95 @@ struct SegWalker {
 };
 
 __device__ __forceinline__ int clamp_len(int L, int cap) { return L < 0 ? 0 : (L > cap ? cap : L); }
+
+constexpr int kMaxSegs = 256;  // visual segments read per sequence
+
+// The visual segments of one sequence in LDS, clipped exactly as SegWalker
+// clips them: segment s covers positions [st[s], en[s]) and visual ranks
+// [rk[s], rk[s + 1]); rk[n] is the sequence's visual count.
+struct SegTable {
+  int st[kMaxSegs];
+  int en[kMaxSegs];
+  int rk[kMaxSegs + 1];
+  int n;
+};
+
+// Fills `t` with one wave (lane = 0..63, every lane calls) in two rounds of
+// independent loads instead of one dependent load per segment. SegWalker's
+// clipping unrolls to prefix scans: with a_s = clamp(start_s, 0, L) and
+// e_s = clamp(start_s + max(len_s, 0), 0, L),
+//   en_s = max(0, max_{s' <= s} max(a_s', e_s')),  st_s = max(a_s, en_{s-1}).
+// The caller synchronises before reading `t`.
+__device__ __forceinline__ void load_segments(SegTable& t, const int32_t* seg, int nseg, int L, int lane) {
+  constexpr int PER = kMaxSegs / 64;
+  nseg = nseg < 0 ? 0 : (nseg > kMaxSegs ? kMaxSegs : nseg);
+  int a[PER], m[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int s = PER * lane + j;
+    a[j] = 0;
+    m[j] = 0;
+    if (s < nseg) {
+      const long st = seg[2 * s];
+      const long ln = seg[2 * s + 1];
+      const long e = st + (ln > 0 ? ln : 0);
+      a[j] = static_cast<int>(st < 0 ? 0 : (st > L ? L : st));
+      const int ce = static_cast<int>(e < 0 ? 0 : (e > L ? L : e));
+      m[j] = a[j] > ce ? a[j] : ce;
+    }
+  }
+  // exclusive prefix max of the lane maxima
+  int lm = 0;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) lm = m[j] > lm ? m[j] : lm;
+  int incl = lm;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int v = __shfl_up(incl, off);
+    if (lane >= off) incl = v > incl ? v : incl;
+  }
+  int prev = __shfl_up(incl, 1);
+  prev = lane == 0 ? 0 : prev;
+  int st[PER], en[PER], len = 0;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    st[j] = a[j] > prev ? a[j] : prev;
+    en[j] = m[j] > prev ? m[j] : prev;
+    prev = en[j];
+    if (PER * lane + j < nseg) len += en[j] - st[j];
+  }
+  // exclusive prefix sum of the lane lengths
+  int rinc = len;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int v = __shfl_up(rinc, off);
+    if (lane >= off) rinc += v;
+  }
+  int r = rinc - len;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const int s = PER * lane + j;
+    if (s < nseg) {
+      t.st[s] = st[j];
+      t.en[s] = en[j];
+      t.rk[s] = r;
+      r += en[j] - st[j];
+    }
+  }
+  if (lane == 63) t.rk[nseg] = rinc;
+  if (lane == 0) t.n = nseg;
+}
+
+// position of visual rank r (0 <= r < t.rk[t.n]): binary search on the ranks
+__device__ __forceinline__ int rank_to_pos(const SegTable& t, int r) {
+  int lo = 0, hi = t.n;  // invariant: rk[lo] <= r < rk[hi]
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (t.rk[mid] <= r) lo = mid;
+    else hi = mid;
+  }
+  return t.st[lo] + (r - t.rk[lo]);
+}
 
 // visual-token count of sequence b under the clipping rules of SegWalker
 __device__ __forceinline__ int count_visual(const int32_t* seg_off, const int32_t* seg, int b, int L) {

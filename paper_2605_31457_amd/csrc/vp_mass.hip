@@ -7,74 +7,81 @@
 namespace vp {
 namespace {
 
-// One work-group per sequence, one wave per head (lanes over parts): merges
-// the per-part statistics of every head (visual rows and text rows are kept
-// apart by the context pass; max-shifted sums, combined in double with
-// fixed-order wave reductions), writes m^{vis}_{t,h}, the head mean M_vis and
-// head max M_vis,max, and the per-head (max, score normaliser) the scores
-// kernel needs.
-__global__ __launch_bounds__(256) void mass_finalize_kernel(const MassArgs a) {
-  constexpr int kWaves = 4;
+constexpr int kFinThreads = 512;
+
+// One work-group per sequence; every head gets a group of `lph` lanes (a power
+// of two, lph * Hq <= 512 when possible, so all heads reduce at once) that
+// strides over the parts. Merges the per-part statistics of the visual and
+// text rows (kept apart by the context pass) onto the head's maximum in
+// double, with fixed-order reductions; writes m^{vis}_{t,h}, the per-head
+// (max, Eq. (2) normaliser) for the scores, and the head mean M_vis and head
+// max M_vis,max of Sec. 4.3.
+__global__ __launch_bounds__(kFinThreads) void mass_finalize_kernel(const MassArgs a) {
+  __shared__ double s_mass[kFinThreads];
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wid = tid >> 6;
   const int L = clamp_len(a.seq_len[b], a.max_seq_len);
   const int nv = parts_used(L, a.nparts);
-  double msum = 0.0;
-  double mmax = 0.0;
-  for (int h = wid; h < a.Hq; h += kWaves) {
+  int lph = 64;
+  while (lph > 1 && lph * a.Hq > kFinThreads) lph >>= 1;
+  const int hpr = kFinThreads / lph;  // heads per round
+  const int sub = tid % lph;
+  double msum = 0.0, mmax = 0.0;
+  for (int h0 = 0; h0 < a.Hq; h0 += hpr) {
+    const int h = h0 + tid / lph;
+    const bool on = h < a.Hq;
     // per part: [0] visual {m, Ls, Lm, -}, [1] text {m, l, Lm, Ls}
-    const float4* st = reinterpret_cast<const float4*>(a.stats + (static_cast<size_t>(b) * a.Hq + h) * a.nparts * 8);
+    const float4* st =
+        reinterpret_cast<const float4*>(a.stats + (static_cast<size_t>(b) * a.Hq + (on ? h : 0)) * a.nparts * 8);
     float m = kNegInf;
-    for (int c = lane; c < nv; c += 64) m = fmaxf(m, fmaxf(st[2 * c].x, st[2 * c + 1].x));
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+    if (on) {
+#pragma unroll 4
+      for (int c = sub; c < nv; c += lph) m = fmaxf(m, fmaxf(st[2 * c].x, st[2 * c + 1].x));
+    }
+    for (int off = 1; off < lph; off <<= 1) m = fmaxf(m, __shfl_xor(m, off));
     double Ls = 0.0, Lm = 0.0, Vm = 0.0;
-    for (int c = lane; c < nv; c += 64) {
-      const float4 v = st[2 * c];
-      const float4 t = st[2 * c + 1];
-      if (v.x != kNegInf) {
-        const double fm = fast_exp2((v.x - m) * a.inv_tau_m);
-        Ls += static_cast<double>(fast_exp2((v.x - m) * a.inv_tau_s)) * v.y;
-        Lm += fm * v.z;
-        Vm += fm * v.z;
-      }
-      if (t.x != kNegInf) {
-        Ls += static_cast<double>(fast_exp2((t.x - m) * a.inv_tau_s)) * t.w;
-        Lm += static_cast<double>(fast_exp2((t.x - m) * a.inv_tau_m)) * t.z;
+    if (on) {
+#pragma unroll 4
+      for (int c = sub; c < nv; c += lph) {
+        const float4 v = st[2 * c];
+        const float4 t = st[2 * c + 1];
+        if (v.x != kNegInf) {
+          const double fm = fast_exp2((v.x - m) * a.inv_tau_m);
+          Ls += static_cast<double>(fast_exp2((v.x - m) * a.inv_tau_s)) * v.y;
+          Lm += fm * v.z;
+          Vm += fm * v.z;
+        }
+        if (t.x != kNegInf) {
+          Ls += static_cast<double>(fast_exp2((t.x - m) * a.inv_tau_s)) * t.w;
+          Lm += static_cast<double>(fast_exp2((t.x - m) * a.inv_tau_m)) * t.z;
+        }
       }
     }
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) {
+    for (int off = 1; off < lph; off <<= 1) {
       Ls += __shfl_xor(Ls, off);
       Lm += __shfl_xor(Lm, off);
       Vm += __shfl_xor(Vm, off);
     }
     const double mass = Lm > 0.0 ? Vm / Lm : 0.0;
-    if (lane == 0) {
+    if (on && sub == 0) {
       a.mass_head[static_cast<size_t>(b) * a.Hq + h] = static_cast<float>(mass);
       *reinterpret_cast<float2*>(a.head + (static_cast<size_t>(b) * a.Hq + h) * 2) =
           make_float2(m, static_cast<float>(Ls));
+      s_mass[tid / lph] = mass;
     }
-    msum += mass;
-    mmax = mass > mmax ? mass : mmax;
+    __syncthreads();
+    if (tid == 0) {
+      const int nh = min(hpr, a.Hq - h0);
+      for (int i = 0; i < nh; ++i) {
+        msum += s_mass[i];
+        mmax = s_mass[i] > mmax ? s_mass[i] : mmax;
+      }
+    }
+    __syncthreads();
   }
-  __shared__ double s_sum[kWaves];
-  __shared__ double s_max[kWaves];
-  if (lane == 0) {
-    s_sum[wid] = msum;
-    s_max[wid] = mmax;
-  }
-  __syncthreads();
   if (tid == 0) {
-    double t = 0.0, mx = 0.0;
-    for (int v = 0; v < kWaves; ++v) {
-      t += s_sum[v];
-      mx = s_max[v] > mx ? s_max[v] : mx;
-    }
-    a.mass_seq[2 * b + 0] = static_cast<float>(t / a.Hq);
-    a.mass_seq[2 * b + 1] = static_cast<float>(mx);
+    a.mass_seq[2 * b + 0] = static_cast<float>(msum / a.Hq);
+    a.mass_seq[2 * b + 1] = static_cast<float>(mmax);
   }
 }
 
@@ -85,52 +92,55 @@ __global__ __launch_bounds__(256) void scores_kernel(const MassArgs a) {
   extern __shared__ float sh[];  // [Hq] max, [Hq] 1/Ls
   float* s_m = sh;
   float* s_inv = sh + a.Hq;
-  __shared__ int s_nv;
-  __shared__ SegWalker s_w;  // walker at the segment holding this block's first rank
+  __shared__ SegTable tab;
   const int b = blockIdx.y;
   const int tid = threadIdx.x;
-  const int rank0 = blockIdx.x * blockDim.x;
-  if (tid == 0) {
-    const int L = clamp_len(a.seq_len[b], a.max_seq_len);
-    const int o0 = a.seg_off[b];
-    SegWalker w;
-    w.start(a.seg + 2 * static_cast<long>(o0), a.seg_off[b + 1] - o0, L);
-    SegWalker t = w;
-    const int nv = t.total();
-    s_nv = nv < a.max_vis ? nv : a.max_vis;
-    while (w.s < w.nseg && w.rank + (w.en - w.st) <= rank0) w.next();
-    s_w = w;
-  }
+  const int L = clamp_len(a.seq_len[b], a.max_seq_len);
+  const int o0 = a.seg_off[b];
+  if (tid < 64) load_segments(tab, a.seg + 2 * static_cast<long>(o0), a.seg_off[b + 1] - o0, L, tid);
   for (int h = tid; h < a.Hq; h += blockDim.x) {
-    const float* hs = a.head + (static_cast<size_t>(b) * a.Hq + h) * 2;
-    s_m[h] = hs[0];
-    s_inv[h] = hs[1] > 0.f ? 1.0f / hs[1] : 0.f;
+    const float2 hs = *reinterpret_cast<const float2*>(a.head + (static_cast<size_t>(b) * a.Hq + h) * 2);
+    s_m[h] = hs.x;
+    s_inv[h] = hs.y > 0.f ? 1.0f / hs.y : 0.f;
   }
   __syncthreads();
-  const int i = rank0 + tid;
-  if (i >= s_nv) return;
-  SegWalker w = s_w;
-  while (w.s < w.nseg && w.rank + (w.en - w.st) <= i) w.next();
-  const int pos = w.st + (i - w.rank);
+  const int nv = min(tab.rk[tab.n], a.max_vis);
+  const int i = blockIdx.x * blockDim.x + tid;
+  if (i >= nv) return;
+  const int pos = rank_to_pos(tab, i);
   const float* z = a.zs + static_cast<size_t>(b) * a.Hq * a.zs_stride + pos;
+  // the Hq logits of this position, 16 loads in flight at a time
+  constexpr int kBatch = 16;
   float s = 0.f;
-  for (int h = 0; h < a.Hq; ++h)
-    s += fast_exp2((z[static_cast<size_t>(h) * a.zs_stride] - s_m[h]) * a.inv_tau_s) * s_inv[h];
+  for (int h0 = 0; h0 < a.Hq; h0 += kBatch) {
+    float zz[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j)
+      zz[j] = h0 + j < a.Hq ? z[static_cast<size_t>(h0 + j) * a.zs_stride] : 0.f;
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j)
+      if (h0 + j < a.Hq) s += fast_exp2((zz[j] - s_m[h0 + j]) * a.inv_tau_s) * s_inv[h0 + j];
+  }
   a.scores[static_cast<size_t>(b) * a.max_vis + i] = s / static_cast<float>(a.Hq);
 }
 
+// one wave per sequence: the visual count from the segment table, then Eq. (7)
 __global__ __launch_bounds__(64) void budget_kernel(const BudgetArgs a) {
-  const int b = blockIdx.x * blockDim.x + threadIdx.x;
-  if (b >= a.B) return;
+  __shared__ SegTable tab;
+  const int b = blockIdx.x;
+  const int lane = threadIdx.x;
   const int L = clamp_len(a.seq_len[b], a.max_seq_len);
-  const int nv = count_visual(a.seg_off, a.seg, b, L);
-  a.k[b] = budget_rule(static_cast<double>(a.mass_seq[2 * b + 1]), nv, a.r_lo_bp, a.r_hi_bp, a.clamp);
+  const int o0 = a.seg_off[b];
+  load_segments(tab, a.seg + 2 * static_cast<long>(o0), a.seg_off[b + 1] - o0, L, lane);
+  __syncthreads();
+  if (lane == 0)
+    a.k[b] = budget_rule(static_cast<double>(a.mass_seq[2 * b + 1]), tab.rk[tab.n], a.r_lo_bp, a.r_hi_bp, a.clamp);
 }
 
 }  // namespace
 
 hipError_t launch_mass_finalize(const MassArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(mass_finalize_kernel, dim3(a.B), dim3(256), 0, st, a);
+  hipLaunchKernelGGL(mass_finalize_kernel, dim3(a.B), dim3(kFinThreads), 0, st, a);
   return hipGetLastError();
 }
 
@@ -141,7 +151,7 @@ hipError_t launch_scores(const MassArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_budget(const BudgetArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(budget_kernel, dim3((a.B + 63) / 64), dim3(64), 0, st, a);
+  hipLaunchKernelGGL(budget_kernel, dim3(a.B), dim3(64), 0, st, a);
   return hipGetLastError();
 }
 

@@ -186,3 +186,45 @@ def test_sparse_attention_on_given_selection():
         rr = O.decode_step_sequence(w.q[0], w.K[0], w.V[0], 3358, w.segments[0], p, k_override=k_use)
         assert np.array_equal(rr.vis_idx, sel)
         np.testing.assert_allclose(got, rr.out, atol=2e-2, rtol=1e-2)
+
+
+def _clip_layout(L, segs):
+    """The documented reading of an unclean device layout: segments are taken in
+    order, each clipped to [end of the previous one, L); lengths < 0 count as 0."""
+    out, prev = [], 0
+    for a, n in segs:
+        lo = max(a, prev)
+        lo = 0 if lo < 0 else min(lo, L)
+        hi = a + max(n, 0)
+        hi = lo if hi < lo else min(hi, L)
+        if hi > lo:
+            out.append((lo, hi - lo))
+        prev = hi
+    return out
+
+
+def test_unclean_device_layout_is_clipped():
+    """Overlapping, unsorted, empty, negative and overrunning segments and a
+    length beyond capacity give exactly the results of the clipped layout."""
+    S_cap = 256
+    raw_lens = [300, 200]
+    raw_segs = [[(-5, 20), (10, 30), (35, 0), (30, 50), (250, 100)], [(150, -3), (100, 60), (40, 20)]]
+    lens = [min(n, S_cap) for n in raw_lens]
+    segs = [_clip_layout(L, s) for L, s in zip(lens, raw_segs)]
+    assert segs == [[(0, 15), (15, 25), (40, 40), (250, 6)], [(150, 10)]]
+    w = small_workload(seed=15, B=2, Hq=8, Hkv=2, d=64, lens=lens, segs=segs, S_cap=S_cap)
+    ref, _ = P.plant(w, P.params_of(w))
+    ds = S.DeviceStep(w)
+    off, seg = W.layout_arrays(raw_segs)
+    ds.seq_len = torch.tensor(raw_lens, dtype=torch.int32, device=ds.device)
+    ds.seg_off = torch.from_numpy(off).to(ds.device)
+    ds.seg = torch.from_numpy(seg.reshape(-1)).to(ds.device)
+    ds.layout = S.vp.vp_layout(seq_len=ds.seq_len.data_ptr(), vis_seg_off=ds.seg_off.data_ptr(),
+                               vis_seg=ds.seg.data_ptr())
+    ds.shape.max_segs = 5
+    _log(f"clipped layout: n_vis={[sum(n for _, n in s) for s in segs]} k={[ref[b].k for b in range(2)]}")
+    for fused in (True, False):
+        ds.run(fused=fused)
+        g = ds.results()
+        for b in range(2):
+            check_sequence(f"clipped fused={fused}", w, g, b, ref[b])
