@@ -1,19 +1,20 @@
 #!/usr/bin/env python3
 """Throughput of the VisionPulse per-decode-step path on one MI355X.
 
-One step = vp_visual_mass -> vp_budget -> vp_select_topk -> vp_sparse_decode_attn
-over the whole batch on one layer's KV cache (the anchor layer), with the text
-attention fused into the mass pass. Inputs are seeded synthetic tensors shaped
+One step = one vp_decode_step call (the results of vp_visual_mass ->
+vp_budget -> vp_select_topk -> vp_sparse_decode_attn, in fewer launches) over
+the whole batch on one layer's KV cache (the anchor layer); --calls times the
+four separate calls instead. Inputs are seeded synthetic tensors shaped
 like the paper's LMM decode workloads (paper_2605_31457_amd.workloads), resident
 in HBM before timing. To keep the 256 MB Infinity Cache from serving the cache
 reads, the step rotates over R distinct copies of the KV cache (R * KV bytes
 >= 1 GiB), as a real model's layers would.
 
 Prints one JSON line: steps/s, the roofline of the kernel that carries most of
-the step's bytes (the text pass: every text K and V row; HIP events recorded
-around each kernel launch of vp_visual_mass inside the timed steps give its
-duration, and that of the visual pass) and the fp64 reference timed on this
-host's cores.
+the step's bytes (the text pass: every text K and V row; HIP events that the
+step records between its launches, inside the timed steps, give its duration
+and those of the other phases) and the fp64 reference timed on this host's
+cores.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
 """
@@ -114,6 +115,7 @@ def main():
     ap.add_argument("--rotate", type=int, default=0, help="KV copies to rotate over (0: >= 1 GiB)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calls", action="store_true", help="time the four separate calls instead of vp_decode_step")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -150,18 +152,37 @@ def main():
     hip = Hip()
     stream = torch.cuda.current_stream()
     sp = stream.cuda_stream
-    NEV = 3  # before the visual pass, between the passes, after the text pass
-    evs_all = [[hip.event() for _ in range(NEV)] for _ in range(steps)]
+    # step events: [0] visual pass [1] text pass [2] tail [3] kept pass [4] merge [5].
+    # An event record costs a few microseconds of queue time, which is visible on
+    # small steps, so the timed steps record only the two around the text pass
+    # (the roofline kernel); the per-phase split comes from separate steps after.
+    NEV = vp.VP_STEP_EVENTS
+    evs_all = [[None, hip.event(), hip.event(), None, None, None] for _ in range(steps)]
+    n_phase = min(steps, 50)
+    evs_phase = [[hip.event() for _ in range(NEV)] for _ in range(n_phase)]
+    # argument arrays built ahead of the timed loop
+    arr_all = [vp.event_array(e) for e in evs_all]
+    arr_all3 = [vp.event_array(e[:3]) for e in evs_all]
+    arr_phase = [vp.event_array(e) for e in evs_phase]
+    arr_phase3 = [vp.event_array(e[:3]) for e in evs_phase]
     ev_t0, ev_t1 = hip.event(), hip.event()
 
-    def one_step(i, evs=()):
+    def one_step(i, evs=(), arr6=(), arr3=()):
         K, V = bufs[i % R]
+        if not args.calls:
+            vp.vp_decode_step(ds.shape, ds.layout, ds.params, ds.q, K, V, ds.mass_head, ds.mass_seq, ds.scores,
+                              ds.k, ds.vis_idx, ds.out, ds.ws, ds.ws_bytes, sp, events=arr6)
+            return
         vp.vp_visual_mass_timed(ds.shape, ds.layout, ds.params, ds.q, K, V, ds.mass_head, ds.mass_seq,
-                                ds.scores, ds.ws, ds.ws_bytes, sp, events=evs)
+                                ds.scores, ds.ws, ds.ws_bytes, sp, events=arr3)
         vp.vp_budget(ds.shape, ds.layout, ds.params, ds.mass_seq, ds.k, sp)
         vp.vp_select_topk(ds.shape, ds.layout, ds.scores, ds.k, ds.vis_idx, sp)
+        if evs and evs[3]:
+            hip.h.hipEventRecord(evs[3], sp)
         vp.vp_sparse_decode_attn(ds.shape, ds.layout, ds.params, ds.q, K, V, ds.vis_idx, ds.k, ds.out,
                                  vp.VP_ATTN_TEXT_FROM_WORKSPACE, ds.ws, ds.ws_bytes, sp)
+        if evs and evs[5]:
+            hip.h.hipEventRecord(evs[5], sp)
 
     for i in range(warmup):
         one_step(i)
@@ -171,13 +192,19 @@ def main():
     hip.h.hipEventRecord(ev_t0, sp)
     t0 = time.perf_counter()
     for i in range(steps):
-        one_step(warmup + i, evs_all[i])
+        one_step(warmup + i, evs_all[i], arr_all[i], arr_all3[i])
     hip.h.hipEventRecord(ev_t1, sp)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     gpu_ms = hip.elapsed_ms(ev_t0, ev_t1)
-    vis_ms = float(np.mean([hip.elapsed_ms(e[0], e[1]) for e in evs_all]))
     text_ms = float(np.mean([hip.elapsed_ms(e[1], e[2]) for e in evs_all]))
+    for i in range(n_phase):
+        one_step(warmup + steps + i, evs_phase[i], arr_phase[i], arr_phase3[i])
+    torch.cuda.synchronize()
+
+    def phase(i, j):
+        return float(np.mean([hip.elapsed_ms(e[i], e[j]) for e in evs_phase]))
+    vis_ms, tail_ms, attn_ms = phase(0, 1), phase(2, 3), phase(3, 5)
     assert np.array_equal(ds.k.cpu().numpy(), ks), "budget changed between warm-up and timed steps"
 
     nb = algorithmic_bytes(w, ks)
@@ -214,6 +241,9 @@ def main():
                      "avg_launch_ms": text_ms, "share_of_step": text_ms / ms_per_step},
         "visual_pass": {"achieved": nb["visual"] / (vis_ms * 1e-3) / 1e9, "unit": "GB/s",
                         "algorithmic_bytes_per_launch": nb["visual"], "avg_launch_ms": vis_ms},
+        "phases_ms": {"visual_pass": vis_ms, "text_pass": text_ms,
+                      "mass_budget_scores_topk": tail_ms, "kept_pass_and_merge": attn_ms},
+        "entry_point": "four calls" if args.calls else "vp_decode_step",
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the fp64 reference on the host", file=sys.stderr, flush=True)

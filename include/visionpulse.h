@@ -197,6 +197,33 @@ vp_status vp_sparse_decode_attn(const vp_shape* shape, const vp_layout* layout, 
                                 const int32_t* vis_idx, const int32_t* k, void* out, int32_t flags,
                                 void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * vp_decode_step -- one whole decode step (Sec. 4.1-4.3): the results of
+ *   vp_visual_mass(V) -> vp_budget -> vp_select_topk
+ *     -> vp_sparse_decode_attn(VP_ATTN_TEXT_FROM_WORKSPACE)
+ * on the same arguments, in fewer launches: where a sequence's visual tokens
+ * fit one work-group's LDS (max_vis up to ~30 K, n_q_heads <= 256) and the
+ * batch is small, the mass reduction, budget, scores and top-k of each
+ * sequence run in one work-group. All outputs are written as by the four
+ * calls (same arithmetic, same reduction order): mass_head [B, Hq],
+ * mass_seq [B, 2], scores [B, max_vis], k [B], vis_idx [B, k_cap],
+ * out [B, Hq, d]; V is required.
+ *
+ * events: optional caller-created hipEvent_t recorded on `stream`, i < n_events
+ * (at most VP_STEP_EVENTS; NULL entries skipped):
+ *   [0] before the visual pass   [1] before the text pass
+ *   [2] after the text pass      [3] before the kept-row pass
+ *   [4] before the merge         [5] after the merge.
+ * Errors as for the four calls; VP_ERR_RANGE if n_events is outside
+ * [0, VP_STEP_EVENTS]. The workspace must not be shared by concurrent calls.
+ */
+#define VP_STEP_EVENTS 6
+vp_status vp_decode_step(const vp_shape* shape, const vp_layout* layout, const vp_params* params,
+                         const void* q, const void* K, const void* V,
+                         float* mass_head, float* mass_seq, float* scores, int32_t* k, int32_t* vis_idx,
+                         void* out, void* workspace, size_t workspace_bytes, void* stream,
+                         void* const* events, int32_t n_events);
+
 /* Host mirror of vp_budget's rule for one sequence (pure; for callers that keep
  * the mass on the host). Returns -1 for invalid parameters. */
 int32_t vp_budget_host(double m_max, int32_t n_vis, const vp_params* params);

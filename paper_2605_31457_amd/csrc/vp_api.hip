@@ -146,6 +146,97 @@ AttendArgs attend_args(const vp_shape* s, const vp_layout* l, const vp_params* p
 #define VP_TARGET_PARTS 4096
 #endif
 
+MassArgs mass_args(const vp_shape* s, const vp_layout* l, const Plan& plan, const AttendArgs& a, char* ws,
+                   float* mass_head, float* mass_seq, float* scores) {
+  MassArgs m{};
+  m.seq_len = l->seq_len;
+  m.seg_off = l->vis_seg_off;
+  m.seg = l->vis_seg;
+  m.B = s->batch;
+  m.Hq = s->n_q_heads;
+  m.max_seq_len = s->max_seq_len;
+  m.max_vis = s->max_vis;
+  m.nparts = plan.nparts;
+  m.zs_stride = plan.zs_stride;
+  m.inv_tau_m = a.inv_tau_m;
+  m.inv_tau_s = a.inv_tau_s;
+  m.stats = a.stats;
+  m.zs = a.zs;
+  m.head = reinterpret_cast<float*>(ws + plan.head);
+  m.mass_head = mass_head;
+  m.mass_seq = mass_seq;
+  m.scores = scores;
+  return m;
+}
+
+BudgetArgs budget_args(const vp_shape* s, const vp_layout* l, const vp_params* p, const float* mass_seq, int32_t* k) {
+  BudgetArgs b{};
+  b.seq_len = l->seq_len;
+  b.seg_off = l->vis_seg_off;
+  b.seg = l->vis_seg;
+  b.B = s->batch;
+  b.max_seq_len = s->max_seq_len;
+  b.r_lo_bp = p->r_lo_bp;
+  b.r_hi_bp = p->r_hi_bp;
+  b.clamp = p->clamp;
+  b.mass_seq = mass_seq;
+  b.k = k;
+  return b;
+}
+
+TopkArgs topk_args(const vp_shape* s, const vp_layout* l, const float* scores, const int32_t* k, int32_t* vis_idx) {
+  TopkArgs t{};
+  t.seq_len = l->seq_len;
+  t.seg_off = l->vis_seg_off;
+  t.seg = l->vis_seg;
+  t.B = s->batch;
+  t.max_seq_len = s->max_seq_len;
+  t.max_vis = s->max_vis;
+  t.k_cap = s->k_cap;
+  t.scores = scores;
+  t.k = k;
+  t.vis_idx = vis_idx;
+  return t;
+}
+
+MergeArgs merge_args(const vp_shape* s, const vp_layout* l, const Plan& plan, const AttendArgs& a, const int32_t* k,
+                     void* out) {
+  MergeArgs m{};
+  m.seq_len = l->seq_len;
+  m.kk = k;
+  m.B = s->batch;
+  m.Hq = s->n_q_heads;
+  m.max_seq_len = s->max_seq_len;
+  m.k_cap = s->k_cap;
+  m.nparts = plan.nparts;
+  m.split = plan.split;
+  m.nsplit = plan.nsplit;
+  m.dtype = s->dtype;
+  m.stats = a.stats;
+  m.acc = a.acc;
+  m.kstats = a.kstats;
+  m.kacc = a.kacc;
+  m.out = out;
+  return m;
+}
+
+// The fused per-sequence tail (one work-group per sequence) replaces four
+// launches; it pays off while the batch's visual tokens are few enough that
+// one CU per sequence is not the bottleneck.
+#ifndef VP_TAIL_MAX_TOKENS
+#define VP_TAIL_MAX_TOKENS (1 << 17)
+#endif
+bool use_tail(const vp_shape* s) {
+  return tail_fits(s->n_q_heads, s->max_vis) &&
+         static_cast<int64_t>(s->batch) * s->max_vis <= static_cast<int64_t>(VP_TAIL_MAX_TOKENS);
+}
+
+vp_status check_budget_cap(const vp_shape* s, const vp_params* p) {
+  if (s->k_cap < max_budget(s, p))
+    return fail(VP_ERR_SHAPE, "k_cap %d < largest budget %d for max_vis %d", s->k_cap, max_budget(s, p), s->max_vis);
+  return VP_OK;
+}
+
 Plan make_plan(const vp_shape& s) {
   Plan p{};
   // Context pass: about VP_TARGET_PARTS one-wave work-groups in all, each
@@ -248,24 +339,7 @@ vp_status vp_visual_mass_timed(const vp_shape* shape, const vp_layout* layout, c
   if (hipError_t e = launch_attend(a, V ? MODE_TEXT_BOTH : MODE_TEXT_STATS, shape->dtype, shape->head_dim, st))
     return hip_fail(e, "text pass launch");
   if (hipError_t e = mark(2)) return hip_fail(e, "event record");
-  MassArgs m{};
-  m.seq_len = layout->seq_len;
-  m.seg_off = layout->vis_seg_off;
-  m.seg = layout->vis_seg;
-  m.B = shape->batch;
-  m.Hq = shape->n_q_heads;
-  m.max_seq_len = shape->max_seq_len;
-  m.max_vis = shape->max_vis;
-  m.nparts = plan.nparts;
-  m.zs_stride = plan.zs_stride;
-  m.inv_tau_m = a.inv_tau_m;
-  m.inv_tau_s = a.inv_tau_s;
-  m.stats = a.stats;
-  m.zs = a.zs;
-  m.head = reinterpret_cast<float*>(ws + plan.head);
-  m.mass_head = mass_head;
-  m.mass_seq = mass_seq;
-  m.scores = scores;
+  const MassArgs m = mass_args(shape, layout, plan, a, ws, mass_head, mass_seq, scores);
   if (hipError_t e = launch_mass_finalize(m, st)) return hip_fail(e, "mass finalize launch");
   if (hipError_t e = mark(3)) return hip_fail(e, "event record");
   if (hipError_t e = launch_scores(m, st)) return hip_fail(e, "scores launch");
@@ -287,21 +361,9 @@ vp_status vp_budget(const vp_shape* shape, const vp_layout* layout, const vp_par
   if (vp_status e = check_layout(layout)) return e;
   if (vp_status e = check_params(params)) return e;
   if (!mass_seq || !k) return fail(VP_ERR_NULL, "mass_seq and k required");
-  if (shape->k_cap < max_budget(shape, params))
-    return fail(VP_ERR_SHAPE, "k_cap %d < largest budget %d for max_vis %d", shape->k_cap, max_budget(shape, params),
-                shape->max_vis);
-  BudgetArgs b{};
-  b.seq_len = layout->seq_len;
-  b.seg_off = layout->vis_seg_off;
-  b.seg = layout->vis_seg;
-  b.B = shape->batch;
-  b.max_seq_len = shape->max_seq_len;
-  b.r_lo_bp = params->r_lo_bp;
-  b.r_hi_bp = params->r_hi_bp;
-  b.clamp = params->clamp;
-  b.mass_seq = mass_seq;
-  b.k = k;
-  if (hipError_t e = launch_budget(b, static_cast<hipStream_t>(stream))) return hip_fail(e, "budget launch");
+  if (vp_status e = check_budget_cap(shape, params)) return e;
+  if (hipError_t e = launch_budget(budget_args(shape, layout, params, mass_seq, k), static_cast<hipStream_t>(stream)))
+    return hip_fail(e, "budget launch");
   return VP_OK;
 }
 
@@ -311,18 +373,8 @@ vp_status vp_select_topk(const vp_shape* shape, const vp_layout* layout, const f
   if (vp_status e = check_shape(shape)) return e;
   if (vp_status e = check_layout(layout)) return e;
   if (!scores || !k || !vis_idx) return fail(VP_ERR_NULL, "scores, k, vis_idx required");
-  TopkArgs t{};
-  t.seq_len = layout->seq_len;
-  t.seg_off = layout->vis_seg_off;
-  t.seg = layout->vis_seg;
-  t.B = shape->batch;
-  t.max_seq_len = shape->max_seq_len;
-  t.max_vis = shape->max_vis;
-  t.k_cap = shape->k_cap;
-  t.scores = scores;
-  t.k = k;
-  t.vis_idx = vis_idx;
-  if (hipError_t e = launch_topk(t, static_cast<hipStream_t>(stream))) return hip_fail(e, "top-k launch");
+  if (hipError_t e = launch_topk(topk_args(shape, layout, scores, k, vis_idx), static_cast<hipStream_t>(stream)))
+    return hip_fail(e, "top-k launch");
   return VP_OK;
 }
 
@@ -350,23 +402,65 @@ vp_status vp_sparse_decode_attn(const vp_shape* shape, const vp_layout* layout, 
   }
   if (hipError_t e = launch_attend(a, MODE_KEPT, shape->dtype, shape->head_dim, st))
     return hip_fail(e, "kept pass launch");
-  MergeArgs m{};
-  m.seq_len = layout->seq_len;
-  m.kk = k;
-  m.B = shape->batch;
-  m.Hq = shape->n_q_heads;
-  m.max_seq_len = shape->max_seq_len;
-  m.k_cap = shape->k_cap;
-  m.nparts = plan.nparts;
-  m.split = plan.split;
-  m.nsplit = plan.nsplit;
-  m.dtype = shape->dtype;
-  m.stats = a.stats;
-  m.acc = a.acc;
-  m.kstats = a.kstats;
-  m.kacc = a.kacc;
-  m.out = out;
-  if (hipError_t e = launch_merge(m, shape->head_dim, st)) return hip_fail(e, "merge launch");
+  if (hipError_t e = launch_merge(merge_args(shape, layout, plan, a, k, out), shape->head_dim, st))
+    return hip_fail(e, "merge launch");
+  return VP_OK;
+}
+
+vp_status vp_decode_step(const vp_shape* shape, const vp_layout* layout, const vp_params* params, const void* q,
+                         const void* K, const void* V, float* mass_head, float* mass_seq, float* scores, int32_t* k,
+                         int32_t* vis_idx, void* out, void* workspace, size_t workspace_bytes, void* stream,
+                         void* const* events, int32_t n_events) {
+  g_last_error.clear();
+  if (n_events < 0 || n_events > VP_STEP_EVENTS)
+    return fail(VP_ERR_RANGE, "n_events %d outside [0, %d]", n_events, VP_STEP_EVENTS);
+  if (n_events > 0 && !events) return fail(VP_ERR_NULL, "events is NULL with n_events %d", n_events);
+  if (vp_status e = check_shape(shape)) return e;
+  if (vp_status e = check_layout(layout)) return e;
+  if (vp_status e = check_params(params)) return e;
+  if (!q || !K || !V || !mass_head || !mass_seq || !scores || !k || !vis_idx || !out)
+    return fail(VP_ERR_NULL, "q, K, V, mass_head, mass_seq, scores, k, vis_idx, out required");
+  if (!aligned16(q) || !aligned16(K) || !aligned16(V)) return fail(VP_ERR_SHAPE, "q, K, V must be 16-byte aligned");
+  if (vp_status e = check_budget_cap(shape, params)) return e;
+  Plan plan;
+  if (vp_status e = check_ws(shape, workspace, workspace_bytes, plan)) return e;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  char* ws = static_cast<char*>(workspace);
+  AttendArgs a = attend_args(shape, layout, params, plan, ws, q, K, V);
+  a.vis_idx = vis_idx;
+  a.kk = k;
+  auto mark = [&](int i) -> hipError_t {
+    return (i < n_events && events[i]) ? hipEventRecord(static_cast<hipEvent_t>(events[i]), st) : hipSuccess;
+  };
+  const int dt = shape->dtype, hd = shape->head_dim;
+  if (hipError_t e = mark(0)) return hip_fail(e, "event record");
+  if (hipError_t e = launch_attend(a, MODE_VIS, dt, hd, st)) return hip_fail(e, "visual pass launch");
+  if (hipError_t e = mark(1)) return hip_fail(e, "event record");
+  if (hipError_t e = launch_attend(a, MODE_TEXT_BOTH, dt, hd, st)) return hip_fail(e, "text pass launch");
+  if (hipError_t e = mark(2)) return hip_fail(e, "event record");
+  const MassArgs m = mass_args(shape, layout, plan, a, ws, mass_head, mass_seq, scores);
+  if (use_tail(shape)) {
+    TailArgs t{};
+    t.m = m;
+    t.r_lo_bp = params->r_lo_bp;
+    t.r_hi_bp = params->r_hi_bp;
+    t.clamp = params->clamp;
+    t.k_cap = shape->k_cap;
+    t.k = k;
+    t.vis_idx = vis_idx;
+    if (hipError_t e = launch_tail(t, st)) return hip_fail(e, "tail launch");
+  } else {
+    if (hipError_t e = launch_mass_finalize(m, st)) return hip_fail(e, "mass finalize launch");
+    if (hipError_t e = launch_scores(m, st)) return hip_fail(e, "scores launch");
+    if (hipError_t e = launch_budget(budget_args(shape, layout, params, mass_seq, k), st))
+      return hip_fail(e, "budget launch");
+    if (hipError_t e = launch_topk(topk_args(shape, layout, scores, k, vis_idx), st)) return hip_fail(e, "top-k launch");
+  }
+  if (hipError_t e = mark(3)) return hip_fail(e, "event record");
+  if (hipError_t e = launch_attend(a, MODE_KEPT, dt, hd, st)) return hip_fail(e, "kept pass launch");
+  if (hipError_t e = mark(4)) return hip_fail(e, "event record");
+  if (hipError_t e = launch_merge(merge_args(shape, layout, plan, a, k, out), hd, st)) return hip_fail(e, "merge launch");
+  if (hipError_t e = mark(5)) return hip_fail(e, "event record");
   return VP_OK;
 }
 

@@ -92,6 +92,19 @@ struct MassArgs {
 hipError_t launch_mass_finalize(const MassArgs& a, hipStream_t st);
 hipError_t launch_scores(const MassArgs& a, hipStream_t st);
 
+// per-sequence tail of a decode step (mass reduction, budget, scores, top-k)
+constexpr int kTailMaxHeads = 256;
+struct TailArgs {
+  MassArgs m;
+  int r_lo_bp, r_hi_bp, clamp;
+  int k_cap;
+  int32_t* k;
+  int32_t* vis_idx;
+};
+
+bool tail_fits(int n_q_heads, int max_vis);
+hipError_t launch_tail(const TailArgs& t, hipStream_t st);
+
 struct BudgetArgs {
   const int32_t* seq_len;
   const int32_t* seg_off;

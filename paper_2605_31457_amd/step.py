@@ -81,6 +81,11 @@ class DeviceStep:
                                  self.k, self.out, vp.VP_ATTN_TEXT_FROM_WORKSPACE if fused else 0,
                                  self.ws, self.ws_bytes, stream)
 
+    def decode_step(self, stream=None, events=()):
+        vp.vp_decode_step(self.shape, self.layout, self.params, self.q, self.K, self.V, self.mass_head,
+                          self.mass_seq, self.scores, self.k, self.vis_idx, self.out, self.ws, self.ws_bytes,
+                          stream, events)
+
     def run(self, fused=True, stream=None):
         self.visual_mass(fused, stream)
         self.budget(stream)

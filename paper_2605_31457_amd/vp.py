@@ -67,6 +67,8 @@ def lib() -> ctypes.CDLL:
             "vp_sparse_decode_attn": ([P(vp_shape), P(vp_layout), P(vp_params), V, V, V, V, V, V,
                                        ctypes.c_int32, V, S, V], ctypes.c_int),
             "vp_budget_host": ([ctypes.c_double, ctypes.c_int32, P(vp_params)], ctypes.c_int32),
+            "vp_decode_step": ([P(vp_shape), P(vp_layout), P(vp_params), V, V, V, V, V, V, V, V, V, V, S, V,
+                                ctypes.POINTER(V), ctypes.c_int32], ctypes.c_int),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -114,6 +116,18 @@ def vp_visual_mass(shape, layout, params, q, K, V, mass_head, mass_seq, scores, 
         _p(mass_head), _p(mass_seq), _p(scores), _p(workspace), nbytes, _stream(stream)))
 
 
+def event_array(events):
+    """(ctypes array of hipEvent_t, count) for an events argument: a sequence
+    of handles / None, or an array already built by this function (build it
+    ahead of a timed loop: constructing one costs tens of microseconds)."""
+    if isinstance(events, tuple) and len(events) == 2 and isinstance(events[0], ctypes.Array):
+        return events
+    n = len(events)
+    if n == 0:
+        return None, 0
+    return (ctypes.c_void_p * n)(*[e for e in events]), n
+
+
 VP_MASS_EVENTS = 5
 
 
@@ -122,12 +136,26 @@ def vp_visual_mass_timed(shape, layout, params, q, K, V, mass_head, mass_seq, sc
     """events: up to VP_MASS_EVENTS hipEvent_t handles (None entries skipped),
     recorded before/between/after the call's kernel launches."""
     nbytes = workspace.numel() * workspace.element_size() if workspace_bytes is None else workspace_bytes
-    n = len(events)
-    arr = (ctypes.c_void_p * max(n, 1))(*[e for e in events]) if n else None
+    arr, n = event_array(events)
     _check("vp_visual_mass_timed", lib().vp_visual_mass_timed(
         ctypes.byref(shape), ctypes.byref(layout), ctypes.byref(params), _p(q), _p(K), _p(V),
         _p(mass_head), _p(mass_seq), _p(scores), _p(workspace), nbytes, _stream(stream),
         arr, n))
+
+
+VP_STEP_EVENTS = 6
+
+
+def vp_decode_step(shape, layout, params, q, K, V, mass_head, mass_seq, scores, k, vis_idx, out, workspace,
+                   workspace_bytes=None, stream=None, events=()):
+    """One whole decode step (the four calls' results, fewer launches).
+    events: up to VP_STEP_EVENTS hipEvent_t handles (None entries skipped)."""
+    nbytes = workspace.numel() * workspace.element_size() if workspace_bytes is None else workspace_bytes
+    arr, n = event_array(events)
+    _check("vp_decode_step", lib().vp_decode_step(
+        ctypes.byref(shape), ctypes.byref(layout), ctypes.byref(params), _p(q), _p(K), _p(V),
+        _p(mass_head), _p(mass_seq), _p(scores), _p(k), _p(vis_idx), _p(out), _p(workspace), nbytes,
+        _stream(stream), arr, n))
 
 
 def vp_budget(shape, layout, params, mass_seq, k, stream=None):

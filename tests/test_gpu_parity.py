@@ -81,6 +81,52 @@ def test_small_shapes(name):
         _, g = _run(w, fused=fused)
         for b in range(w.B):
             check_sequence(f"{name} fused={fused}", w, g, b, ref[b])
+    _step_equals_calls(w, g)
+
+
+def _step_equals_calls(w, calls, ds=None, **kw):
+    """vp_decode_step gives exactly what the four calls give (same arithmetic and
+    reduction order), and so passes the same reference checks."""
+    ds = ds or S.DeviceStep(w, **kw)
+    ds.decode_step()
+    g = ds.results()
+    for key in ("mass_head", "mass_seq", "scores", "k", "vis_idx", "out"):
+        assert np.array_equal(g[key], calls[key]), key
+    return g
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_decode_step_config(cfg):
+    w = W.generate(cfg)
+    ref, _ = P.plant(w, P.params_of(w))
+    _, calls = _run(w)
+    g = _step_equals_calls(w, calls)
+    for b in range(w.B):
+        check_sequence(f"step cfg{cfg}", w, g, b, ref[b])
+
+
+def test_decode_step_config4_full_batch():
+    base = W.generate(4, seqs=[0, 1, 2, 3])
+    ref, _ = P.plant(base, P.params_of(base))
+    w = tile_batch(base, 64)
+    _log("cfg4 decode step: B=64 x 32768")
+    ds, calls = _run(w)
+    g = _step_equals_calls(w, calls, ds=ds)
+    for b in range(64):
+        check_sequence("step cfg4", w, g, b, ref[b % 4], b_src=b % 4)
+
+
+def test_decode_step_many_visual_tokens():
+    """40000 visual tokens in one sequence: more keys than one work-group's LDS
+    holds, so the step takes the separate kernels and the top-k reads its keys
+    from memory."""
+    w = small_workload(seed=16, B=1, Hq=4, Hkv=1, d=64, lens=[41000], segs=[[(500, 40000)]])
+    ref, _ = P.plant(w, P.params_of(w))
+    _log(f"40k visual: k={ref[0].k}")
+    _, calls = _run(w)
+    check_sequence("40k calls", w, calls, 0, ref[0])
+    g = _step_equals_calls(w, calls)
+    check_sequence("40k step", w, g, 0, ref[0])
 
 
 def test_fused_and_unfused_text_paths_agree():
