@@ -36,9 +36,9 @@ WORKLOAD_NAMES = {
     2: "7B-class decode layer: B=1, 28/4 heads, d=128, 1296 visual (36x36) at 14 + 2048 text",
     3: "7B-class ragged batch: B=16, 28/4 heads, d=128, 4096 visual + U{1024..8192} text",
     4: "7B-class multi-image 32k: B=64, 28/4 heads, d=128, 4 x 4096 visual + 16384 text",
-    5: "72B-class decode: B=8, 64/8 heads, d=128, 6400 visual + 4097 text (loop step 0)",
+    5: "72B-class decode loop: B=8, 64/8 heads, d=128, 6400 visual + 4097..4608 text over 512 steps",
 }
-DEFAULT_STEPS = {1: (200, 20), 2: (400, 40), 3: (100, 10), 4: (20, 3), 5: (100, 10)}
+DEFAULT_STEPS = {1: (200, 20), 2: (400, 40), 3: (100, 10), 4: (20, 3), 5: (512, 16)}
 
 
 class Hip:
@@ -63,20 +63,22 @@ class Hip:
         return t.value
 
 
-def algorithmic_bytes(w, ks):
+def algorithmic_bytes(w, ks, lens=None):
     """Bytes the method must move at least once per step, by kernel.
 
     Visual pass: the K rows of visual tokens (their Eq. (6) logits). Text pass:
     the K and V rows of text tokens. Kept pass: K and V rows of the k kept
-    visual tokens. q, outputs, scores and indices are < 1% and not counted."""
+    visual tokens. q, outputs, scores and indices are < 1% and not counted.
+    lens: per-step sequence lengths of a decode loop (same for every sequence);
+    the figures are then averages over its steps."""
     esz = 2 if w.dtype == "bf16" else 4
     row = w.Hkv * w.d * esz
     vis = text = kept = 0
     for b in range(w.B):
-        L = int(w.seq_len[b])
+        Ls = [int(w.seq_len[b])] if lens is None else list(lens)
         nv = sum(n for _, n in w.segments[b])
         vis += nv * row
-        text += 2 * (L - nv) * row
+        text += sum(2 * (L - nv) * row for L in Ls) / len(Ls)
         kept += 2 * int(ks[b]) * row
     return {"visual": vis, "text": text, "kept": kept}
 
@@ -138,8 +140,29 @@ def main():
 
     vp.lib()  # fail loudly if the HIP library is missing
     print(f"[bench] generating config {cfg}", file=sys.stderr, flush=True)
-    w = W.generate(cfg)
-    ds = S.DeviceStep(w)
+    loop = None
+    if cfg == 5:
+        # the decode loop: all 512 appended rows and drifting queries are
+        # generated and made resident first; step t runs with q_t and length
+        # 10497 + t (rows past a step's length are not part of its cache)
+        stream5 = W.Cfg5Stream(steps=512)
+        w = stream5.w
+        qs = []
+        for t in range(stream5.steps):
+            q_t, kr, vr, pos = stream5.step_inputs(t)
+            w.K[:, :, pos] = kr
+            w.V[:, :, pos] = vr
+            qs.append(q_t)
+        ds = S.DeviceStep(w)
+        q_all = torch.from_numpy(np.ascontiguousarray(np.stack(qs)).view(np.int16)).view(torch.bfloat16).to(ds.device)
+        lens = torch.tensor([[stream5.base_len + t + 1] * w.B for t in range(stream5.steps)], dtype=torch.int32,
+                            device=ds.device)
+        layouts = [vp.vp_layout(seq_len=lens[t].data_ptr(), vis_seg_off=ds.seg_off.data_ptr(),
+                                vis_seg=ds.seg.data_ptr()) for t in range(stream5.steps)]
+        loop = (stream5.steps, q_all, layouts, [stream5.base_len + t + 1 for t in range(stream5.steps)])
+    else:
+        w = W.generate(cfg)
+        ds = S.DeviceStep(w)
     kv_bytes = ds.K.numel() * ds.K.element_size() * 2
     R = args.rotate or max(1, math.ceil(MALL_DEFEAT_BYTES / kv_bytes))
     bufs = [(ds.K, ds.V)]
@@ -169,17 +192,20 @@ def main():
 
     def one_step(i, evs=(), arr6=(), arr3=()):
         K, V = bufs[i % R]
+        q, lay = ds.q, ds.layout
+        if loop is not None:
+            q, lay = loop[1][i % loop[0]], loop[2][i % loop[0]]
         if not args.calls:
-            vp.vp_decode_step(ds.shape, ds.layout, ds.params, ds.q, K, V, ds.mass_head, ds.mass_seq, ds.scores,
+            vp.vp_decode_step(ds.shape, lay, ds.params, q, K, V, ds.mass_head, ds.mass_seq, ds.scores,
                               ds.k, ds.vis_idx, ds.out, ds.ws, ds.ws_bytes, sp, events=arr6)
             return
-        vp.vp_visual_mass_timed(ds.shape, ds.layout, ds.params, ds.q, K, V, ds.mass_head, ds.mass_seq,
+        vp.vp_visual_mass_timed(ds.shape, lay, ds.params, q, K, V, ds.mass_head, ds.mass_seq,
                                 ds.scores, ds.ws, ds.ws_bytes, sp, events=arr3)
-        vp.vp_budget(ds.shape, ds.layout, ds.params, ds.mass_seq, ds.k, sp)
-        vp.vp_select_topk(ds.shape, ds.layout, ds.scores, ds.k, ds.vis_idx, sp)
+        vp.vp_budget(ds.shape, lay, ds.params, ds.mass_seq, ds.k, sp)
+        vp.vp_select_topk(ds.shape, lay, ds.scores, ds.k, ds.vis_idx, sp)
         if evs and evs[3]:
             hip.h.hipEventRecord(evs[3], sp)
-        vp.vp_sparse_decode_attn(ds.shape, ds.layout, ds.params, ds.q, K, V, ds.vis_idx, ds.k, ds.out,
+        vp.vp_sparse_decode_attn(ds.shape, lay, ds.params, q, K, V, ds.vis_idx, ds.k, ds.out,
                                  vp.VP_ATTN_TEXT_FROM_WORKSPACE, ds.ws, ds.ws_bytes, sp)
         if evs and evs[5]:
             hip.h.hipEventRecord(evs[5], sp)
@@ -205,9 +231,10 @@ def main():
     def phase(i, j):
         return float(np.mean([hip.elapsed_ms(e[i], e[j]) for e in evs_phase]))
     vis_ms, tail_ms, attn_ms = phase(0, 1), phase(2, 3), phase(3, 5)
-    assert np.array_equal(ds.k.cpu().numpy(), ks), "budget changed between warm-up and timed steps"
+    if loop is None:
+        assert np.array_equal(ds.k.cpu().numpy(), ks), "budget changed between warm-up and timed steps"
 
-    nb = algorithmic_bytes(w, ks)
+    nb = algorithmic_bytes(w, ks, None if loop is None else loop[3])
     step_bytes = nb["visual"] + nb["text"] + nb["kept"]
     ms_per_step = wall * 1e3 / steps
     achieved = nb["text"] / (text_ms * 1e-3) / 1e9

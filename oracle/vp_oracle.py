@@ -215,19 +215,22 @@ class SequenceResult:
     scores: np.ndarray           # [N_v] S_i, visual rank order
     k: int
     vis_idx: np.ndarray          # [k] positions, ascending
-    out: np.ndarray              # [Hq, d]
+    out: np.ndarray | None       # [Hq, d] (None when not requested)
     Z: np.ndarray | None = field(default=None, repr=False)
 
 
 def decode_step_sequence(q: np.ndarray, K: np.ndarray, V: np.ndarray,
                          seq_len: int, segments, params: OracleParams,
                          keep_logits: bool = False,
-                         k_override: int | None = None) -> SequenceResult:
+                         k_override: int | None = None,
+                         with_output: bool = True) -> SequenceResult:
     """The whole per-step path for one sequence at the anchor layer.
 
-    q: [Hq, d]; K, V: [Hkv, >=seq_len, d] (stored values: uint16 bf16 bits or float32).
+    q: [Hq, d]; K, V: [Hkv, >=seq_len, d] (stored values: uint16 bf16 bits or
+    float32; float64 arrays are taken as already widened).
     ``k_override`` replaces the Eq. (7) budget (used to test selection and
-    attention on their own).
+    attention on their own). ``with_output=False`` stops after the selection
+    (out is None): the attention output is the costly part on long contexts.
     """
     Hq, d = q.shape
     Hkv = K.shape[0]
@@ -262,10 +265,12 @@ def decode_step_sequence(q: np.ndarray, K: np.ndarray, V: np.ndarray,
     sel = select_top_k(S, vis_pos, k)
 
     # attention over the pruned context J = kept visual U text
-    J = np.sort(np.concatenate([sel, txt_pos]))
-    out = np.empty((Hq, d), dtype=np.float64)
-    for h in range(Hq):
-        out[h] = pruned_attention(qf[h], Kf[h // G], Vf[h // G], J, sm_scale)
+    out = None
+    if with_output:
+        J = np.sort(np.concatenate([sel, txt_pos]))
+        out = np.empty((Hq, d), dtype=np.float64)
+        for h in range(Hq):
+            out[h] = pruned_attention(qf[h], Kf[h // G], Vf[h // G], J, sm_scale)
 
     return SequenceResult(m_head, M_vis, M_max, S, k, sel, out,
                           Z if keep_logits else None)

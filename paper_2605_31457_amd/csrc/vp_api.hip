@@ -221,13 +221,18 @@ MergeArgs merge_args(const vp_shape* s, const vp_layout* l, const Plan& plan, co
 }
 
 // The fused per-sequence tail (one work-group per sequence) replaces four
-// launches; it pays off while the batch's visual tokens are few enough that
-// one CU per sequence is not the bottleneck.
+// launches, but streams a sequence's spilled logits (Hq x N_v floats) through
+// one CU. Measured: it wins at 28 heads x 1296 tokens (145 KB) and loses at
+// 28 x 4096 (459 KB, 16 sequences) and 64 x 6400 (1.6 MB, 8 sequences).
+#ifndef VP_TAIL_MAX_SPILL
+#define VP_TAIL_MAX_SPILL (256 << 10)  // bytes of spilled logits per sequence
+#endif
 #ifndef VP_TAIL_MAX_TOKENS
-#define VP_TAIL_MAX_TOKENS (1 << 17)
+#define VP_TAIL_MAX_TOKENS (1 << 17)  // visual tokens over the batch
 #endif
 bool use_tail(const vp_shape* s) {
-  return tail_fits(s->n_q_heads, s->max_vis) &&
+  const int64_t spill = static_cast<int64_t>(s->n_q_heads) * s->max_vis * 4;
+  return tail_fits(s->n_q_heads, s->max_vis) && spill <= static_cast<int64_t>(VP_TAIL_MAX_SPILL) &&
          static_cast<int64_t>(s->batch) * s->max_vis <= static_cast<int64_t>(VP_TAIL_MAX_TOKENS);
 }
 
@@ -452,9 +457,14 @@ vp_status vp_decode_step(const vp_shape* shape, const vp_layout* layout, const v
   } else {
     if (hipError_t e = launch_mass_finalize(m, st)) return hip_fail(e, "mass finalize launch");
     if (hipError_t e = launch_scores(m, st)) return hip_fail(e, "scores launch");
-    if (hipError_t e = launch_budget(budget_args(shape, layout, params, mass_seq, k), st))
-      return hip_fail(e, "budget launch");
-    if (hipError_t e = launch_topk(topk_args(shape, layout, scores, k, vis_idx), st)) return hip_fail(e, "top-k launch");
+    // the top-k kernel takes the Eq. (7) budget itself (one launch fewer)
+    TopkArgs tk = topk_args(shape, layout, scores, k, vis_idx);
+    tk.mass_seq = mass_seq;
+    tk.k_out = k;
+    tk.r_lo_bp = params->r_lo_bp;
+    tk.r_hi_bp = params->r_hi_bp;
+    tk.clamp = params->clamp;
+    if (hipError_t e = launch_topk(tk, st)) return hip_fail(e, "top-k launch");
   }
   if (hipError_t e = mark(3)) return hip_fail(e, "event record");
   if (hipError_t e = launch_attend(a, MODE_KEPT, dt, hd, st)) return hip_fail(e, "kept pass launch");

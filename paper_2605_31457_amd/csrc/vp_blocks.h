@@ -125,11 +125,11 @@ __device__ __forceinline__ float reduce_mass(const MassArgs& a, int b, int tid, 
 // ---------------------------------------------------------------------------
 // Eq. (2) score of the visual token at cache position pos of sequence b:
 // S = (1/Hq) sum_h 2^((z_h - m_h) / tau_score) / Ls_h from the spilled logits,
-// with 16 loads in flight at a time. hm/hinv: per-head max and 1/Ls.
+// with 32 loads in flight at a time. hm/hinv: per-head max and 1/Ls.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float token_score(const MassArgs& a, int b, int pos, const float* hm, const float* hinv) {
   const float* z = a.zs + static_cast<size_t>(b) * a.Hq * a.zs_stride + pos;
-  constexpr int kBatch = 16;
+  constexpr int kBatch = 32;
   float s = 0.f;
   for (int h0 = 0; h0 < a.Hq; h0 += kBatch) {
     float zz[kBatch];

@@ -125,6 +125,11 @@ struct TopkArgs {
   const float* scores;
   const int32_t* k;
   int32_t* vis_idx;
+  // optional: when mass_seq is set, k[b] is not read but computed by Eq. (7)
+  // from mass_seq (the budget of vp_budget) and written to k_out
+  const float* mass_seq;
+  int32_t* k_out;
+  int r_lo_bp, r_hi_bp, clamp;
 };
 
 hipError_t launch_topk(const TopkArgs& a, hipStream_t st);

@@ -38,7 +38,13 @@ __global__ __launch_bounds__(kSelThreads) void topk_kernel(const TopkArgs a, int
   if (wid == 0) load_segments(tab, a.seg + 2 * static_cast<long>(o0), a.seg_off[b + 1] - o0, L, lane);
   __syncthreads();
   const int n = min(tab.rk[tab.n], a.max_vis);
-  int k = a.k[b];
+  int k;
+  if (a.mass_seq) {
+    k = budget_rule(static_cast<double>(a.mass_seq[2 * b + 1]), tab.rk[tab.n], a.r_lo_bp, a.r_hi_bp, a.clamp);
+    if (tid == 0) a.k_out[b] = k;
+  } else {
+    k = a.k[b];
+  }
   k = k < 0 ? 0 : k;
   k = k > n ? n : k;
   k = k > a.k_cap ? a.k_cap : k;
