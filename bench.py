@@ -83,6 +83,29 @@ def algorithmic_bytes(w, ks, lens=None):
     return {"visual": vis, "text": text, "kept": kept}
 
 
+def counter_traffic(cfg: int):
+    """HBM bytes per launch of the text pass from the FETCH_SIZE / WRITE_SIZE
+    counter runs summarised in profiles/ (FETCH_SIZE scaled by a plain copy's
+    reading), or None when they were taken on other kernel sources or another
+    configuration."""
+    import glob
+    import hashlib
+    root = os.path.dirname(os.path.abspath(__file__))
+    path = os.path.join(root, "profiles", "text_pass_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        rec = json.load(fh)
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(root, "paper_2605_31457_amd", "csrc", "*"))):
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as src:
+            h.update(src.read())
+    if h.hexdigest() != rec.get("source_sha256") or str(cfg) not in rec.get("configs", {}):
+        return None
+    return rec["configs"][str(cfg)]["traffic_bytes"]
+
+
 def cpu_baseline(w, budget_s: float):
     """fp64 reference on this host: whole sequences until about budget_s seconds."""
     import numpy as np
@@ -118,6 +141,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calls", action="store_true", help="time the four separate calls instead of vp_decode_step")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device-to-device copy of MIB MiB (3 times): the reference "
+                         "for scaling the FETCH_SIZE / WRITE_SIZE counters")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -132,6 +158,16 @@ def main():
     from paper_2605_31457_amd import step as S
     from paper_2605_31457_amd import vp
     from paper_2605_31457_amd import workloads as W
+
+    if args.copy_calibration:
+        n = args.copy_calibration << 20
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n, "copies": 3}), flush=True)
+        return
 
     cfg = args.config
     steps, warmup = DEFAULT_STEPS[cfg]
@@ -264,7 +300,7 @@ def main():
         "roofline": {"kernel": f"text pass (attend_kernel<{w.dtype},{w.d},MODE_TEXT_BOTH>: text K/V, "
                                "Eq. (6)/(2) statistics, attention partial)", "bound": "hbm",
                      "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS,
-                     "traffic": None, "algorithmic_bytes_per_launch": nb["text"],
+                     "traffic": counter_traffic(cfg), "algorithmic_bytes_per_launch": nb["text"],
                      "avg_launch_ms": text_ms, "share_of_step": text_ms / ms_per_step},
         "visual_pass": {"achieved": nb["visual"] / (vis_ms * 1e-3) / 1e9, "unit": "GB/s",
                         "algorithmic_bytes_per_launch": nb["visual"], "avg_launch_ms": vis_ms},

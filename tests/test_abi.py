@@ -118,10 +118,45 @@ def test_calls_reject_nulls_and_bad_params_before_launch(L):
     assert "workspace" in L.vp_last_error().decode() or L.vp_last_error().decode() != ""
 
 
+def test_decode_step_rejects_bad_arguments_before_launch(L):
+    s, lay, p = _shape(), _layout(), _params()
+    ws_bytes = vp.vp_workspace_size(s)
+    fake = 0x10000  # never dereferenced: every case below fails validation first
+
+    def step(shape=s, params=p, V=fake, out=fake, ws=fake, nbytes=ws_bytes, events=()):
+        vp.vp_decode_step(shape, lay, params, fake, fake, V, fake, fake, fake, fake, fake, out, ws, nbytes, 0,
+                          events=events)
+
+    with pytest.raises(vp.VPError, match="VP_ERR_NULL"):
+        step(V=None)  # the step needs V (text attention is fused into the context pass)
+    with pytest.raises(vp.VPError, match="VP_ERR_NULL"):
+        step(out=None)
+    with pytest.raises(vp.VPError, match="VP_ERR_WORKSPACE"):
+        step(nbytes=ws_bytes - 1)
+    with pytest.raises(vp.VPError, match="VP_ERR_WORKSPACE"):
+        step(ws=fake + 16)
+    with pytest.raises(vp.VPError, match="VP_ERR_SHAPE"):
+        step(shape=_shape(k_cap=10))
+    with pytest.raises(vp.VPError, match="VP_ERR_RANGE"):
+        step(params=_params(tau_score=-1.0))
+    with pytest.raises(vp.VPError, match="VP_ERR_RANGE"):
+        step(events=[None] * (vp.VP_STEP_EVENTS + 1))
+    with pytest.raises(vp.VPError, match="VP_ERR_DTYPE"):
+        step(shape=_shape(dtype=9))
+
+
+def test_event_array_is_reusable():
+    arr, n = vp.event_array([None, None, None])
+    assert n == 3 and len(arr) == 3
+    assert vp.event_array((arr, n)) == (arr, n)
+    assert vp.event_array(()) == (None, 0)
+
+
 def test_header_constants_match_binding():
     text = open(HEADER).read()
     consts = dict(re.findall(r"#define\s+(VP_[A-Z_]+)\s+(\d+)", text))
     assert int(consts["VP_MASS_EVENTS"]) == vp.VP_MASS_EVENTS
+    assert int(consts["VP_STEP_EVENTS"]) == vp.VP_STEP_EVENTS
     assert int(consts["VP_ATTN_TEXT_FROM_WORKSPACE"]) == vp.VP_ATTN_TEXT_FROM_WORKSPACE
 
 
