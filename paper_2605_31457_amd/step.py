@@ -7,6 +7,8 @@ libvisionpulse.so.
 """
 from __future__ import annotations
 
+import ctypes
+
 import numpy as np
 import torch
 
@@ -44,7 +46,10 @@ class DeviceStep:
         self.seg = torch.from_numpy(seg.reshape(-1) if seg.size else np.zeros(2, np.int32)).to(self.device)
         B, Hq, d = w.B, w.Hq, w.d
         self.max_vis = max_vis or w.max_vis
-        self.k_cap = k_cap or w.k_cap
+        self.params = make_params(w)
+        # row capacity of the kept-index output: the largest budget the rule
+        # allows for max_vis visual tokens (its value at full visual mass)
+        self.k_cap = k_cap or max(1, int(vp.lib().vp_budget_host(1.0, self.max_vis, ctypes.byref(self.params))))
         st = self.K.stride()
         self.shape = vp.vp_shape(batch=B, n_q_heads=Hq, n_kv_heads=w.Hkv, head_dim=d,
                                  dtype=vp.VP_BF16 if w.dtype == "bf16" else vp.VP_F32,
@@ -53,7 +58,6 @@ class DeviceStep:
                                  kv_stride_s=st[2])
         self.layout = vp.vp_layout(seq_len=self.seq_len.data_ptr(), vis_seg_off=self.seg_off.data_ptr(),
                                    vis_seg=self.seg.data_ptr())
-        self.params = make_params(w)
         f32 = dict(dtype=torch.float32, device=self.device)
         i32 = dict(dtype=torch.int32, device=self.device)
         self.mass_head = torch.zeros(B, Hq, **f32)

@@ -23,7 +23,7 @@ from dataclasses import dataclass, field
 import numpy as np
 
 __all__ = ["Workload", "CONFIGS", "generate", "bf16_round", "bf16_to_f32",
-           "Cfg5Stream", "layout_arrays", "k_cap_for"]
+           "Cfg5Stream", "layout_arrays"]
 
 
 # --------------------------------------------------------------------------
@@ -81,19 +81,8 @@ class Workload:
     def max_segs(self) -> int:
         return int(max(1, max(len(s) for s in self.segments)))
 
-    @property
-    def k_cap(self) -> int:
-        return k_cap_for(self.max_vis, self.r_hi_bp, self.clamp)
-
     def elem_bytes(self) -> int:
         return 2 if self.dtype == "bf16" else 4
-
-
-def k_cap_for(max_vis: int, r_hi_bp: int, clamp: bool) -> int:
-    """Row capacity of the kept-index output: the largest budget the clamp allows."""
-    if not clamp:
-        return max(1, max_vis)
-    return max(1, (r_hi_bp * max_vis) // 10000, -((-100 * max_vis) // 10000))
 
 
 def layout_arrays(segments):

@@ -274,3 +274,29 @@ def test_unclean_device_layout_is_clipped():
         g = ds.results()
         for b in range(2):
             check_sequence(f"clipped fused={fused}", w, g, b, ref[b])
+
+
+PRESETS = {
+    # the 10% retention preset: tau = 0.4, clamp (0.05 N, 0.10 N)
+    "retain10": dict(tau_mass=0.4, r_lo_bp=500, r_hi_bp=1000),
+    # fixed-ratio budgets: r_lo = r_hi = r gives k = ceil(r N_v)
+    "fixed1pct": dict(r_lo_bp=100, r_hi_bp=100),
+    "fixed5pct": dict(r_lo_bp=500, r_hi_bp=500),
+    # scores at the mass temperature (reading A3's variant)
+    "tau_score_0.1": dict(tau_score=0.1),
+}
+
+
+@pytest.mark.parametrize("preset", sorted(PRESETS))
+def test_budget_presets(preset):
+    """Budget and estimator presets are parameters of the same kernels: the
+    10% setting, fixed ratios and tempered scores, on four config-3 sequences."""
+    w = W.generate(3, B=4)
+    for key, val in PRESETS[preset].items():
+        setattr(w, key, val)
+    ref, _ = P.plant(w, P.params_of(w))
+    _log(f"preset {preset}: k={[ref[b].k for b in range(w.B)]}")
+    ds, calls = _run(w)
+    for b in range(w.B):
+        check_sequence(f"{preset}", w, calls, b, ref[b])
+    _step_equals_calls(w, calls, ds=ds)
