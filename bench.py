@@ -131,6 +131,77 @@ def cpu_baseline(w, budget_s: float):
                       f"{el:.1f} s wall; steps/s = 1 / (mean time per sequence x B={w.B})"}
 
 
+def bench_layers(args, w, ds, bufs, loop, steps, warmup, sp, hip):
+    """A per-token attention step over L layers, timed as a whole: the anchor
+    layer's vp_decode_step and L-1 calls of vp_sparse_decode_attn on the other
+    layers' caches with the anchor's kept set (Sec. 4.1: layers after the
+    anchor reuse its selection); with --dense, L layers of full attention
+    (vp_sparse_decode_attn on a layout with no visual segments, so every cached
+    row goes through the streaming text pass). Layer l of step i reads cache
+    copy (i * L + l) mod R."""
+    import numpy as np
+    import torch
+    from paper_2605_31457_amd import vp
+    L, R = args.layers, len(bufs)
+    out_l = torch.empty_like(ds.out)
+    lay_dense = None
+    if args.dense:
+        seg_off0 = torch.zeros(w.B + 1, dtype=torch.int32, device=ds.device)
+        seg0 = torch.zeros(2, dtype=torch.int32, device=ds.device)
+        k0 = torch.zeros(w.B, dtype=torch.int32, device=ds.device)
+        lay_dense = [vp.vp_layout(seq_len=(loop[2][t].seq_len if loop else ds.layout.seq_len),
+                                  vis_seg_off=seg_off0.data_ptr(), vis_seg=seg0.data_ptr())
+                     for t in range(loop[0] if loop else 1)]
+
+    def one(i):
+        t = i % loop[0] if loop else 0
+        q = loop[1][t] if loop else ds.q
+        lay = loop[2][t] if loop else ds.layout
+        if args.dense:
+            for layer in range(L):
+                K, V = bufs[(i * L + layer) % R]
+                vp.vp_sparse_decode_attn(ds.shape, lay_dense[t], ds.params, q, K, V, ds.vis_idx, k0, out_l, 0,
+                                         ds.ws, ds.ws_bytes, sp)
+            return
+        K, V = bufs[(i * L) % R]
+        vp.vp_decode_step(ds.shape, lay, ds.params, q, K, V, ds.mass_head, ds.mass_seq, ds.scores, ds.k,
+                          ds.vis_idx, ds.out, ds.ws, ds.ws_bytes, sp)
+        for layer in range(1, L):
+            K, V = bufs[(i * L + layer) % R]
+            vp.vp_sparse_decode_attn(ds.shape, lay, ds.params, q, K, V, ds.vis_idx, ds.k, out_l, 0,
+                                     ds.ws, ds.ws_bytes, sp)
+
+    for i in range(warmup):
+        one(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        one(warmup + i)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ks = ds.k.cpu().numpy()
+    nb = algorithmic_bytes(w, ks, None if loop is None else loop[3])
+    esz = 2 if w.dtype == "bf16" else 4
+    row = w.Hkv * w.d * esz
+    if args.dense:
+        # every cached K and V row of every sequence, per layer
+        if loop:
+            per_layer = w.B * 2 * row * sum(loop[3]) / len(loop[3])
+        else:
+            per_layer = sum(2 * int(n) * row for n in w.seq_len)
+        step_bytes = L * per_layer
+    else:
+        step_bytes = nb["visual"] + nb["text"] + nb["kept"] + (L - 1) * (nb["text"] + nb["kept"])
+    ms = wall * 1e3 / steps
+    res = {"metric": "per-token attention steps/s over several layers", "value": steps / wall, "unit": "steps/s",
+           "n_gpus": 1, "steps": steps, "warmup": warmup, "ms_per_step": ms, "higher_is_better": True,
+           "layers": L, "mode": "dense" if args.dense else "anchor decode step + sparse layers",
+           "step_algorithmic_bytes": step_bytes, "step_achieved_GBps": step_bytes / (ms * 1e-3) / 1e9,
+           "dtype": w.dtype, "data": "synthetic", "config": {"workload": f"config {args.config}: "
+                                                             f"{WORKLOAD_NAMES[args.config]}", "kv_copies": R}}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -141,6 +212,11 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calls", action="store_true", help="time the four separate calls instead of vp_decode_step")
+    ap.add_argument("--layers", type=int, default=1,
+                    help="time a per-token step over this many layers: the anchor layer's decode step, then "
+                         "every other layer's attention over the anchor's kept set on its own KV cache")
+    ap.add_argument("--dense", action="store_true",
+                    help="with --layers: every layer attends to all of its cached tokens instead")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (3 times): the reference "
                          "for scaling the FETCH_SIZE / WRITE_SIZE counters")
@@ -201,6 +277,9 @@ def main():
         ds = S.DeviceStep(w)
     kv_bytes = ds.K.numel() * ds.K.element_size() * 2
     R = args.rotate or max(1, math.ceil(MALL_DEFEAT_BYTES / kv_bytes))
+    layered = args.layers > 1 or args.dense
+    if layered:
+        R = max(R, args.layers)  # every layer of a step reads its own cache copy
     bufs = [(ds.K, ds.V)]
     for _ in range(R - 1):
         bufs.append((ds.K.clone(), ds.V.clone()))
@@ -211,6 +290,9 @@ def main():
     hip = Hip()
     stream = torch.cuda.current_stream()
     sp = stream.cuda_stream
+    if layered:
+        bench_layers(args, w, ds, bufs, loop, steps, warmup, sp, hip)
+        return
     # step events: [0] visual pass [1] text pass [2] tail [3] kept pass [4] merge [5].
     # An event record costs a few microseconds of queue time, which is visible on
     # small steps, so the timed steps record only the two around the text pass

@@ -300,3 +300,40 @@ def test_budget_presets(preset):
     for b in range(w.B):
         check_sequence(f"{preset}", w, calls, b, ref[b])
     _step_equals_calls(w, calls, ds=ds)
+
+
+def test_later_layers_reuse_the_anchor_selection():
+    """Layers after the anchor attend over the anchor's kept set on their own KV
+    (Sec. 4.1): vp_sparse_decode_attn reading the text part itself, on two other
+    layers' caches and queries, against the reference attention over the same
+    context. A layout with no visual segments and k = 0 gives dense attention."""
+    w = W.generate(2)
+    ref, _ = P.plant(w, P.params_of(w))
+    ds, g = _run(w)
+    check_sequence("anchor", w, g, 0, ref[0])
+    sel = g["vis_idx"][0, :int(g["k"][0])]
+    for seed in (21, 22):
+        wl = W.generate(2, seed=seed)  # another layer: same layout, its own q, K, V
+        dl = S.DeviceStep(wl)
+        dl.vis_idx.copy_(ds.vis_idx)
+        dl.k.copy_(ds.k)
+        dl.sparse_decode_attn(fused=False)
+        got = dl.results()["out"][0]
+        L = int(wl.seq_len[0])
+        J = np.sort(np.concatenate([sel, O.text_positions(L, wl.segments[0])]))
+        qf = O.as_f64(wl.q[0])
+        G = wl.Hq // wl.Hkv
+        sm = 1.0 / np.sqrt(wl.d)
+        want = np.stack([O.pruned_attention(qf[h], wl.K[0, h // G], wl.V[0, h // G], J, sm) for h in range(wl.Hq)])
+        np.testing.assert_allclose(got, want, atol=2e-2, rtol=1e-2, err_msg=f"layer seed {seed}")
+        # dense: every cached row attended
+        seg_off0 = torch.zeros(2, dtype=torch.int32, device=dl.device)
+        seg0 = torch.zeros(2, dtype=torch.int32, device=dl.device)
+        dl.layout = S.vp.vp_layout(seq_len=dl.seq_len.data_ptr(), vis_seg_off=seg_off0.data_ptr(),
+                                   vis_seg=seg0.data_ptr())
+        dl.k.zero_()
+        dl.sparse_decode_attn(fused=False)
+        got = dl.results()["out"][0]
+        J = np.arange(L)
+        want = np.stack([O.pruned_attention(qf[h], wl.K[0, h // G], wl.V[0, h // G], J, sm) for h in range(wl.Hq)])
+        np.testing.assert_allclose(got, want, atol=2e-2, rtol=1e-2, err_msg=f"dense layer seed {seed}")
