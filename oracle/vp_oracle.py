@@ -30,7 +30,9 @@ Readings where the paper is silent:
      with N = N_v and r in basis points (integer arithmetic);
   A10 ties in Top-K go to the lower position; the index set is returned ascending;
   A12 the pruned softmax is renormalised over the kept context only; an empty
-     context yields a zero output.
+     context yields a zero output;
+  A18 the Top-p budget counts visual tokens in the Eq. (3) order until their
+     Eq. (2) scores sum to p (all of them if they never do).
 
 Parity status: every function below is pinned by tests/test_oracle_pins.py
 (closed forms, invariants, brute force, library cross-checks and the
@@ -45,7 +47,7 @@ import numpy as np
 
 __all__ = [
     "as_f64", "logits", "tempered_attention", "visual_mass", "retention_bounds",
-    "budget", "importance_scores", "select_top_k", "pruned_attention",
+    "budget", "budget_top_p", "importance_scores", "select_top_k", "pruned_attention",
     "OracleParams", "SequenceResult", "decode_step_sequence", "decode_step",
     "visual_positions", "text_positions",
 ]
@@ -175,6 +177,20 @@ def select_top_k(S: np.ndarray, vis_pos: np.ndarray, k: int) -> np.ndarray:
         return np.zeros(0, dtype=np.int64)
     order = np.lexsort((vis_pos, -S))          # primary key -S, secondary position
     return np.sort(vis_pos[order[:k]])
+
+
+def budget_top_p(S: np.ndarray, vis_pos: np.ndarray, p: float) -> int:
+    """The Top-p budget the paper compares against (Sec. 5, budgeting strategies):
+    the smallest number of visual tokens, taken in the Eq. (3) order (descending
+    S, ties to the lower position), whose scores sum to at least p; every visual
+    token when all of them sum to less (reading A18). p <= 0 gives 0.
+    """
+    if p <= 0 or len(S) == 0:
+        return 0
+    order = np.lexsort((vis_pos, -S))
+    csum = np.cumsum(S[order])
+    reach = np.nonzero(csum >= p)[0]
+    return int(reach[0] + 1) if len(reach) else len(S)
 
 
 # --------------------------------------------------------------------------

@@ -241,6 +241,36 @@ def test_selection_invariant_min_selected_ge_max_rest():
     assert r.scores[sel].min() >= r.scores[~sel].max()
 
 
+def test_top_p_budget_brute_force_and_closed_forms():
+    """Top-p (A18) pinned without reusing its code path: (a) brute force, the
+    smallest subset size k such that SOME k tokens reach p is the answer (the
+    largest-k-scores subset is the best of any size), on tiny inputs with ties;
+    (b) equal scores s give ceil(p / s); (c) p above the total keeps every
+    token; p <= 0 keeps none; (d) it is monotone in p."""
+    rng = np.random.default_rng(18)
+    for trial in range(60):
+        n = int(rng.integers(1, 8))
+        pos = np.sort(rng.choice(np.arange(30), size=n, replace=False))
+        S = np.round(rng.random(n) * 4) / 16 if trial % 2 else rng.random(n) / n
+        total = S.sum()
+        for p in (0.0, total * 0.3, total * 0.5 + 1e-9, total * 0.999, total * 1.5, 1e-12):
+            k = O.budget_top_p(S, pos, p)
+            if p <= 0:
+                assert k == 0
+                continue
+            best = [max(S[list(c)].sum() for c in itertools.combinations(range(n), m)) for m in range(1, n + 1)]
+            reach = [m + 1 for m, b in enumerate(best) if b >= p]
+            assert k == (reach[0] if reach else n), (S, p, k)
+    # dyadic scores sum exactly, so the closed form holds without rounding slack
+    for s, p, want in ((2.0 ** -7, 10 * 2.0 ** -7, 10), (2.0 ** -6, 0.1, 7), (2.0 ** -5, 0.5, 16),
+                       (2.0 ** -10, 2.0 ** -3 + 2.0 ** -11, 129), (2.0 ** -2, 0.9, 4)):
+        S = np.full(200, s)
+        assert O.budget_top_p(S, np.arange(200), p) == want == min(200, math.ceil(p / s))
+    S = rng.random(50) / 100
+    ks = [O.budget_top_p(S, np.arange(50), p) for p in np.linspace(0, S.sum() * 1.2, 40)]
+    assert ks == sorted(ks) and ks[-1] == 50
+
+
 # ---------------------------------------------------------------------------
 # pruned attention against the library's attention
 # ---------------------------------------------------------------------------
