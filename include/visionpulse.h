@@ -168,6 +168,21 @@ vp_status vp_budget(const vp_shape* shape, const vp_layout* layout, const vp_par
                     const float* mass_seq, int32_t* k, void* stream);
 
 /*
+ * vp_budget_top_p -- the Top-p budget the paper compares the mass rule against
+ * (Sec. 5, budgeting strategies): for every sequence, the smallest number of
+ * visual tokens, taken in the Eq. (3) order (descending score, ties to the
+ * lower position), whose Eq. (2) scores sum to at least p; N_v when all of them
+ * sum to less; 0 when p == 0. The sums are exact in 2^-40 fixed point (each
+ * fp32 score rounded down), so the count is deterministic. Feed k to
+ * vp_select_topk (which clamps it to k_cap).
+ *
+ * scores: [B, max_vis] float (from vp_visual_mass); k: [B] int32 device.
+ * VP_ERR_RANGE unless 0 <= p <= 1.
+ */
+vp_status vp_budget_top_p(const vp_shape* shape, const vp_layout* layout, const float* scores, float p,
+                          int32_t* k, void* stream);
+
+/*
  * vp_select_topk -- Eq. (3): for every sequence, the k[b] visual tokens with the
  * largest score, ties to the lower position; written as absolute cache
  * positions in ascending order to vis_idx[b, 0 .. k[b]) and -1 in

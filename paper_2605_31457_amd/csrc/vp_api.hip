@@ -387,6 +387,27 @@ vp_status vp_select_topk(const vp_shape* shape, const vp_layout* layout, const f
   return VP_OK;
 }
 
+vp_status vp_budget_top_p(const vp_shape* shape, const vp_layout* layout, const float* scores, float p, int32_t* k,
+                          void* stream) {
+  g_last_error.clear();
+  if (vp_status e = check_shape(shape)) return e;
+  if (vp_status e = check_layout(layout)) return e;
+  if (!scores || !k) return fail(VP_ERR_NULL, "scores and k required");
+  if (!(p >= 0.f && p <= 1.f)) return fail(VP_ERR_RANGE, "p %g outside [0, 1]", static_cast<double>(p));
+  TopPArgs t{};
+  t.seq_len = layout->seq_len;
+  t.seg_off = layout->vis_seg_off;
+  t.seg = layout->vis_seg;
+  t.B = shape->batch;
+  t.max_seq_len = shape->max_seq_len;
+  t.max_vis = shape->max_vis;
+  t.p = p;
+  t.scores = scores;
+  t.k = k;
+  if (hipError_t e = launch_top_p(t, static_cast<hipStream_t>(stream))) return hip_fail(e, "top-p launch");
+  return VP_OK;
+}
+
 vp_status vp_sparse_decode_attn(const vp_shape* shape, const vp_layout* layout, const vp_params* params,
                                 const void* q, const void* K, const void* V, const int32_t* vis_idx,
                                 const int32_t* k, void* out, int32_t flags, void* workspace, size_t workspace_bytes,

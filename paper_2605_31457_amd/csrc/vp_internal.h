@@ -134,6 +134,18 @@ struct TopkArgs {
 
 hipError_t launch_topk(const TopkArgs& a, hipStream_t st);
 
+struct TopPArgs {
+  const int32_t* seq_len;
+  const int32_t* seg_off;
+  const int32_t* seg;
+  int B, max_seq_len, max_vis;
+  float p;
+  const float* scores;
+  int32_t* k;
+};
+
+hipError_t launch_top_p(const TopPArgs& a, hipStream_t st);
+
 struct MergeArgs {
   const int32_t* seq_len;
   const int32_t* kk;

@@ -64,6 +64,7 @@ def lib() -> ctypes.CDLL:
                                       ctypes.POINTER(V), ctypes.c_int32], ctypes.c_int),
             "vp_budget": ([P(vp_shape), P(vp_layout), P(vp_params), V, V, V], ctypes.c_int),
             "vp_select_topk": ([P(vp_shape), P(vp_layout), V, V, V, V], ctypes.c_int),
+            "vp_budget_top_p": ([P(vp_shape), P(vp_layout), V, ctypes.c_float, V, V], ctypes.c_int),
             "vp_sparse_decode_attn": ([P(vp_shape), P(vp_layout), P(vp_params), V, V, V, V, V, V,
                                        ctypes.c_int32, V, S, V], ctypes.c_int),
             "vp_budget_host": ([ctypes.c_double, ctypes.c_int32, P(vp_params)], ctypes.c_int32),
@@ -161,6 +162,11 @@ def vp_decode_step(shape, layout, params, q, K, V, mass_head, mass_seq, scores, 
 def vp_budget(shape, layout, params, mass_seq, k, stream=None):
     _check("vp_budget", lib().vp_budget(ctypes.byref(shape), ctypes.byref(layout), ctypes.byref(params),
                                         _p(mass_seq), _p(k), _stream(stream)))
+
+
+def vp_budget_top_p(shape, layout, scores, p, k, stream=None):
+    _check("vp_budget_top_p", lib().vp_budget_top_p(ctypes.byref(shape), ctypes.byref(layout), _p(scores),
+                                                    float(p), _p(k), _stream(stream)))
 
 
 def vp_select_topk(shape, layout, scores, k, vis_idx, stream=None):

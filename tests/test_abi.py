@@ -145,6 +145,16 @@ def test_decode_step_rejects_bad_arguments_before_launch(L):
         step(shape=_shape(dtype=9))
 
 
+def test_top_p_rejects_bad_arguments(L):
+    s, lay = _shape(), _layout()
+    fake = 0x10000
+    for p in (-0.1, 1.5, float("nan")):
+        with pytest.raises(vp.VPError, match="VP_ERR_RANGE"):
+            vp.vp_budget_top_p(s, lay, fake, p, fake, 0)
+    with pytest.raises(vp.VPError, match="VP_ERR_NULL"):
+        vp.vp_budget_top_p(s, lay, None, 0.1, fake, 0)
+
+
 def test_event_array_is_reusable():
     arr, n = vp.event_array([None, None, None])
     assert n == 3 and len(arr) == 3

@@ -337,3 +337,85 @@ def test_later_layers_reuse_the_anchor_selection():
         J = np.arange(L)
         want = np.stack([O.pruned_attention(qf[h], wl.K[0, h // G], wl.V[0, h // G], J, sm) for h in range(wl.Hq)])
         np.testing.assert_allclose(got, want, atol=2e-2, rtol=1e-2, err_msg=f"dense layer seed {seed}")
+
+
+def _prefix_margin(S, vis, p):
+    """Distance from p to the nearest prefix sum of S in the Eq. (3) order."""
+    csum = np.cumsum(S[np.lexsort((vis, -S))])
+    return np.min(np.abs(csum - p)) if len(csum) else np.inf
+
+
+def test_top_p_budget_kernel():
+    """vp_budget_top_p on given fp32 scores (random, tied, dyadic, all equal,
+    empty) against the reference Top-p budget on the same values; every p is
+    kept at least 1e-7 from any prefix sum (the kernel's fixed-point sums are
+    exact to n * 2^-40)."""
+    rng = np.random.default_rng(19)
+    n_vis = [16384, 4096, 1296, 37, 1, 300, 0]
+    segs = [[(16 + 8188 * i, 4096) for i in range(4)], [(0, 4096)], [(14, 1296)], [(3, 10), (20, 27)],
+            [(0, 1)], [(0, 100), (150, 100), (300, 100)], []]
+    lens = [32768, 5000, 3358, 50, 1, 400, 64]
+    w = small_workload(seed=20, B=7, Hq=4, Hkv=1, d=64, lens=lens, segs=segs, spike=0)
+    ds = S.DeviceStep(w, k_cap=1000, max_vis=16384)
+    checked = 0
+    for trial in range(8):
+        sc = np.zeros((7, 16384), np.float32)
+        for b, n in enumerate(n_vis):
+            if trial % 4 == 0:
+                x = rng.random(n) ** 3
+            elif trial % 4 == 1:
+                x = np.floor(rng.random(n) * 8) + 1          # heavy ties
+            elif trial % 4 == 2:
+                x = np.ones(n)                                 # all equal
+            else:
+                x = rng.exponential(size=n)
+            sc[b, :n] = (x / max(x.sum(), 1e-30) * rng.uniform(0.3, 1.0)).astype(np.float32)
+        ds.scores.copy_(torch.from_numpy(sc))
+        for p in (0.0, 0.1, 0.37, 0.9, 1.0):
+            want = []
+            for b, n in enumerate(n_vis):
+                vis = O.visual_positions(lens[b], segs[b])
+                S64 = sc[b, :n].astype(np.float64)
+                if p > 0 and _prefix_margin(S64, vis, p) < 1e-7:
+                    want.append(None)      # too close to a prefix sum to be decided in fp32 input
+                else:
+                    want.append(O.budget_top_p(S64, vis, p))
+            S.vp.vp_budget_top_p(ds.shape, ds.layout, ds.scores, p, ds.k)
+            got = ds.k.cpu().numpy()
+            for b, wv in enumerate(want):
+                if wv is not None:
+                    assert int(got[b]) == wv, (trial, p, b, int(got[b]), wv)
+                    checked += 1
+    _log(f"top-p: {checked} budgets checked")
+    assert checked > 200
+
+
+def test_top_p_step_selects_the_reference_set():
+    """Scores from the GPU step, the Top-p budget, then the selection: the set
+    equals the reference's Top-p selection on the reference scores."""
+    w = W.generate(2)
+    ref, _ = P.plant(w, P.params_of(w))
+    ds, g = _run(w)
+    r = ref[0]
+    vis = O.visual_positions(int(w.seq_len[0]), w.segments[0])
+    ds_k = S.DeviceStep(w, k_cap=len(vis))
+    ds_k.scores.copy_(ds.scores)
+    checked = 0
+    for p in (0.05, 0.1, 0.2, 0.3):
+        if _prefix_margin(r.scores, vis, p) < 1e-5:
+            continue
+        checked += 1
+        kp = O.budget_top_p(r.scores, vis, p)
+        S.vp.vp_budget_top_p(ds_k.shape, ds_k.layout, ds_k.scores, p, ds_k.k)
+        assert int(ds_k.k.cpu()[0]) == kp, p
+        ds_k.select_topk()
+        idx = ds_k.vis_idx.cpu().numpy()[0]
+        want = O.select_top_k(r.scores, vis, kp)
+        # the planted gap sits at the Eq. (7) cut; elsewhere compare within rounding
+        got = idx[:kp]
+        if not np.array_equal(got, want):
+            order = np.lexsort((vis, -r.scores))
+            cut = r.scores[order[kp - 1]]
+            diff = np.setxor1d(got, want)
+            assert np.all(np.abs(r.scores[np.searchsorted(vis, diff)] - cut) <= 2e-5 * cut), p
+    assert checked >= 2
