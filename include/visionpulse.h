@@ -146,6 +146,8 @@ vp_status vp_visual_mass(const vp_shape* shape, const vp_layout* layout, const v
  *   [0] before the visual pass      [1] after it, before the text pass
  *   [2] after the text pass         [3] after the mass reduction
  *   [4] after the scores kernel.
+ * (With VP_PLAN_ONE_CONTEXT_LAUNCH and V given, [0] and [1] both precede the
+ * one launch of both passes; see vp_step_plan.)
  * events may be NULL when n_events is 0. Results are identical to
  * vp_visual_mass. VP_ERR_RANGE if n_events is outside [0, VP_MASS_EVENTS].
  */
@@ -228,6 +230,7 @@ vp_status vp_sparse_decode_attn(const vp_shape* shape, const vp_layout* layout, 
  * (at most VP_STEP_EVENTS; NULL entries skipped):
  *   [0] before the visual pass   [1] before the text pass
  *   [2] after the text pass      [3] before the kept-row pass
+ *   (with VP_PLAN_ONE_CONTEXT_LAUNCH, [0] and [1] both precede that launch)
  *   [4] before the merge         [5] after the merge.
  * Errors as for the four calls; VP_ERR_RANGE if n_events is outside
  * [0, VP_STEP_EVENTS]. The workspace must not be shared by concurrent calls.
@@ -238,6 +241,22 @@ vp_status vp_decode_step(const vp_shape* shape, const vp_layout* layout, const v
                          float* mass_head, float* mass_seq, float* scores, int32_t* k, int32_t* vis_idx,
                          void* out, void* workspace, size_t workspace_bytes, void* stream,
                          void* const* events, int32_t n_events);
+
+/*
+ * vp_step_plan -- how vp_visual_mass (with V) and vp_decode_step will launch
+ * their kernels for this shape (pure host computation; for profiling and
+ * benchmarks). flags is a bit set of
+ *   VP_PLAN_ONE_CONTEXT_LAUNCH  the visual and text passes share one launch
+ *                               (small caches); events [0] and [1] are then
+ *                               recorded together before it, so [1]..[2]
+ *                               times the whole context pass;
+ *   VP_PLAN_FUSED_TAIL          vp_decode_step runs the mass reduction,
+ *                               budget, scores and top-k in one launch per
+ *                               sequence (small visual sets).
+ */
+#define VP_PLAN_ONE_CONTEXT_LAUNCH 1
+#define VP_PLAN_FUSED_TAIL 2
+vp_status vp_step_plan(const vp_shape* shape, const vp_params* params, int32_t* flags);
 
 /* Host mirror of vp_budget's rule for one sequence (pure; for callers that keep
  * the mass on the host). Returns -1 for invalid parameters. */

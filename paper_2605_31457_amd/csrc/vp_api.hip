@@ -240,6 +240,17 @@ bool use_tail(const vp_shape* s) {
          static_cast<int64_t>(s->batch) * s->max_vis <= static_cast<int64_t>(VP_TAIL_MAX_TOKENS);
 }
 
+// Both context passes in one launch: saves a launch and overlaps the two
+// passes' latency chains where the cache is small; kept apart otherwise, so
+// the visual pass's logit writes stay out of the text pass's read stream.
+#ifndef VP_DUAL_MAX_TILES
+#define VP_DUAL_MAX_TILES 4096  // 32-row tiles over the batch and KV heads
+#endif
+bool use_dual(const vp_shape* s) {
+  const int64_t tiles = static_cast<int64_t>(s->batch) * s->n_kv_heads * ((s->max_seq_len + 31) / 32);
+  return tiles <= static_cast<int64_t>(VP_DUAL_MAX_TILES);
+}
+
 vp_status check_budget_cap(const vp_shape* s, const vp_params* p) {
   if (s->k_cap < max_budget(s, p))
     return fail(VP_ERR_SHAPE, "k_cap %d < largest budget %d for max_vis %d", s->k_cap, max_budget(s, p), s->max_vis);
@@ -342,11 +353,17 @@ vp_status vp_visual_mass_timed(const vp_shape* shape, const vp_layout* layout, c
     return (i < n_events && events[i]) ? hipEventRecord(static_cast<hipEvent_t>(events[i]), st) : hipSuccess;
   };
   if (hipError_t e = mark(0)) return hip_fail(e, "event record");
-  if (hipError_t e = launch_attend(a, MODE_VIS, shape->dtype, shape->head_dim, st))
-    return hip_fail(e, "visual pass launch");
-  if (hipError_t e = mark(1)) return hip_fail(e, "event record");
-  if (hipError_t e = launch_attend(a, V ? MODE_TEXT_BOTH : MODE_TEXT_STATS, shape->dtype, shape->head_dim, st))
-    return hip_fail(e, "text pass launch");
+  if (V && use_dual(shape)) {
+    if (hipError_t e = mark(1)) return hip_fail(e, "event record");
+    if (hipError_t e = launch_attend(a, MODE_DUAL, shape->dtype, shape->head_dim, st))
+      return hip_fail(e, "context pass launch");
+  } else {
+    if (hipError_t e = launch_attend(a, MODE_VIS, shape->dtype, shape->head_dim, st))
+      return hip_fail(e, "visual pass launch");
+    if (hipError_t e = mark(1)) return hip_fail(e, "event record");
+    if (hipError_t e = launch_attend(a, V ? MODE_TEXT_BOTH : MODE_TEXT_STATS, shape->dtype, shape->head_dim, st))
+      return hip_fail(e, "text pass launch");
+  }
   if (hipError_t e = mark(2)) return hip_fail(e, "event record");
   const MassArgs m = mass_args(shape, layout, plan, a, ws, mass_head, mass_seq, scores);
   if (hipError_t e = launch_mass_finalize(m, st)) return hip_fail(e, "mass finalize launch");
@@ -384,6 +401,15 @@ vp_status vp_select_topk(const vp_shape* shape, const vp_layout* layout, const f
   if (!scores || !k || !vis_idx) return fail(VP_ERR_NULL, "scores, k, vis_idx required");
   if (hipError_t e = launch_topk(topk_args(shape, layout, scores, k, vis_idx), static_cast<hipStream_t>(stream)))
     return hip_fail(e, "top-k launch");
+  return VP_OK;
+}
+
+vp_status vp_step_plan(const vp_shape* shape, const vp_params* params, int32_t* flags) {
+  g_last_error.clear();
+  if (vp_status e = check_shape(shape)) return e;
+  if (vp_status e = check_params(params)) return e;
+  if (!flags) return fail(VP_ERR_NULL, "flags is NULL");
+  *flags = (use_dual(shape) ? VP_PLAN_ONE_CONTEXT_LAUNCH : 0) | (use_tail(shape) ? VP_PLAN_FUSED_TAIL : 0);
   return VP_OK;
 }
 
@@ -464,9 +490,14 @@ vp_status vp_decode_step(const vp_shape* shape, const vp_layout* layout, const v
   };
   const int dt = shape->dtype, hd = shape->head_dim;
   if (hipError_t e = mark(0)) return hip_fail(e, "event record");
-  if (hipError_t e = launch_attend(a, MODE_VIS, dt, hd, st)) return hip_fail(e, "visual pass launch");
-  if (hipError_t e = mark(1)) return hip_fail(e, "event record");
-  if (hipError_t e = launch_attend(a, MODE_TEXT_BOTH, dt, hd, st)) return hip_fail(e, "text pass launch");
+  if (use_dual(shape)) {
+    if (hipError_t e = mark(1)) return hip_fail(e, "event record");
+    if (hipError_t e = launch_attend(a, MODE_DUAL, dt, hd, st)) return hip_fail(e, "context pass launch");
+  } else {
+    if (hipError_t e = launch_attend(a, MODE_VIS, dt, hd, st)) return hip_fail(e, "visual pass launch");
+    if (hipError_t e = mark(1)) return hip_fail(e, "event record");
+    if (hipError_t e = launch_attend(a, MODE_TEXT_BOTH, dt, hd, st)) return hip_fail(e, "text pass launch");
+  }
   if (hipError_t e = mark(2)) return hip_fail(e, "event record");
   const MassArgs m = mass_args(shape, layout, plan, a, ws, mass_head, mass_seq, scores);
   if (use_tail(shape)) {

@@ -490,27 +490,34 @@ struct Pass {
   }
 };
 
+// LDS layout of one pass: per sub-tile a K block, a V block (passes that read
+// V) and a logit stage (visual pass); the total also sets how many work-groups
+// stay resident per CU
 template <int DT, int D, int MODE>
-__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(attend_waves(DT, MODE)))) void attend_kernel(
-    const AttendArgs a) {
+struct PassLds {
   using C = Cfg<DT, D>;
   using P = Pass<DT, D, MODE>;
-  constexpr int NSUB = P::KEPT ? VP_KEPT_SUBS : VP_TILE_SUBS;
-  // per sub-tile: K block, V block (passes that read V), logit stage (visual pass)
-  constexpr int VB = P::ATTN ? C::SUB_ROWS_BYTES : 0;
-  constexpr int SB = P::VIS ? C::STAGE_BYTES : 0;
-  constexpr int SUB = C::SUB_ROWS_BYTES + VB + SB;
-  // LDS per work-group also sets how many stay resident per CU
-  constexpr int LDS_BYTES = max_i(NSUB * SUB, lds_floor(DT, MODE));
-  __shared__ __attribute__((aligned(1024))) unsigned char lds[LDS_BYTES];
+  static constexpr int NSUB = P::KEPT ? VP_KEPT_SUBS : VP_TILE_SUBS;
+  static constexpr int VB = P::ATTN ? C::SUB_ROWS_BYTES : 0;
+  static constexpr int SB = P::VIS ? C::STAGE_BYTES : 0;
+  static constexpr int SUB = C::SUB_ROWS_BYTES + VB + SB;
+  static constexpr int BYTES = max_i(NSUB * SUB, lds_floor(DT, MODE));
+};
+
+// The work of one work-group (part `part` of KV head g of sequence b).
+template <int DT, int D, int MODE>
+__device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* lds, int part, int g, int b) {
+  using C = Cfg<DT, D>;
+  using P = Pass<DT, D, MODE>;
+  using Q = PassLds<DT, D, MODE>;
+  constexpr int NSUB = Q::NSUB;
+  constexpr int VB = Q::VB;
+  constexpr int SUB = Q::SUB;
 
   P s(a);
   s.lane = threadIdx.x;
   s.n16 = s.lane & 15;
   s.a4 = s.lane >> 4;
-  const int b = blockIdx.z;
-  const int g = blockIdx.y;
-  const int part = blockIdx.x;
   s.L = clamp_len(a.seq_len[b], a.max_seq_len);
   s.kept = nullptr;
   if constexpr (P::KEPT) {
@@ -627,11 +634,36 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(attend_waves
   }
 }
 
+template <int DT, int D, int MODE>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(attend_waves(DT, MODE)))) void attend_kernel(
+    const AttendArgs a) {
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[PassLds<DT, D, MODE>::BYTES];
+  attend_body<DT, D, MODE>(a, lds, blockIdx.x, blockIdx.y, blockIdx.z);
+}
+
+// Both context passes in one launch (grid.x = 2 parts): the first half of the
+// work-groups takes the visual role, the second the text role. Used where the
+// batch is small and launch latency, not bandwidth, bounds the step.
+template <int DT, int D>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(attend_waves(DT, MODE_TEXT_BOTH)))) void
+attend_dual_kernel(const AttendArgs a) {
+  constexpr int BYTES = max_i(PassLds<DT, D, MODE_VIS>::BYTES, PassLds<DT, D, MODE_TEXT_BOTH>::BYTES);
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[BYTES];
+  const int x = blockIdx.x;
+  if (x < a.nparts)
+    attend_body<DT, D, MODE_VIS>(a, lds, x, blockIdx.y, blockIdx.z);
+  else
+    attend_body<DT, D, MODE_TEXT_BOTH>(a, lds, x - a.nparts, blockIdx.y, blockIdx.z);
+}
+
 template <int DT, int D>
 hipError_t launch_dd(const AttendArgs& a, int mode, hipStream_t st) {
-  const dim3 grid(mode == MODE_KEPT ? a.nsplit : a.nparts, a.Hkv, a.B);
+  const dim3 grid(mode == MODE_KEPT ? a.nsplit : (mode == MODE_DUAL ? 2 * a.nparts : a.nparts), a.Hkv, a.B);
   const dim3 block(64);
   switch (mode) {
+    case MODE_DUAL:
+      hipLaunchKernelGGL((attend_dual_kernel<DT, D>), grid, block, 0, st, a);
+      break;
     case MODE_VIS:
       hipLaunchKernelGGL((attend_kernel<DT, D, MODE_VIS>), grid, block, 0, st, a);
       break;

@@ -37,7 +37,8 @@ enum Mode : int {
   MODE_TEXT_STATS = 2,  // text rows: Eq. (6)/(2) normaliser statistics
   MODE_TEXT_ATTN = 4,   // text rows: attention partial (reads V)
   MODE_TEXT_BOTH = 6,
-  MODE_KEPT = 8         // kept visual rows: attention partial
+  MODE_KEPT = 8,        // kept visual rows: attention partial
+  MODE_DUAL = 16        // visual pass and text pass (statistics + attention) in one launch
 };
 
 struct AttendArgs {

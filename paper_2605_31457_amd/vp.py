@@ -65,6 +65,7 @@ def lib() -> ctypes.CDLL:
             "vp_budget": ([P(vp_shape), P(vp_layout), P(vp_params), V, V, V], ctypes.c_int),
             "vp_select_topk": ([P(vp_shape), P(vp_layout), V, V, V, V], ctypes.c_int),
             "vp_budget_top_p": ([P(vp_shape), P(vp_layout), V, ctypes.c_float, V, V], ctypes.c_int),
+            "vp_step_plan": ([P(vp_shape), P(vp_params), P(ctypes.c_int32)], ctypes.c_int),
             "vp_sparse_decode_attn": ([P(vp_shape), P(vp_layout), P(vp_params), V, V, V, V, V, V,
                                        ctypes.c_int32, V, S, V], ctypes.c_int),
             "vp_budget_host": ([ctypes.c_double, ctypes.c_int32, P(vp_params)], ctypes.c_int32),
@@ -162,6 +163,16 @@ def vp_decode_step(shape, layout, params, q, K, V, mass_head, mass_seq, scores, 
 def vp_budget(shape, layout, params, mass_seq, k, stream=None):
     _check("vp_budget", lib().vp_budget(ctypes.byref(shape), ctypes.byref(layout), ctypes.byref(params),
                                         _p(mass_seq), _p(k), _stream(stream)))
+
+
+VP_PLAN_ONE_CONTEXT_LAUNCH = 1
+VP_PLAN_FUSED_TAIL = 2
+
+
+def vp_step_plan(shape, params) -> int:
+    flags = ctypes.c_int32()
+    _check("vp_step_plan", lib().vp_step_plan(ctypes.byref(shape), ctypes.byref(params), ctypes.byref(flags)))
+    return flags.value
 
 
 def vp_budget_top_p(shape, layout, scores, p, k, stream=None):
