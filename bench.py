@@ -83,11 +83,12 @@ def algorithmic_bytes(w, ks, lens=None):
     return {"visual": vis, "text": text, "kept": kept}
 
 
-def counter_traffic(cfg: int):
-    """HBM bytes per launch of the text pass from the FETCH_SIZE / WRITE_SIZE
-    counter runs summarised in profiles/ (FETCH_SIZE scaled by a plain copy's
-    reading), or None when they were taken on other kernel sources or another
-    configuration."""
+def counter_traffic(cfg: int, kernel: str):
+    """HBM bytes per launch of the roofline kernel ("text": the text pass;
+    "one_launch": both context passes in one launch) from the FETCH_SIZE /
+    WRITE_SIZE counter runs summarised in profiles/ (FETCH_SIZE scaled by a
+    plain copy's reading), or None when they were taken on other kernel
+    sources, another configuration or another kernel."""
     import glob
     import hashlib
     root = os.path.dirname(os.path.abspath(__file__))
@@ -101,9 +102,10 @@ def counter_traffic(cfg: int):
         h.update(os.path.basename(f).encode())
         with open(f, "rb") as src:
             h.update(src.read())
-    if h.hexdigest() != rec.get("source_sha256") or str(cfg) not in rec.get("configs", {}):
+    entry = rec.get("configs", {}).get(str(cfg))
+    if h.hexdigest() != rec.get("source_sha256") or entry is None or entry.get("kernel") != kernel:
         return None
-    return rec["configs"][str(cfg)]["traffic_bytes"]
+    return entry["traffic_bytes"]
 
 
 def cpu_baseline(w, budget_s: float):
@@ -393,7 +395,8 @@ def main():
                      (f"text pass (attend_kernel<{w.dtype},{w.d},MODE_TEXT_BOTH>: text K/V, "
                       "Eq. (6)/(2) statistics, attention partial)"), "bound": "hbm",
                      "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS,
-                     "traffic": None if one_launch else counter_traffic(cfg), "algorithmic_bytes_per_launch": roof_bytes,
+                     "traffic": counter_traffic(cfg, "one_launch" if one_launch else "text"),
+                     "algorithmic_bytes_per_launch": roof_bytes,
                      "avg_launch_ms": text_ms, "share_of_step": text_ms / ms_per_step},
         "visual_pass": {"achieved": nb["visual"] / (vis_ms * 1e-3) / 1e9, "unit": "GB/s",
                         "algorithmic_bytes_per_launch": nb["visual"], "avg_launch_ms": vis_ms},
