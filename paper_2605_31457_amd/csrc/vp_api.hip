@@ -30,7 +30,7 @@ vp_status hip_fail(hipError_t e, const char* what) {
 }
 
 constexpr int kMaxGroup = 16;
-constexpr int kMaxHq = 1024;
+constexpr int kMaxHq = kMaxHq_;
 constexpr int kMaxBatch = 65535;
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
@@ -137,6 +137,8 @@ AttendArgs attend_args(const vp_shape* s, const vp_layout* l, const vp_params* p
   a.nsplit = plan.nsplit;
   a.kstats = reinterpret_cast<float*>(ws + plan.kstats);
   a.kacc = reinterpret_cast<float*>(ws + plan.kacc);
+  a.sync = reinterpret_cast<uint32_t*>(ws + plan.sync);
+  a.segtab = ws + plan.segtab;
   return a;
 }
 
@@ -224,22 +226,6 @@ MergeArgs merge_args(const vp_shape* s, const vp_layout* l, const Plan& plan, co
   return m;
 }
 
-// The fused per-sequence tail (one work-group per sequence) replaces four
-// launches, but streams a sequence's spilled logits (Hq x N_v floats) through
-// one CU. Measured: it wins at 28 heads x 1296 tokens (145 KB) and loses at
-// 28 x 4096 (459 KB, 16 sequences) and 64 x 6400 (1.6 MB, 8 sequences).
-#ifndef VP_TAIL_MAX_SPILL
-#define VP_TAIL_MAX_SPILL (256 << 10)  // bytes of spilled logits per sequence
-#endif
-#ifndef VP_TAIL_MAX_TOKENS
-#define VP_TAIL_MAX_TOKENS (1 << 17)  // visual tokens over the batch
-#endif
-bool use_tail(const vp_shape* s) {
-  const int64_t spill = static_cast<int64_t>(s->n_q_heads) * s->max_vis * 4;
-  return tail_fits(s->n_q_heads, s->max_vis) && spill <= static_cast<int64_t>(VP_TAIL_MAX_SPILL) &&
-         static_cast<int64_t>(s->batch) * s->max_vis <= static_cast<int64_t>(VP_TAIL_MAX_TOKENS);
-}
-
 // Both context passes in one launch: saves a launch and overlaps the two
 // passes' latency chains where the cache is small; kept apart otherwise, so
 // the visual pass's logit writes stay out of the text pass's read stream.
@@ -256,6 +242,10 @@ vp_status check_budget_cap(const vp_shape* s, const vp_params* p) {
     return fail(VP_ERR_SHAPE, "k_cap %d < largest budget %d for max_vis %d", s->k_cap, max_budget(s, p), s->max_vis);
   return VP_OK;
 }
+
+#ifndef VP_SELECT_WGS
+#define VP_SELECT_WGS 256  // target work-groups of the select launch: one per CU
+#endif
 
 Plan make_plan(const vp_shape& s) {
   Plan p{};
@@ -293,7 +283,21 @@ Plan make_plan(const vp_shape& s) {
   off = align256(off + B * Hq * p.nsplit * 2 * 4);
   p.kacc = off;
   off = align256(off + B * Hq * p.nsplit * d * 4);
+  p.sync = off;
+  off = align256(off + B * 4);
+  p.segtab = off;
+  off = align256(off + B * kSegTableBytes);
   p.total = off;
+  // Select kernel: chunks of whole rounds (a round scores 1024 / lanes-per-token
+  // visual ranks), enough rounds per chunk that the launch has about
+  // VP_SELECT_WGS work-groups, so the spilled logits stream through many CUs.
+  const int64_t tpr = select_tokens_per_round(s.n_q_heads);
+  const int64_t want = static_cast<int64_t>(s.batch) * s.max_vis;
+  int64_t rounds = (want + tpr * VP_SELECT_WGS - 1) / (tpr * VP_SELECT_WGS);
+  if (rounds < 1) rounds = 1;
+  const int64_t chunk = tpr * rounds;
+  p.sel_chunks = static_cast<int>((s.max_vis + chunk - 1) / chunk);
+  p.sel_chunk = p.sel_chunks == 1 ? s.max_vis : static_cast<int>(chunk);
   return p;
 }
 
@@ -409,7 +413,7 @@ vp_status vp_step_plan(const vp_shape* shape, const vp_params* params, int32_t* 
   if (vp_status e = check_shape(shape)) return e;
   if (vp_status e = check_params(params)) return e;
   if (!flags) return fail(VP_ERR_NULL, "flags is NULL");
-  *flags = (use_dual(shape) ? VP_PLAN_ONE_CONTEXT_LAUNCH : 0) | (use_tail(shape) ? VP_PLAN_FUSED_TAIL : 0);
+  *flags = (use_dual(shape) ? VP_PLAN_ONE_CONTEXT_LAUNCH : 0) | (make_plan(*shape).sel_chunks == 1 ? VP_PLAN_FUSED_TAIL : 0);
   return VP_OK;
 }
 
@@ -499,29 +503,19 @@ vp_status vp_decode_step(const vp_shape* shape, const vp_layout* layout, const v
     if (hipError_t e = launch_attend(a, MODE_TEXT_BOTH, dt, hd, st)) return hip_fail(e, "text pass launch");
   }
   if (hipError_t e = mark(2)) return hip_fail(e, "event record");
-  const MassArgs m = mass_args(shape, layout, plan, a, ws, mass_head, mass_seq, scores);
-  if (use_tail(shape)) {
-    TailArgs t{};
-    t.m = m;
-    t.r_lo_bp = params->r_lo_bp;
-    t.r_hi_bp = params->r_hi_bp;
-    t.clamp = params->clamp;
-    t.k_cap = shape->k_cap;
-    t.k = k;
-    t.vis_idx = vis_idx;
-    if (hipError_t e = launch_tail(t, st)) return hip_fail(e, "tail launch");
-  } else {
-    if (hipError_t e = launch_mass_finalize(m, st)) return hip_fail(e, "mass finalize launch");
-    if (hipError_t e = launch_scores(m, st)) return hip_fail(e, "scores launch");
-    // the top-k kernel takes the Eq. (7) budget itself (one launch fewer)
-    TopkArgs tk = topk_args(shape, layout, scores, k, vis_idx);
-    tk.mass_seq = mass_seq;
-    tk.k_out = k;
-    tk.r_lo_bp = params->r_lo_bp;
-    tk.r_hi_bp = params->r_hi_bp;
-    tk.clamp = params->clamp;
-    if (hipError_t e = launch_topk(tk, st)) return hip_fail(e, "top-k launch");
-  }
+  SelectArgs t{};
+  t.m = mass_args(shape, layout, plan, a, ws, mass_head, mass_seq, scores);
+  t.r_lo_bp = params->r_lo_bp;
+  t.r_hi_bp = params->r_hi_bp;
+  t.clamp = params->clamp;
+  t.k_cap = shape->k_cap;
+  t.k = k;
+  t.vis_idx = vis_idx;
+  t.chunk = plan.sel_chunk;
+  t.nchunks = plan.sel_chunks;
+  t.sync = a.sync;
+  t.segtab = a.segtab;
+  if (hipError_t e = launch_select(t, st)) return hip_fail(e, "select launch");
   if (hipError_t e = mark(3)) return hip_fail(e, "event record");
   if (hipError_t e = launch_attend(a, MODE_KEPT, dt, hd, st)) return hip_fail(e, "kept pass launch");
   if (hipError_t e = mark(4)) return hip_fail(e, "event record");

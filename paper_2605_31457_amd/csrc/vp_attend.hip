@@ -634,10 +634,29 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
   }
 }
 
+// The extra work-group of a launch with the visual role (x = its last index,
+// KV head 0): the sequence's clipped segment table (positions and visual
+// ranks) for the select kernel, and a new step's arrival counter at zero.
+__device__ __forceinline__ void step_setup(const AttendArgs& a, int g, int b) {
+  if (g != 0) return;
+  const int lane = threadIdx.x;
+  if (a.sync && lane == 0) a.sync[b] = 0u;
+  if (a.segtab) {
+    const int L = clamp_len(a.seq_len[b], a.max_seq_len);
+    const int o0 = a.seg_off[b];
+    load_segments(static_cast<SegTable*>(a.segtab)[b], a.seg + 2 * static_cast<long>(o0), a.seg_off[b + 1] - o0, L,
+                  lane);
+  }
+}
+
 template <int DT, int D, int MODE>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(attend_waves(DT, MODE)))) void attend_kernel(
     const AttendArgs a) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[PassLds<DT, D, MODE>::BYTES];
+  if (MODE == MODE_VIS && static_cast<int>(blockIdx.x) == a.nparts) {
+    step_setup(a, blockIdx.y, blockIdx.z);
+    return;
+  }
   attend_body<DT, D, MODE>(a, lds, blockIdx.x, blockIdx.y, blockIdx.z);
 }
 
@@ -652,13 +671,18 @@ attend_dual_kernel(const AttendArgs a) {
   const int x = blockIdx.x;
   if (x < a.nparts)
     attend_body<DT, D, MODE_VIS>(a, lds, x, blockIdx.y, blockIdx.z);
-  else
+  else if (x < 2 * a.nparts)
     attend_body<DT, D, MODE_TEXT_BOTH>(a, lds, x - a.nparts, blockIdx.y, blockIdx.z);
+  else
+    step_setup(a, blockIdx.y, blockIdx.z);
 }
 
 template <int DT, int D>
 hipError_t launch_dd(const AttendArgs& a, int mode, hipStream_t st) {
-  const dim3 grid(mode == MODE_KEPT ? a.nsplit : (mode == MODE_DUAL ? 2 * a.nparts : a.nparts), a.Hkv, a.B);
+  // launches with the visual role carry one more work-group per sequence (step_setup)
+  const int gx = mode == MODE_KEPT ? a.nsplit
+                                   : (mode == MODE_DUAL ? 2 * a.nparts + 1 : (mode == MODE_VIS ? a.nparts + 1 : a.nparts));
+  const dim3 grid(gx, a.Hkv, a.B);
   const dim3 block(64);
   switch (mode) {
     case MODE_DUAL:

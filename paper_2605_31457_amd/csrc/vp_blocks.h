@@ -9,144 +9,287 @@
 namespace vp {
 
 // ---------------------------------------------------------------------------
-// mass reduction
+// Per-head reduction of the context pass's statistics (Eq. (5)/(6), with the
+// head mean and head max of Sec. 4.3, and the Eq. (2) normaliser)
 // ---------------------------------------------------------------------------
-constexpr int kMassThreads = 512;  // threads that take part in reduce_mass
+constexpr int kSelThreads = 1024;  // threads of every per-sequence block below
+constexpr int kSelWaves = kSelThreads / 64;
+
+// Per-head results in LDS (dynamic shared memory, Hq entries each; see
+// head_lds_bytes): the head's maximum logit (log2 domain), the reciprocal
+// of its Eq. (2) normaliser and its visual mass m^vis_{t,h}; then the head mean
+// M_vis and head max M_vis,max as fp32.
+struct HeadLds {
+  float* hm;
+  float* hinv;
+  double* mass;
+  float* mseq;  // [0] M_vis, [1] M_vis,max
+};
+__host__ __device__ inline int head_lds_bytes(int Hq) {
+  return ((2 * Hq * 4 + 7) / 8) * 8 + Hq * 8 + 16;
+}
+__device__ __forceinline__ HeadLds head_lds(unsigned char* base, int Hq) {
+  HeadLds h;
+  h.hm = reinterpret_cast<float*>(base);
+  h.hinv = h.hm + Hq;
+  h.mass = reinterpret_cast<double*>(base + ((2 * Hq * 4 + 7) / 8) * 8);
+  h.mseq = reinterpret_cast<float*>(h.mass + Hq);
+  return h;
+}
+
+// Cross-lane all-reduce inside aligned groups of `width` lanes (a power of two
+// <= 64, uniform): butterflies on the DPP network (quad permutes, half-row and
+// row mirrors), then a swizzle across 16 lanes and a permute across 32.
+template <typename Op>
+__device__ __forceinline__ uint32_t group_allreduce_u32(uint32_t v, int width, Op op) {
+  auto dpp = [](uint32_t x, int ctrl) -> uint32_t {
+    switch (ctrl) {
+      case 0xB1: return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0xB1, 0xf, 0xf, false));
+      case 0x4E: return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x4E, 0xf, 0xf, false));
+      case 0x141: return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x141, 0xf, 0xf, false));
+      default: return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x140, 0xf, 0xf, false));
+    }
+  };
+  if (width > 1) v = op(v, dpp(v, 0xB1));   // quad_perm [1,0,3,2]: lane ^ 1
+  if (width > 2) v = op(v, dpp(v, 0x4E));   // quad_perm [2,3,0,1]: lane ^ 2
+  if (width > 4) v = op(v, dpp(v, 0x141));  // row_half_mirror: the other quad of 8
+  if (width > 8) v = op(v, dpp(v, 0x140));  // row_mirror: the other half of 16
+  if (width > 16) v = op(v, static_cast<uint32_t>(__builtin_amdgcn_ds_swizzle(static_cast<int>(v), 0x401F)));  // lane ^ 16
+  if (width > 32) v = op(v, static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), 32)));
+  return v;
+}
+__device__ __forceinline__ float group_max_f32(float v, int width) {
+  return __uint_as_float(group_allreduce_u32(__float_as_uint(v), width, [](uint32_t a, uint32_t b) {
+    return __float_as_uint(fmaxf(__uint_as_float(a), __uint_as_float(b)));
+  }));
+}
+// double sums: the two halves travel separately, the add happens in double
+__device__ __forceinline__ double group_sum_f64(double v, int width) {
+  auto step = [&](auto mov) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = mov(static_cast<uint32_t>(u)), hi = mov(static_cast<uint32_t>(u >> 32));
+    v += __builtin_bit_cast(double, (static_cast<uint64_t>(hi) << 32) | lo);
+  };
+  if (width > 1) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0xB1, 0xf, 0xf, false)); });
+  if (width > 2) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x4E, 0xf, 0xf, false)); });
+  if (width > 4) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x141, 0xf, 0xf, false)); });
+  if (width > 8) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x140, 0xf, 0xf, false)); });
+  if (width > 16) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_ds_swizzle(static_cast<int>(x), 0x401F)); });
+  if (width > 32) step([](uint32_t x) { return static_cast<uint32_t>(__shfl_xor(static_cast<int>(x), 32)); });
+  return v;
+}
+__device__ __forceinline__ double group_max_f64(double v, int width) {
+  auto step = [&](auto mov) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = mov(static_cast<uint32_t>(u)), hi = mov(static_cast<uint32_t>(u >> 32));
+    const double o = __builtin_bit_cast(double, (static_cast<uint64_t>(hi) << 32) | lo);
+    v = o > v ? o : v;
+  };
+  if (width > 1) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0xB1, 0xf, 0xf, false)); });
+  if (width > 2) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x4E, 0xf, 0xf, false)); });
+  if (width > 4) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x141, 0xf, 0xf, false)); });
+  if (width > 8) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x140, 0xf, 0xf, false)); });
+  if (width > 16) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_ds_swizzle(static_cast<int>(x), 0x401F)); });
+  if (width > 32) step([](uint32_t x) { return static_cast<uint32_t>(__shfl_xor(static_cast<int>(x), 32)); });
+  return v;
+}
+
+// Lanes that share one head in reduce_heads: the fewest (a power of two) whose
+// four parts each cover the part capacity, at most 64 and at most
+// kSelThreads / Hq.
+__device__ __forceinline__ int lanes_per_head(int Hq, int nparts) {
+  int l = 1;
+  while (l < 64 && 4 * l < nparts && 2 * l * Hq <= kSelThreads) l <<= 1;
+  return l;
+}
 
 // Merges the per-part statistics of sequence b (visual and text rows, kept
 // apart by the context pass) for every head onto the head's maximum, in
-// double with fixed-order reductions. Threads 0..kMassThreads-1 of the block
-// call it (all of them; others may skip it but must reach the same barriers).
-// Every head gets a group of `lph` lanes (a power of two, lph * Hq <= 512 when
-// possible) that strides over the parts.
-// Writes m^{vis}_{t,h}, the per-head (max, Eq. (2) normaliser) to a.head and,
-// when hm/hinv are given, to LDS as (max, 1/normaliser); returns (in thread 0)
-// M_vis,max and writes (M_vis, M_vis,max) to a.mass_seq.
-// s_mass: kMassThreads doubles of LDS. Contains two block barriers.
-__device__ __forceinline__ float reduce_mass(const MassArgs& a, int b, int tid, double* s_mass, float* hm,
-                                             float* hinv) {
-  const int L = clamp_len(a.seq_len[b], a.max_seq_len);
-  const int nv = parts_used(L, a.nparts);
-  int lph = 64;
-  while (lph > 1 && lph * a.Hq > kMassThreads) lph >>= 1;
-  const int hpr = kMassThreads / lph;  // heads per round
+// double with fixed-order reductions, by a kSelThreads block (every thread
+// calls it; two block barriers). Every head gets a group of lanes (a power of
+// two, lanes_per_head; one round of heads since Hq <= kSelThreads) that
+// strides over the parts and reduces on the DPP network. When the part capacity allows, each lane's (up to four) parts are
+// requested at entry at addresses that do not depend on the sequence length,
+// `between()` runs while they are in flight (the caller's other independent
+// loads), and the maximum and the sums then come from registers; more parts
+// take two sweeps with the same arithmetic order. The head mean and head max
+// are summed by one wave in a fixed order.
+// L is the sequence's clamped length. Fills `hs`; with `write_out` also writes
+// m^vis_{t,h} (mass_head), the per-head (max, Eq. (2) normaliser) (head) and
+// (M_vis, M_vis,max) (mass_seq).
+namespace detail {
+constexpr int kPartsPerLane = 4;
+// parts c0, c0 + step, ... of one head (slots past `cap` read as empty parts)
+__device__ __forceinline__ void load_parts(float4 (&v)[kPartsPerLane], float4 (&t)[kPartsPerLane], const float4* st,
+                                           bool on, int c0, int step, int cap) {
+  const float4 empty = make_float4(kNegInf, 0.f, 0.f, 0.f);
+#pragma unroll
+  for (int u = 0; u < kPartsPerLane; ++u) {
+    const int c = c0 + u * step;
+    const bool ok = on && c < cap;
+    const int cc = ok ? c : 0;  // part 0 always exists; its duplicate loads share one line
+    const float4 x = st[2 * cc];
+    const float4 y = st[2 * cc + 1];
+    v[u] = ok ? x : empty;
+    t[u] = ok ? y : empty;
+  }
+}
+__device__ __forceinline__ float max_parts(float m, const float4 (&v)[kPartsPerLane],
+                                           const float4 (&t)[kPartsPerLane], bool on, int c0, int step, int nv) {
+#pragma unroll
+  for (int u = 0; u < kPartsPerLane; ++u)
+    if (on && c0 + u * step < nv) m = fmaxf(m, fmaxf(v[u].x, t[u].x));
+  return m;
+}
+// Eq. (2) normaliser Ls, Eq. (6) denominator Lm and Eq. (5) numerator Vm of
+// the parts, rescaled to the head maximum m (double accumulation)
+__device__ __forceinline__ void sum_parts(double& Ls, double& Lm, double& Vm, const float4 (&v)[kPartsPerLane],
+                                          const float4 (&t)[kPartsPerLane], bool on, int c0, int step, int nv,
+                                          float m, float inv_tau_m, float inv_tau_s) {
+#pragma unroll
+  for (int u = 0; u < kPartsPerLane; ++u) {
+    const bool ok = on && c0 + u * step < nv;
+    const bool okv = ok && v[u].x != kNegInf;
+    const bool okt = ok && t[u].x != kNegInf;
+    const float dv = okv ? v[u].x - m : 0.f;
+    const float dt = okt ? t[u].x - m : 0.f;
+    const double fm = okv ? static_cast<double>(fast_exp2(dv * inv_tau_m)) : 0.0;
+    const double fs = okv ? static_cast<double>(fast_exp2(dv * inv_tau_s)) : 0.0;
+    const double gm = okt ? static_cast<double>(fast_exp2(dt * inv_tau_m)) : 0.0;
+    const double gs = okt ? static_cast<double>(fast_exp2(dt * inv_tau_s)) : 0.0;
+    Ls += fs * (okv ? v[u].y : 0.f);
+    Lm += fm * (okv ? v[u].z : 0.f);
+    Vm += fm * (okv ? v[u].z : 0.f);
+    Ls += gs * (okt ? t[u].w : 0.f);
+    Lm += gm * (okt ? t[u].z : 0.f);
+  }
+}
+}  // namespace detail
+
+template <typename Between>
+__device__ __forceinline__ void reduce_heads(const MassArgs& a, int b, int L, int tid, const HeadLds& hs,
+                                             bool write_out, Between between) {
+  using namespace detail;
+  const int lph = lanes_per_head(a.Hq, a.nparts);
   const int sub = tid % lph;
-  const bool member = tid < kMassThreads;
-  double msum = 0.0, mmax = 0.0;
-  for (int h0 = 0; h0 < a.Hq; h0 += hpr) {
-    const int h = h0 + tid / lph;
-    const bool on = member && h < a.Hq;
-    // per part: [0] visual {m, Ls, Lm, -}, [1] text {m, l, Lm, Ls}
-    const float4* st =
-        reinterpret_cast<const float4*>(a.stats + (static_cast<size_t>(b) * a.Hq + (on ? h : 0)) * a.nparts * 8);
-    // four parts per lane per round, loaded before use (clamped indices keep
-    // every load in bounds; selects, not branches, drop the extra ones)
-    constexpr int U = 4;
-    float m = kNegInf;
-    if (on) {
-      for (int c0 = sub; c0 < nv; c0 += U * lph) {
-        float x[2 * U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int c = min(c0 + u * lph, nv - 1);
-          x[2 * u] = st[2 * c].x;
-          x[2 * u + 1] = st[2 * c + 1].x;
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-          if (c0 + u * lph < nv) m = fmaxf(m, fmaxf(x[2 * u], x[2 * u + 1]));
-      }
+  const int h = tid / lph;
+  const bool on = h < a.Hq;
+  constexpr int U = kPartsPerLane;
+  // per part: [0] visual {m, Ls, Lm, -}, [1] text {m, l, Lm, Ls}
+  const float4* st =
+      reinterpret_cast<const float4*>(a.stats + (static_cast<size_t>(b) * a.Hq + (on ? h : 0)) * a.nparts * 8);
+  const bool one_round = a.nparts <= U * lph;
+  float4 v[U], t[U];
+  if (one_round) load_parts(v, t, st, on, sub, lph, a.nparts);
+  between();
+  const int nv = parts_used(L, a.nparts);
+  float m = kNegInf;
+  double Ls = 0.0, Lm = 0.0, Vm = 0.0;
+  if (one_round) {
+    m = max_parts(m, v, t, on, sub, lph, nv);
+    m = group_max_f32(m, lph);
+    sum_parts(Ls, Lm, Vm, v, t, on, sub, lph, nv, m, a.inv_tau_m, a.inv_tau_s);
+  } else {
+    for (int c0 = sub; c0 < nv; c0 += U * lph) {
+      load_parts(v, t, st, on, c0, lph, nv);
+      m = max_parts(m, v, t, on, c0, lph, nv);
     }
-    for (int off = 1; off < lph; off <<= 1) m = fmaxf(m, __shfl_xor(m, off));
-    double Ls = 0.0, Lm = 0.0, Vm = 0.0;
-    if (on) {
-      for (int c0 = sub; c0 < nv; c0 += U * lph) {
-        float4 v[U], t[U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const int c = min(c0 + u * lph, nv - 1);
-          v[u] = st[2 * c];
-          t[u] = st[2 * c + 1];
-        }
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-          const bool ok = c0 + u * lph < nv;
-          const bool okv = ok && v[u].x != kNegInf;
-          const bool okt = ok && t[u].x != kNegInf;
-          const float dv = okv ? v[u].x - m : 0.f;
-          const float dt = okt ? t[u].x - m : 0.f;
-          const double fm = okv ? static_cast<double>(fast_exp2(dv * a.inv_tau_m)) : 0.0;
-          const double fs = okv ? static_cast<double>(fast_exp2(dv * a.inv_tau_s)) : 0.0;
-          const double gm = okt ? static_cast<double>(fast_exp2(dt * a.inv_tau_m)) : 0.0;
-          const double gs = okt ? static_cast<double>(fast_exp2(dt * a.inv_tau_s)) : 0.0;
-          Ls += fs * v[u].y;
-          Lm += fm * v[u].z;
-          Vm += fm * v[u].z;
-          Ls += gs * t[u].w;
-          Lm += gm * t[u].z;
-        }
-      }
+    m = group_max_f32(m, lph);
+    for (int c0 = sub; c0 < nv; c0 += U * lph) {
+      load_parts(v, t, st, on, c0, lph, nv);
+      sum_parts(Ls, Lm, Vm, v, t, on, c0, lph, nv, m, a.inv_tau_m, a.inv_tau_s);
     }
-    for (int off = 1; off < lph; off <<= 1) {
-      Ls += __shfl_xor(Ls, off);
-      Lm += __shfl_xor(Lm, off);
-      Vm += __shfl_xor(Vm, off);
-    }
+  }
+  Ls = group_sum_f64(Ls, lph);
+  Lm = group_sum_f64(Lm, lph);
+  Vm = group_sum_f64(Vm, lph);
+  if (on && sub == 0) {
     const double mass = Lm > 0.0 ? Vm / Lm : 0.0;
-    if (on && sub == 0) {
-      const float ls = static_cast<float>(Ls);
+    const float ls = static_cast<float>(Ls);
+    hs.hm[h] = m;
+    hs.hinv[h] = ls > 0.f ? 1.0f / ls : 0.f;
+    hs.mass[h] = mass;
+    if (write_out) {
       a.mass_head[static_cast<size_t>(b) * a.Hq + h] = static_cast<float>(mass);
       *reinterpret_cast<float2*>(a.head + (static_cast<size_t>(b) * a.Hq + h) * 2) = make_float2(m, ls);
-      if (hm) {
-        hm[h] = m;
-        hinv[h] = ls > 0.f ? 1.0f / ls : 0.f;
-      }
-      s_mass[tid / lph] = mass;
     }
-    __syncthreads();
+  }
+  __syncthreads();
+  // head mean and head max: lane j takes heads j, j + 64, ... in order, then a fixed butterfly
+  if (tid < 64) {
+    double msum = 0.0, mmax = 0.0;
+    for (int hh = tid; hh < a.Hq; hh += 64) {
+      msum += hs.mass[hh];
+      mmax = hs.mass[hh] > mmax ? hs.mass[hh] : mmax;
+    }
+    msum = group_sum_f64(msum, 64);
+    mmax = group_max_f64(mmax, 64);
     if (tid == 0) {
-      const int nh = min(hpr, a.Hq - h0);
-      for (int i = 0; i < nh; ++i) {
-        msum += s_mass[i];
-        mmax = s_mass[i] > mmax ? s_mass[i] : mmax;
+      const float mv = static_cast<float>(msum / a.Hq);
+      const float mx = static_cast<float>(mmax);
+      hs.mseq[0] = mv;
+      hs.mseq[1] = mx;
+      if (write_out) {
+        a.mass_seq[2 * b + 0] = mv;
+        a.mass_seq[2 * b + 1] = mx;
       }
     }
-    __syncthreads();
   }
-  float mx = 0.f;
-  if (tid == 0) {
-    mx = static_cast<float>(mmax);
-    a.mass_seq[2 * b + 0] = static_cast<float>(msum / a.Hq);
-    a.mass_seq[2 * b + 1] = mx;
-  }
-  return mx;
+  __syncthreads();
 }
 
+// One head's term of the Eq. (2) score of a visual token: s + 2^((z - m)/tau) / Ls,
+// with z the token's logit and m, 1/Ls the head's maximum and normaliser
+// (explicit fma, so every kernel that scores rounds the same way).
+__device__ __forceinline__ float score_term(float s, float z, float hm, float hinv, float inv_tau) {
+  return fmaf(fast_exp2((z - hm) * inv_tau), hinv, s);
+}
+
+// Summation order of the Eq. (2) head sum, shared by every kernel that scores:
+// the Hq heads are cut into `ng` consecutive groups of `hpg` heads (ng a power
+// of two <= 64, so the lanes of one token sit in one wave); each group is
+// summed in head order from zero, then the group sums are added in group order
+// and the total is divided by Hq.
+struct ScoreGroups {
+  int ng;   // groups (lanes per token)
+  int hpg;  // heads per group
+};
+__host__ __device__ inline ScoreGroups score_groups(int Hq) {
+  int ng = 1;
+  while (ng < 64 && ng * 8 < Hq) ng <<= 1;
+  return ScoreGroups{ng, (Hq + ng - 1) / ng};
+}
+constexpr int kMaxHeadsPerGroup = kMaxHq_ / 64;
+
 // ---------------------------------------------------------------------------
-// Eq. (2) score of the visual token at cache position pos of sequence b:
-// S = (1/Hq) sum_h 2^((z_h - m_h) / tau_score) / Ls_h from the spilled logits,
-// with 32 loads in flight at a time. hm/hinv: per-head max and 1/Ls.
+// Eq. (2) score of the visual token at cache position pos of sequence b by one
+// thread (the same groups and order as the select kernel's lanes):
+// S = (1/Hq) sum_h 2^((z_h - m_h) / tau_score) / Ls_h from the spilled logits.
+// hm/hinv: per-head max and 1/Ls.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float token_score(const MassArgs& a, int b, int pos, const float* hm, const float* hinv) {
   const float* z = a.zs + static_cast<size_t>(b) * a.Hq * a.zs_stride + pos;
-  constexpr int kBatch = 32;
-  float s = 0.f;
-  for (int h0 = 0; h0 < a.Hq; h0 += kBatch) {
-    float zz[kBatch];
+  const ScoreGroups sg = score_groups(a.Hq);
+  float total = 0.f;
+  for (int g = 0; g < sg.ng; ++g) {
+    const int h0 = g * sg.hpg;
+    const int h1 = min(a.Hq, h0 + sg.hpg);
+    float zz[kMaxHeadsPerGroup];
 #pragma unroll
-    for (int j = 0; j < kBatch; ++j) zz[j] = z[static_cast<size_t>(min(h0 + j, a.Hq - 1)) * a.zs_stride];
+    for (int j = 0; j < kMaxHeadsPerGroup; ++j)
+      if (h0 + j < h1) zz[j] = z[static_cast<size_t>(h0 + j) * a.zs_stride];
+    float p = 0.f;
 #pragma unroll
-    for (int j = 0; j < kBatch; ++j)
-      if (h0 + j < a.Hq) s += fast_exp2((zz[j] - hm[h0 + j]) * a.inv_tau_s) * hinv[h0 + j];
+    for (int j = 0; j < kMaxHeadsPerGroup; ++j)
+      if (h0 + j < h1) p = score_term(p, zz[j], hm[h0 + j], hinv[h0 + j], a.inv_tau_s);
+    total = g == 0 ? p : total + p;
   }
-  return s / static_cast<float>(a.Hq);
+  return total / static_cast<float>(a.Hq);
 }
 
 // ---------------------------------------------------------------------------
 // Eq. (3) selection by one 1024-thread block
 // ---------------------------------------------------------------------------
-constexpr int kSelThreads = 1024;
-constexpr int kSelWaves = kSelThreads / 64;
 constexpr int kDigitBits = 13;
 constexpr int kBins = 1 << kDigitBits;
 constexpr int kBinsPerThread = kBins / kSelThreads;
@@ -154,6 +297,19 @@ constexpr int kBinsPerThread = kBins / kSelThreads;
 // thread's own run of counters starts on a different bank for every lane
 constexpr int kHistWords = kBins + kBins / kBinsPerThread;
 __device__ __forceinline__ int hslot(int bin) { return bin + bin / kBinsPerThread; }
+
+// Inclusive prefix sum over the 64 lanes of a wave on the DPP network: shifts
+// by 1, 2, 4, 8 inside each 16-lane row, then the row totals carried into the
+// later rows by the lane-15 and lane-31 broadcasts.
+__device__ __forceinline__ int wave_incl_sum(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xf, 0xf, false);  // row_shr:1
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xf, 0xf, false);  // row_shr:2
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xf, 0xf, false);  // row_shr:4
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xf, 0xf, false);  // row_shr:8
+  v += __builtin_amdgcn_update_dpp(0, v, 0x142, 0xa, 0xf, false);  // row_bcast:15 into rows 1 and 3
+  v += __builtin_amdgcn_update_dpp(0, v, 0x143, 0xc, 0xf, false);  // row_bcast:31 into rows 2 and 3
+  return v;
+}
 
 // order-preserving map of a float to a 32-bit key
 __device__ __forceinline__ uint32_t order_key(float f) {
@@ -176,16 +332,14 @@ struct SelectShared {
   uint32_t wmax[kSelWaves];
   uint32_t digit;
   int above;
+  int dcount;
 };
 
 // Block min/max of per-thread (kmin, kmax); contains one barrier.
 __device__ __forceinline__ void block_key_range(SelectShared& sh, uint32_t& kmin, uint32_t& kmax, int lane,
                                                 int wid) {
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) {
-    kmin = min(kmin, static_cast<uint32_t>(__shfl_xor(static_cast<int>(kmin), off)));
-    kmax = max(kmax, static_cast<uint32_t>(__shfl_xor(static_cast<int>(kmax), off)));
-  }
+  kmin = __ockl_wfred_min_u32(kmin);
+  kmax = __ockl_wfred_max_u32(kmax);
   if (lane == 0) {
     sh.wmin[wid] = kmin;
     sh.wmax[wid] = kmax;
@@ -204,8 +358,11 @@ __device__ __forceinline__ void block_key_range(SelectShared& sh, uint32_t& kmin
 // next 13 bits of (key - lo) into 8192 counters; a block suffix scan finds the
 // digit holding the k-th largest key and the live range shrinks to it. Digits
 // are relative to the live range, so clustered scores still spread over many
-// counters. Returns the k-th largest key T; `need` becomes the number of keys
-// equal to T that are kept. sh.hist must be zero on entry (it is zero on exit).
+// counters. When every candidate of that digit is kept (its count equals the
+// number still needed) the selection is complete: the kept keys are exactly
+// those >= the digit's lower bound. Returns T with `need` such that the kept
+// keys are every key > T and the first `need` keys equal to T (need = 0 after
+// an early finish). sh.hist must be zero on entry (it is zero on exit).
 // Three barriers per pass; the owner of a counter clears it while scanning.
 template <typename KeyAt>
 __device__ __forceinline__ uint32_t radix_select(SelectShared& sh, KeyAt key_at, int n, int& need, uint32_t kmin,
@@ -230,12 +387,7 @@ __device__ __forceinline__ uint32_t radix_select(SelectShared& sh, KeyAt key_at,
       sh.hist[hslot(bin)] = 0;
       local += c[j];
     }
-    int incl = local;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int v = __shfl_up(incl, off);
-      if (lane >= off) incl += v;
-    }
+    int incl = wave_incl_sum(local);
     if (lane == 63) sh.wcnt[wid] = incl;
     __syncthreads();
     for (int v = 0; v < wid; ++v) incl += sh.wcnt[v];
@@ -247,6 +399,7 @@ __device__ __forceinline__ uint32_t radix_select(SelectShared& sh, KeyAt key_at,
         if (acc < need && need <= acc + c[j]) {
           sh.digit = static_cast<uint32_t>(kBins - 1 - kBinsPerThread * tid - j);
           sh.above = acc;
+          sh.dcount = c[j];
         }
         acc += c[j];
       }
@@ -255,6 +408,10 @@ __device__ __forceinline__ uint32_t radix_select(SelectShared& sh, KeyAt key_at,
     const uint32_t d = sh.digit;
     need -= sh.above;
     lo += d << shift;
+    if (sh.dcount == need && lo > 0u) {  // the whole digit is kept
+      need = 0;
+      return lo - 1u;
+    }
     const uint32_t width = (shift >= 32 ? 0xffffffffu : ((1u << shift) - 1u));
     span = min(span - (d << shift), width);
     if (shift == 0) break;
@@ -265,9 +422,14 @@ __device__ __forceinline__ uint32_t radix_select(SelectShared& sh, KeyAt key_at,
 
 // Ordered compaction: writes the positions of the k selected visual ranks
 // (every key > T and the first `need` keys == T; with take_all every key) in
-// ascending order to out[0..k). Wave w owns a contiguous block of ranks; a
-// first sweep counts, one block scan gives every wave its offsets, a second
-// sweep writes. One barrier.
+// ascending order to out[0..k). Wave w owns a contiguous block of ranks. A
+// first sweep counts its keys > T and == T per lane (no cross-lane work in the
+// loop), one block scan gives every wave its offsets, a second sweep finds the
+// kept ranks 64 at a time (ballots, four chunks per step so the LDS reads
+// overlap) and stages them in LDS (the radix counters, free by then); a last
+// pass turns ranks into cache positions and writes them out, so the
+// segment-table search runs once per kept token. When k exceeds the staging
+// room the second sweep writes positions directly. Three barriers.
 template <typename KeyAt>
 __device__ __forceinline__ void ordered_compaction(SelectShared& sh, const SegTable& tab, KeyAt key_at, int n, int k,
                                                    int need, uint32_t T, bool take_all, int32_t* out, int lane,
@@ -276,12 +438,15 @@ __device__ __forceinline__ void ordered_compaction(SelectShared& sh, const SegTa
   const int r0 = min(n, wid * per), r1 = min(n, r0 + per);
   int cgt = 0, ceq = 0;
   if (!take_all) {
-    for (int base = r0; base < r1; base += 64) {
-      const int i = base + lane;
-      const uint32_t u = i < r1 ? key_at(i) : 0u;
-      cgt += __popcll(__ballot(i < r1 && u > T));
-      ceq += __popcll(__ballot(i < r1 && u == T));
+    for (int i = r0 + lane; i < r1; i += 64) {
+      const uint32_t u = key_at(i);
+      cgt += u > T ? 1 : 0;
+      ceq += u == T ? 1 : 0;
     }
+    cgt = __ockl_wfred_add_i32(cgt);
+    ceq = __ockl_wfred_add_i32(ceq);
+  } else {
+    cgt = r1 - r0;
   }
   if (lane == 0) {
     sh.gt[wid] = cgt;
@@ -293,22 +458,40 @@ __device__ __forceinline__ void ordered_compaction(SelectShared& sh, const SegTa
     gt_run += sh.gt[v];
     eq_run += sh.eq[v];
   }
-  for (int base = r0; base < r1; base += 64) {
-    const int i = base + lane;
-    const bool in = i < r1;
-    const uint32_t u = (in && !take_all) ? key_at(i) : 0u;
-    const bool gt = in && (take_all || u > T);
-    const bool eq = in && !take_all && u == T;
-    const uint64_t bgt = __ballot(gt);
-    const uint64_t beq = __ballot(eq);
-    const int g_b = gt_run + lanes_below(bgt);
-    const int e_b = eq_run + lanes_below(beq);
-    if (gt || (eq && e_b < need)) {
-      const int o = g_b + min(need, e_b);
-      if (o < k) out[o] = rank_to_pos(tab, i);
+  const bool staged = k <= kHistWords;
+  uint32_t* stage = sh.hist;
+  constexpr int Q = 4;  // chunks of 64 ranks per step
+  for (int base = r0; base < r1; base += Q * 64) {
+    uint32_t u[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int i = base + q * 64 + lane;
+      u[q] = (i < r1 && !take_all) ? key_at(i) : 0u;
     }
-    gt_run += __popcll(bgt);
-    eq_run += __popcll(beq);
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int i = base + q * 64 + lane;
+      const bool in = i < r1;
+      const bool gt = in && (take_all || u[q] > T);
+      const bool eq = in && !take_all && u[q] == T;
+      const uint64_t bgt = __ballot(gt);
+      const uint64_t beq = __ballot(eq);
+      const int g_b = gt_run + lanes_below(bgt);
+      const int e_b = eq_run + lanes_below(beq);
+      if (gt || (eq && e_b < need)) {
+        const int o = g_b + min(need, e_b);
+        if (o < k) {
+          if (staged) stage[o] = static_cast<uint32_t>(i);
+          else out[o] = rank_to_pos(tab, i);
+        }
+      }
+      gt_run += __popcll(bgt);
+      eq_run += __popcll(beq);
+    }
+  }
+  if (staged) {
+    __syncthreads();
+    for (int o = wid * 64 + lane; o < k; o += kSelThreads) out[o] = rank_to_pos(tab, static_cast<int>(stage[o]));
   }
 }
 

@@ -5,6 +5,8 @@
 
 #include <cstdint>
 
+#include "vp_internal.h"
+
 namespace vp {
 
 constexpr float kLog2e = 1.4426950408889634f;
@@ -98,7 +100,7 @@ constexpr int kMaxSegs = 256;  // visual segments read per sequence
 // The visual segments of one sequence in LDS, clipped exactly as SegWalker
 // clips them: segment s covers positions [st[s], en[s]) and visual ranks
 // [rk[s], rk[s + 1]); rk[n] is the sequence's visual count.
-struct SegTable {
+struct alignas(16) SegTable {
   int st[kMaxSegs];
   int en[kMaxSegs];
   int rk[kMaxSegs + 1];
@@ -170,6 +172,8 @@ __device__ __forceinline__ void load_segments(SegTable& t, const int32_t* seg, i
   if (lane == 63) t.rk[nseg] = rinc;
   if (lane == 0) t.n = nseg;
 }
+
+static_assert(sizeof(SegTable) == kSegTableBytes, "segment table size");
 
 // position of visual rank r (0 <= r < t.rk[t.n]): binary search on the ranks
 __device__ __forceinline__ int rank_to_pos(const SegTable& t, int r) {

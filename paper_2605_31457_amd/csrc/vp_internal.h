@@ -10,6 +10,10 @@
 
 namespace vp {
 
+constexpr int kMaxHq_ = 1024;  // query heads supported
+// bytes of one sequence's segment table (SegTable: 256 starts, 256 ends, 257 ranks, count; 16-byte aligned)
+constexpr size_t kSegTableBytes = 3088;
+
 // Work decomposition and workspace carving, a pure function of the shape.
 struct Plan {
   int nparts;   // context-pass work-groups per (sequence, KV head); part p takes
@@ -24,6 +28,10 @@ struct Plan {
   size_t head;    // float [B][Hq][2]           merged (max, score normaliser)
   size_t kstats;  // float [B][Hq][nsplit][2]   kept-row (max, sum)
   size_t kacc;    // float [B][Hq][nsplit][d]   kept-row value partials
+  size_t sync;    // uint32 [B]                 select-kernel arrival counters
+  size_t segtab;  // SegTable [B]               clipped segment tables (positions, ranks)
+  int sel_chunk;  // visual ranks scored per select work-group
+  int sel_chunks; // select work-groups per sequence
   size_t total;
 };
 
@@ -66,6 +74,8 @@ struct AttendArgs {
   int k_cap, split, nsplit;
   float* kstats;
   float* kacc;
+  uint32_t* sync;       // [B] arrival counters of the select kernel (may be null)
+  void* segtab;         // [B] segment tables (SegTable) for the select kernel (may be null)
 };
 
 // context-pass parts that hold at least one tile of a sequence of length L
@@ -93,18 +103,25 @@ struct MassArgs {
 hipError_t launch_mass_finalize(const MassArgs& a, hipStream_t st);
 hipError_t launch_scores(const MassArgs& a, hipStream_t st);
 
-// per-sequence tail of a decode step (mass reduction, budget, scores, top-k)
-constexpr int kTailMaxHeads = 256;
-struct TailArgs {
+// Everything between the context pass and the kept-row pass of a decode step
+// (mass reduction, scores, budget, top-k) in one launch: grid (nchunks, B).
+constexpr int kMaxSelectHeads = 1024;
+struct SelectArgs {
   MassArgs m;
   int r_lo_bp, r_hi_bp, clamp;
   int k_cap;
   int32_t* k;
   int32_t* vis_idx;
+  int chunk;       // visual ranks scored per work-group
+  int nchunks;     // work-groups per sequence
+  uint32_t* sync;  // [B] arrival counters (nchunks > 1), zeroed by the context pass
+  const void* segtab;  // [B] segment tables written by the context pass
 };
 
-bool tail_fits(int n_q_heads, int max_vis);
-hipError_t launch_tail(const TailArgs& t, hipStream_t st);
+// visual ranks one select work-group scores per round (1024 lanes over the
+// lanes per token of the score order)
+int select_tokens_per_round(int n_q_heads);
+hipError_t launch_select(const SelectArgs& t, hipStream_t st);
 
 struct BudgetArgs {
   const int32_t* seq_len;

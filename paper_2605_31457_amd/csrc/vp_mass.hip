@@ -7,10 +7,11 @@ namespace vp {
 namespace {
 
 // One work-group per sequence: the per-part statistics merged per head, then
-// the head mean and head max (reduce_mass).
-__global__ __launch_bounds__(kMassThreads) void mass_finalize_kernel(const MassArgs a) {
-  __shared__ double s_mass[kMassThreads];
-  reduce_mass(a, blockIdx.x, threadIdx.x, s_mass, nullptr, nullptr);
+// the head mean and head max (reduce_heads, as in the select kernel).
+__global__ __launch_bounds__(kSelThreads) void mass_finalize_kernel(const MassArgs a) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char dyn[];
+  const int b = blockIdx.x;
+  reduce_heads(a, b, clamp_len(a.seq_len[b], a.max_seq_len), threadIdx.x, head_lds(dyn, a.Hq), true, [] {});
 }
 
 // S_i of Eq. (2) for every visual rank i. grid = (ceil(max_vis / 256), B);
@@ -54,7 +55,7 @@ __global__ __launch_bounds__(64) void budget_kernel(const BudgetArgs a) {
 }  // namespace
 
 hipError_t launch_mass_finalize(const MassArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL(mass_finalize_kernel, dim3(a.B), dim3(kMassThreads), 0, st, a);
+  hipLaunchKernelGGL(mass_finalize_kernel, dim3(a.B), dim3(kSelThreads), head_lds_bytes(a.Hq), st, a);
   return hipGetLastError();
 }
 

@@ -1,0 +1,195 @@
+// Everything of one decode step between the context pass and the kept-row
+// pass, in one launch: the Eq. (5)/(6) mass reduction with the head mean and
+// head max (Sec. 4.3), the Eq. (2) score of every visual token (Sec. 4.2), the
+// Eq. (7) budget with the Sec. 5.2 clamp and the Eq. (3) top-k.
+//
+// grid = (chunks, B), 1024 threads per work-group. Work-group c of sequence b
+// reduces the sequence's per-part statistics (every work-group of the sequence
+// does, so none waits for another), scores the visual ranks
+// [c * chunk, (c + 1) * chunk) from the spilled logits and writes them. With
+// one chunk per sequence the keys stay in LDS and the same work-group selects;
+// with several, each work-group publishes its scores (device-scope release)
+// and counts itself in on the sequence's arrival counter (zeroed by the
+// context pass of the same step); the last to arrive reads every score of the
+// sequence back and selects. No work-group ever waits for another.
+//
+// Latency: the statistics and the segment table (built by the context pass)
+// are requested at once at entry; the spilled logits of a thread's tokens (all heads) are one
+// batch of loads; the selection is the LDS radix select of vp_blocks.h.
+// Results equal those of the separate kernels (mass_finalize_kernel,
+// scores_kernel, budget rule, topk_kernel): the same device functions in the
+// same order.
+#include "vp_blocks.h"
+
+namespace vp {
+namespace {
+
+// HB: heads per score group, rounded up (8 or 16)
+template <int HB>
+__global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t, int lds_keys) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char dyn[];
+  __shared__ SelectShared sh;
+  __shared__ SegTable tab;
+  __shared__ int s_last;
+
+  const MassArgs& a = t.m;
+  const int c = blockIdx.x;
+  const int b = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wid = tid >> 6;
+  const HeadLds hs = head_lds(dyn, a.Hq);
+  uint32_t* s_keys = reinterpret_cast<uint32_t*>(dyn + head_lds_bytes(a.Hq));
+
+  const int L = clamp_len(a.seq_len[b], a.max_seq_len);
+  for (int i = tid; i < kHistWords; i += kSelThreads) sh.hist[i] = 0;
+
+  // ---- per-head statistics; wave 0 builds the segment table while the
+  // statistics are in flight (the reduction's barriers publish it) ----
+  reduce_heads(a, b, L, tid, hs, c == 0, [&] {
+    if (wid == 0) {
+      // the context pass left the clipped table in the workspace: one round of loads
+      const uint4* src = reinterpret_cast<const uint4*>(static_cast<const SegTable*>(t.segtab) + b);
+      uint4* dst = reinterpret_cast<uint4*>(&tab);
+      constexpr int kWords = static_cast<int>(sizeof(SegTable) / 16);
+      uint4 w[(kWords + 63) / 64];
+#pragma unroll
+      for (int j = 0; j < (kWords + 63) / 64; ++j) w[j] = src[min(j * 64 + lane, kWords - 1)];
+#pragma unroll
+      for (int j = 0; j < (kWords + 63) / 64; ++j)
+        if (j * 64 + lane < kWords) dst[j * 64 + lane] = w[j];
+    }
+  });
+  const int nvis = tab.rk[tab.n];
+  const int n = min(nvis, a.max_vis);
+  const bool single = t.nchunks == 1;
+  const bool in_lds = n <= lds_keys;
+  float* sc = a.scores + static_cast<size_t>(b) * a.max_vis;
+
+  // ---- Eq. (2) scores of this chunk's visual ranks: ng lanes per token, lane
+  // g sums the heads of group g, the group sums are added in group order ----
+  const ScoreGroups sg = score_groups(a.Hq);
+  const int g = tid & (sg.ng - 1);
+  const int tpw = kSelThreads / sg.ng;  // tokens per round
+  const int h0 = g * sg.hpg;
+  const int h1 = min(a.Hq, h0 + sg.hpg);
+  const int r0 = min(n, c * t.chunk);
+  const int r1 = min(n, r0 + t.chunk);
+  const float* zb = a.zs + static_cast<size_t>(b) * a.Hq * a.zs_stride;
+  uint32_t kmin = 0xffffffffu, kmax = 0u;
+  for (int base = r0; base < r1; base += tpw) {
+    const int i = base + tid / sg.ng;
+    const bool ok = i < r1;
+    const int pos = ok ? rank_to_pos(tab, i) : 0;
+    float zz[HB];
+#pragma unroll
+    for (int j = 0; j < HB; ++j)
+      if (h0 + j < h1) zz[j] = zb[static_cast<size_t>(h0 + j) * a.zs_stride + pos];
+    float p = 0.f;
+#pragma unroll
+    for (int j = 0; j < HB; ++j)
+      if (h0 + j < h1) p = score_term(p, zz[j], hs.hm[h0 + j], hs.hinv[h0 + j], a.inv_tau_s);
+    float total = p;
+    for (int j = 1; j < sg.ng; ++j) total = total + __shfl(p, (lane & ~(sg.ng - 1)) + j);
+    if (ok && g == 0) {
+      const float S = total / static_cast<float>(a.Hq);
+      sc[i] = S;
+      const uint32_t u = order_key(S);
+      if (single && in_lds) s_keys[i] = u;
+      kmin = min(kmin, u);
+      kmax = max(kmax, u);
+    }
+  }
+
+  if (!single) {
+    // publish this chunk's scores and count in; the last work-group of the
+    // sequence selects. The barrier orders the block's stores before thread 0's
+    // device-scope release; the last arrival alone takes the acquire, which makes
+    // the other work-groups' scores visible to the block after the second barrier.
+    __syncthreads();
+    if (tid == 0) {
+      const bool last = __hip_atomic_fetch_add(t.sync + b, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT) ==
+                        static_cast<unsigned>(t.nchunks - 1);
+      if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+      s_last = last;
+    }
+    __syncthreads();
+    if (!s_last) return;
+    kmin = 0xffffffffu;
+    kmax = 0u;
+    constexpr int kBatch = 8;  // loads in flight per thread
+    for (int base = 0; base < n; base += kBatch * kSelThreads) {
+      float v[kBatch];
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) v[j] = sc[min(base + j * kSelThreads + tid, n - 1)];
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        const int i = base + j * kSelThreads + tid;
+        if (i < n) {
+          const uint32_t u = order_key(v[j]);
+          if (in_lds) s_keys[i] = u;
+          kmin = min(kmin, u);
+          kmax = max(kmax, u);
+        }
+      }
+    }
+  }
+
+  // ---- Eq. (7) budget, then Eq. (3) selection ----
+  const int kb = budget_rule(static_cast<double>(hs.mseq[1]), nvis, t.r_lo_bp, t.r_hi_bp, t.clamp);
+  if (tid == 0) t.k[b] = kb;
+  int k = kb > n ? n : kb;
+  k = k > t.k_cap ? t.k_cap : k;
+  int32_t* out = t.vis_idx + static_cast<size_t>(b) * t.k_cap;
+  for (int i = k + tid; i < t.k_cap; i += kSelThreads) out[i] = -1;
+  if (k == 0) return;
+  auto key_at = [&](int i) -> uint32_t { return in_lds ? s_keys[i] : order_key(sc[i]); };
+  const bool take_all = k >= n;
+  uint32_t T = 0u;
+  int need = k;
+  block_key_range(sh, kmin, kmax, lane, wid);
+  if (!take_all) T = radix_select(sh, key_at, n, need, kmin, kmax, tid, lane, wid);
+  ordered_compaction(sh, tab, key_at, n, k, need, T, take_all, out, lane, wid);
+}
+
+// LDS per work-group beyond the kernel's static arrays, and the keys it leaves
+// room for (one GPU model per process is assumed: computed once)
+template <int HB>
+int key_room(int Hq) {
+  static const int stat = [] {
+    hipFuncAttributes attr;
+    return hipFuncGetAttributes(&attr, reinterpret_cast<const void*>(select_kernel<HB>)) == hipSuccess
+               ? static_cast<int>(attr.sharedSizeBytes)
+               : 48 * 1024;
+  }();
+  static const int max_lds = [] {
+    int dev = 0, v = 65536;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess)
+      v = 65536;
+    return v;
+  }();
+  return max(0, max_lds - stat - head_lds_bytes(Hq) - 64) / 4;
+}
+
+template <int HB>
+hipError_t launch_hb(const SelectArgs& t, hipStream_t st) {
+  const int room = key_room<HB>(t.m.Hq);
+  const int keys = min(room, t.m.max_vis);
+  // one chunk keeps its keys in LDS: the launch plan guarantees they fit
+  if (t.nchunks == 1 && keys < t.m.max_vis) return hipErrorInvalidValue;
+  const size_t dyn = static_cast<size_t>(head_lds_bytes(t.m.Hq)) + static_cast<size_t>(keys) * 4;
+  hipLaunchKernelGGL((select_kernel<HB>), dim3(t.nchunks, t.m.B), dim3(kSelThreads), dyn, st, t, keys);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+int select_tokens_per_round(int n_q_heads) { return kSelThreads / score_groups(n_q_heads).ng; }
+
+hipError_t launch_select(const SelectArgs& t, hipStream_t st) {
+  if (t.m.Hq > kMaxSelectHeads || t.nchunks < 1 || t.chunk < 1) return hipErrorInvalidValue;
+  return score_groups(t.m.Hq).hpg <= 8 ? launch_hb<8>(t, st) : launch_hb<16>(t, st);
+}
+
+}  // namespace vp
