@@ -37,63 +37,6 @@ __device__ __forceinline__ HeadLds head_lds(unsigned char* base, int Hq) {
   return h;
 }
 
-// Cross-lane all-reduce inside aligned groups of `width` lanes (a power of two
-// <= 64, uniform): butterflies on the DPP network (quad permutes, half-row and
-// row mirrors), then a swizzle across 16 lanes and a permute across 32.
-template <typename Op>
-__device__ __forceinline__ uint32_t group_allreduce_u32(uint32_t v, int width, Op op) {
-  auto dpp = [](uint32_t x, int ctrl) -> uint32_t {
-    switch (ctrl) {
-      case 0xB1: return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0xB1, 0xf, 0xf, false));
-      case 0x4E: return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x4E, 0xf, 0xf, false));
-      case 0x141: return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x141, 0xf, 0xf, false));
-      default: return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x140, 0xf, 0xf, false));
-    }
-  };
-  if (width > 1) v = op(v, dpp(v, 0xB1));   // quad_perm [1,0,3,2]: lane ^ 1
-  if (width > 2) v = op(v, dpp(v, 0x4E));   // quad_perm [2,3,0,1]: lane ^ 2
-  if (width > 4) v = op(v, dpp(v, 0x141));  // row_half_mirror: the other quad of 8
-  if (width > 8) v = op(v, dpp(v, 0x140));  // row_mirror: the other half of 16
-  if (width > 16) v = op(v, static_cast<uint32_t>(__builtin_amdgcn_ds_swizzle(static_cast<int>(v), 0x401F)));  // lane ^ 16
-  if (width > 32) v = op(v, static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), 32)));
-  return v;
-}
-__device__ __forceinline__ float group_max_f32(float v, int width) {
-  return __uint_as_float(group_allreduce_u32(__float_as_uint(v), width, [](uint32_t a, uint32_t b) {
-    return __float_as_uint(fmaxf(__uint_as_float(a), __uint_as_float(b)));
-  }));
-}
-// double sums: the two halves travel separately, the add happens in double
-__device__ __forceinline__ double group_sum_f64(double v, int width) {
-  auto step = [&](auto mov) {
-    const uint64_t u = __builtin_bit_cast(uint64_t, v);
-    const uint32_t lo = mov(static_cast<uint32_t>(u)), hi = mov(static_cast<uint32_t>(u >> 32));
-    v += __builtin_bit_cast(double, (static_cast<uint64_t>(hi) << 32) | lo);
-  };
-  if (width > 1) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0xB1, 0xf, 0xf, false)); });
-  if (width > 2) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x4E, 0xf, 0xf, false)); });
-  if (width > 4) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x141, 0xf, 0xf, false)); });
-  if (width > 8) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x140, 0xf, 0xf, false)); });
-  if (width > 16) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_ds_swizzle(static_cast<int>(x), 0x401F)); });
-  if (width > 32) step([](uint32_t x) { return static_cast<uint32_t>(__shfl_xor(static_cast<int>(x), 32)); });
-  return v;
-}
-__device__ __forceinline__ double group_max_f64(double v, int width) {
-  auto step = [&](auto mov) {
-    const uint64_t u = __builtin_bit_cast(uint64_t, v);
-    const uint32_t lo = mov(static_cast<uint32_t>(u)), hi = mov(static_cast<uint32_t>(u >> 32));
-    const double o = __builtin_bit_cast(double, (static_cast<uint64_t>(hi) << 32) | lo);
-    v = o > v ? o : v;
-  };
-  if (width > 1) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0xB1, 0xf, 0xf, false)); });
-  if (width > 2) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x4E, 0xf, 0xf, false)); });
-  if (width > 4) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x141, 0xf, 0xf, false)); });
-  if (width > 8) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x140, 0xf, 0xf, false)); });
-  if (width > 16) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_ds_swizzle(static_cast<int>(x), 0x401F)); });
-  if (width > 32) step([](uint32_t x) { return static_cast<uint32_t>(__shfl_xor(static_cast<int>(x), 32)); });
-  return v;
-}
-
 // Lanes that share one head in reduce_heads: the fewest (a power of two) whose
 // four parts each cover the part capacity, at most 64 and at most
 // kSelThreads / Hq.
@@ -325,15 +268,36 @@ __device__ __forceinline__ int lanes_below(uint64_t mask) {
 
 struct SelectShared {
   uint32_t hist[kHistWords];
-  int wcnt[kSelWaves];
-  int gt[kSelWaves];
-  int eq[kSelWaves];
-  uint32_t wmin[kSelWaves];
-  uint32_t wmax[kSelWaves];
+  alignas(16) int wcnt[kSelWaves];
+  alignas(16) int gt[kSelWaves];
+  alignas(16) int eq[kSelWaves];
+  alignas(16) uint32_t wmin[kSelWaves];
+  alignas(16) uint32_t wmax[kSelWaves];
   uint32_t digit;
   int above;
   int dcount;
 };
+
+// The kSelWaves per-wave values of an LDS array in registers (four 16-byte reads)
+__device__ __forceinline__ void wave_values(const int* arr, int (&v)[kSelWaves]) {
+#pragma unroll
+  for (int j = 0; j < kSelWaves / 4; ++j) {
+    const int4 x = reinterpret_cast<const int4*>(arr)[j];
+    v[4 * j] = x.x;
+    v[4 * j + 1] = x.y;
+    v[4 * j + 2] = x.z;
+    v[4 * j + 3] = x.w;
+  }
+}
+// sum of the per-wave values of waves below `wid`
+__device__ __forceinline__ int waves_below(const int* arr, int wid) {
+  int v[kSelWaves];
+  wave_values(arr, v);
+  int s = 0;
+#pragma unroll
+  for (int j = 0; j < kSelWaves; ++j) s += j < wid ? v[j] : 0;
+  return s;
+}
 
 // Block min/max of per-thread (kmin, kmax); contains one barrier.
 __device__ __forceinline__ void block_key_range(SelectShared& sh, uint32_t& kmin, uint32_t& kmax, int lane,
@@ -345,11 +309,13 @@ __device__ __forceinline__ void block_key_range(SelectShared& sh, uint32_t& kmin
     sh.wmax[wid] = kmax;
   }
   __syncthreads();
-  kmin = sh.wmin[0];
-  kmax = sh.wmax[0];
-  for (int v = 1; v < kSelWaves; ++v) {
-    kmin = min(kmin, sh.wmin[v]);
-    kmax = max(kmax, sh.wmax[v]);
+  int lo[kSelWaves], hi[kSelWaves];
+  wave_values(reinterpret_cast<const int*>(sh.wmin), lo);
+  wave_values(reinterpret_cast<const int*>(sh.wmax), hi);
+#pragma unroll
+  for (int v = 0; v < kSelWaves; ++v) {
+    kmin = min(kmin, static_cast<uint32_t>(lo[v]));
+    kmax = max(kmax, static_cast<uint32_t>(hi[v]));
   }
 }
 
@@ -390,7 +356,7 @@ __device__ __forceinline__ uint32_t radix_select(SelectShared& sh, KeyAt key_at,
     int incl = wave_incl_sum(local);
     if (lane == 63) sh.wcnt[wid] = incl;
     __syncthreads();
-    for (int v = 0; v < wid; ++v) incl += sh.wcnt[v];
+    incl += waves_below(sh.wcnt, wid);
     const int excl = incl - local;
     if (excl < need && need <= incl) {
       int acc = excl;
@@ -454,10 +420,8 @@ __device__ __forceinline__ void ordered_compaction(SelectShared& sh, const SegTa
   }
   __syncthreads();
   int gt_run = 0, eq_run = 0;  // keys > T / == T at ranks below the current chunk
-  for (int v = 0; v < wid; ++v) {
-    gt_run += sh.gt[v];
-    eq_run += sh.eq[v];
-  }
+  gt_run = waves_below(sh.gt, wid);
+  eq_run = waves_below(sh.eq, wid);
   const bool staged = k <= kHistWords;
   uint32_t* stage = sh.hist;
   constexpr int Q = 4;  // chunks of 64 ranks per step
@@ -494,5 +458,6 @@ __device__ __forceinline__ void ordered_compaction(SelectShared& sh, const SegTa
     for (int o = wid * 64 + lane; o < k; o += kSelThreads) out[o] = rank_to_pos(tab, static_cast<int>(stage[o]));
   }
 }
+
 
 }  // namespace vp

@@ -41,6 +41,63 @@ __device__ __forceinline__ float sum_over_quads(float v) {
   return v;
 }
 
+// Cross-lane all-reduce inside aligned groups of `width` lanes (a power of two
+// <= 64, uniform): butterflies on the DPP network (quad permutes, half-row and
+// row mirrors), then a swizzle across 16 lanes and a permute across 32.
+template <typename Op>
+__device__ __forceinline__ uint32_t group_allreduce_u32(uint32_t v, int width, Op op) {
+  auto dpp = [](uint32_t x, int ctrl) -> uint32_t {
+    switch (ctrl) {
+      case 0xB1: return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0xB1, 0xf, 0xf, false));
+      case 0x4E: return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x4E, 0xf, 0xf, false));
+      case 0x141: return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x141, 0xf, 0xf, false));
+      default: return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x140, 0xf, 0xf, false));
+    }
+  };
+  if (width > 1) v = op(v, dpp(v, 0xB1));   // quad_perm [1,0,3,2]: lane ^ 1
+  if (width > 2) v = op(v, dpp(v, 0x4E));   // quad_perm [2,3,0,1]: lane ^ 2
+  if (width > 4) v = op(v, dpp(v, 0x141));  // row_half_mirror: the other quad of 8
+  if (width > 8) v = op(v, dpp(v, 0x140));  // row_mirror: the other half of 16
+  if (width > 16) v = op(v, static_cast<uint32_t>(__builtin_amdgcn_ds_swizzle(static_cast<int>(v), 0x401F)));  // lane ^ 16
+  if (width > 32) v = op(v, static_cast<uint32_t>(__shfl_xor(static_cast<int>(v), 32)));
+  return v;
+}
+__device__ __forceinline__ float group_max_f32(float v, int width) {
+  return __uint_as_float(group_allreduce_u32(__float_as_uint(v), width, [](uint32_t a, uint32_t b) {
+    return __float_as_uint(fmaxf(__uint_as_float(a), __uint_as_float(b)));
+  }));
+}
+// double sums: the two halves travel separately, the add happens in double
+__device__ __forceinline__ double group_sum_f64(double v, int width) {
+  auto step = [&](auto mov) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = mov(static_cast<uint32_t>(u)), hi = mov(static_cast<uint32_t>(u >> 32));
+    v += __builtin_bit_cast(double, (static_cast<uint64_t>(hi) << 32) | lo);
+  };
+  if (width > 1) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0xB1, 0xf, 0xf, false)); });
+  if (width > 2) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x4E, 0xf, 0xf, false)); });
+  if (width > 4) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x141, 0xf, 0xf, false)); });
+  if (width > 8) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x140, 0xf, 0xf, false)); });
+  if (width > 16) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_ds_swizzle(static_cast<int>(x), 0x401F)); });
+  if (width > 32) step([](uint32_t x) { return static_cast<uint32_t>(__shfl_xor(static_cast<int>(x), 32)); });
+  return v;
+}
+__device__ __forceinline__ double group_max_f64(double v, int width) {
+  auto step = [&](auto mov) {
+    const uint64_t u = __builtin_bit_cast(uint64_t, v);
+    const uint32_t lo = mov(static_cast<uint32_t>(u)), hi = mov(static_cast<uint32_t>(u >> 32));
+    const double o = __builtin_bit_cast(double, (static_cast<uint64_t>(hi) << 32) | lo);
+    v = o > v ? o : v;
+  };
+  if (width > 1) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0xB1, 0xf, 0xf, false)); });
+  if (width > 2) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x4E, 0xf, 0xf, false)); });
+  if (width > 4) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x141, 0xf, 0xf, false)); });
+  if (width > 8) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_mov_dpp(static_cast<int>(x), 0x140, 0xf, 0xf, false)); });
+  if (width > 16) step([](uint32_t x) { return static_cast<uint32_t>(__builtin_amdgcn_ds_swizzle(static_cast<int>(x), 0x401F)); });
+  if (width > 32) step([](uint32_t x) { return static_cast<uint32_t>(__shfl_xor(static_cast<int>(x), 32)); });
+  return v;
+}
+
 // Walks the visual segments of one sequence in position order, clipping each
 // segment to [previous end, L) so that ranks stay consistent and in range for
 // any device layout. `rank` is the visual rank of position `st`.
