@@ -128,7 +128,8 @@ AttendArgs attend_args(const vp_shape* s, const vp_layout* l, const vp_params* p
   a.thr_t = a.thr_s;
   a.tau_s_one = p->tau_score == 1.0f;
   a.nparts = plan.nparts;
-  a.zs_stride = plan.zs_stride;
+  a.zs_rows = plan.zs_rows;
+  a.zs_gp = plan.zs_gp;
   a.zs = reinterpret_cast<float*>(ws + plan.zs);
   a.stats = reinterpret_cast<float*>(ws + plan.stats);
   a.acc = reinterpret_cast<float*>(ws + plan.acc);
@@ -163,7 +164,10 @@ MassArgs mass_args(const vp_shape* s, const vp_layout* l, const Plan& plan, cons
   m.max_seq_len = s->max_seq_len;
   m.max_vis = s->max_vis;
   m.nparts = plan.nparts;
-  m.zs_stride = plan.zs_stride;
+  m.Hkv = s->n_kv_heads;
+  m.G = s->n_q_heads / s->n_kv_heads;
+  m.zs_rows = plan.zs_rows;
+  m.zs_gp = plan.zs_gp;
   m.inv_tau_m = a.inv_tau_m;
   m.inv_tau_s = a.inv_tau_s;
   m.stats = a.stats;
@@ -269,10 +273,11 @@ Plan make_plan(const vp_shape& s) {
 #endif
   p.nsplit = (s.k_cap + p.split - 1) / p.split;
   const size_t B = s.batch, Hq = s.n_q_heads, d = s.head_dim;
-  p.zs_stride = ((s.max_seq_len + 31) / 32) * 32;
+  p.zs_rows = ((s.max_seq_len + 31) / 32) * 32;
+  p.zs_gp = s.n_q_heads / s.n_kv_heads <= 8 ? 8 : 16;
   size_t off = 0;
   p.zs = off;
-  off = align256(off + B * Hq * static_cast<size_t>(p.zs_stride) * 4);
+  off = align256(off + B * static_cast<size_t>(s.n_kv_heads) * p.zs_rows * static_cast<size_t>(p.zs_gp) * 4);
   p.stats = off;
   off = align256(off + B * Hq * p.nparts * 8 * 4);
   p.acc = off;
@@ -291,7 +296,7 @@ Plan make_plan(const vp_shape& s) {
   // Select kernel: chunks of whole rounds (a round scores 1024 / lanes-per-token
   // visual ranks), enough rounds per chunk that the launch has about
   // VP_SELECT_WGS work-groups, so the spilled logits stream through many CUs.
-  const int64_t tpr = select_tokens_per_round(s.n_q_heads);
+  const int64_t tpr = select_tokens_per_round(s.n_q_heads, s.n_kv_heads);
   const int64_t want = static_cast<int64_t>(s.batch) * s.max_vis;
   int64_t rounds = (want + tpr * VP_SELECT_WGS - 1) / (tpr * VP_SELECT_WGS);
   if (rounds < 1) rounds = 1;

@@ -41,11 +41,13 @@
 // A maximum is raised only when a logit exceeds it by more than a margin that
 // keeps every weight below 2^64, so rescaling is rare.
 // Visual logits are spilled to the workspace for the scores, which need the
-// global (m, Ls) of every head. The spill is indexed by cache position with
-// 128-byte aligned rows, and a full visual sub-tile is transposed through a
-// small LDS stage so that one store instruction writes one whole 128-byte line
-// per head: partial-line writes would compete with the streaming reads for the
-// L1's outstanding-request slots.
+// global (m, Ls) of every head. The spill holds one plane per (sequence, KV
+// group) with a row of zs_gp floats (the group's heads, padded to 8 or 16) per
+// cache position; a full visual sub-tile is transposed through a small LDS
+// stage so that its 32 rows leave as one contiguous 1-2 KB store (whole lines:
+// partial-line writes would compete with the streaming reads for the L1's
+// outstanding-request slots), and the scores read each (token, group) row with
+// 16-byte loads.
 //
 // Attention partial (text rows of the context pass, or the gathered kept rows):
 //   (m_t, l_t, acc[d]) with p_j = 2^(z_j - m_t), acc = sum_j p_j V_j.
@@ -288,8 +290,7 @@ struct Pass {
   const char* Kb;
   const char* Vb;
   size_t rstride;
-  float* zrow;   // spill row of this lane's head
-  float* zbase;  // spill row of the first head of this KV group
+  float* zbase;  // spill plane of this KV group: row p holds the logits of its heads at position p
   QFrag<DT, D> qf;
   // visual pass: lane-local reference and sums (merged over a head's 4 lanes at the end)
   float m_v, Ls_v, Lm_v;
@@ -420,25 +421,24 @@ struct Pass {
       }
       Ls_v += ts;
       Lm_v += tm;
-      // visual logits, position order
+      // visual logits: spill rows of zs_gp floats (this KV group's heads) by position
       if (cls == TILE_VIS && t_end - t0 == 32) {
-        // transpose through the stage: lane (a4, n16) holds head n16, rows
-        // 16*hf + 4*a4 .. +3; lane l then stores 16 bytes of head l/8's line
-        *reinterpret_cast<float4*>(stage + n16 * 32 + 4 * a4) = make_float4(z[0], z[1], z[2], z[3]);
-        *reinterpret_cast<float4*>(stage + n16 * 32 + 16 + 4 * a4) = make_float4(z[4], z[5], z[6], z[7]);
+        // transpose through the stage (row = token, zs_gp heads): lane (a4, n16)
+        // holds head n16 for tokens 16*(i/4) + 4*a4 + i%4; then the 32 rows go
+        // out as one contiguous block of 32 * zs_gp floats, 16 bytes per lane
+        const int gp = a.zs_gp;
+        if (n16 < gp) {
 #pragma unroll
-        for (int round = 0; round < 2; ++round) {
-          const int hh = 8 * round + (lane >> 3);
-          if (round == 0 || a.G > 8) {
-            const float4 v = *reinterpret_cast<const float4*>(stage + hh * 32 + 4 * (lane & 7));
-            if (hh < a.G)
-              *reinterpret_cast<float4*>(zbase + static_cast<size_t>(hh) * a.zs_stride + t0 + 4 * (lane & 7)) = v;
-          }
+          for (int i = 0; i < 8; ++i) stage[(16 * (i >> 2) + 4 * a4 + (i & 3)) * gp + n16] = z[i];
         }
+        float4* dst = reinterpret_cast<float4*>(zbase + static_cast<size_t>(t0) * gp);
+        const float4* src = reinterpret_cast<const float4*>(stage);
+        dst[lane] = src[lane];
+        if (gp > 8) dst[64 + lane] = src[64 + lane];
       } else if (hv && vis) {
 #pragma unroll
         for (int i = 0; i < 8; ++i)
-          if (vis & (1u << i)) zrow[t0 + 16 * (i >> 2) + 4 * a4 + (i & 3)] = z[i];
+          if (vis & (1u << i)) zbase[static_cast<size_t>(t0 + 16 * (i >> 2) + 4 * a4 + (i & 3)) * a.zs_gp + n16] = z[i];
       }
     } else {
       // ---- text rows (or kept rows): attention weights, statistics, value product ----
@@ -551,8 +551,7 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
   s.l_t = s.Lm_t = s.Ls_t = 0.f;
 #pragma unroll
   for (int i = 0; i < C::ACC_N; ++i) s.acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  s.zbase = P::VIS ? a.zs + (static_cast<size_t>(b) * a.Hq + static_cast<size_t>(g) * a.G) * a.zs_stride : nullptr;
-  s.zrow = P::VIS ? s.zbase + static_cast<size_t>(s.hv ? s.n16 : 0) * a.zs_stride : nullptr;
+  s.zbase = P::VIS ? a.zs + (static_cast<size_t>(b) * a.Hkv + g) * a.zs_rows * static_cast<size_t>(a.zs_gp) : nullptr;
 
   Sub cur;
   cur.t0 = s.r0;

@@ -189,45 +189,57 @@ __device__ __forceinline__ float score_term(float s, float z, float hm, float hi
 }
 
 // Summation order of the Eq. (2) head sum, shared by every kernel that scores:
-// the Hq heads are cut into `ng` consecutive groups of `hpg` heads (ng a power
-// of two <= 64, so the lanes of one token sit in one wave); each group is
-// summed in head order from zero, then the group sums are added in group order
-// and the total is divided by Hq.
-struct ScoreGroups {
-  int ng;   // groups (lanes per token)
-  int hpg;  // heads per group
-};
-__host__ __device__ inline ScoreGroups score_groups(int Hq) {
+// lane slot l of ng = min(64, Hkv rounded up to a power of two) sums, in order,
+// the KV groups g = l, l + ng, ..., each group's G heads in head order, from
+// zero; the lane sums are then added in lane order and the total divided by Hq.
+__host__ __device__ inline int score_lanes(int Hkv) {
   int ng = 1;
-  while (ng < 64 && ng * 8 < Hq) ng <<= 1;
-  return ScoreGroups{ng, (Hq + ng - 1) / ng};
+  while (ng < 64 && ng < Hkv) ng <<= 1;
+  return ng;
 }
-constexpr int kMaxHeadsPerGroup = kMaxHq_ / 64;
+
+// p plus the score terms of one KV group's G heads for one token, from its
+// spill row (GP floats, 16-byte aligned); hm/hinv point at the group's first head
+template <int GP>
+__device__ __forceinline__ float group_terms(float p, const float* row, int G, const float* hm, const float* hinv,
+                                             float inv_tau) {
+  float z[GP];
+#pragma unroll
+  for (int q = 0; q < GP / 4; ++q) {
+    const float4 v = reinterpret_cast<const float4*>(row)[q];
+    z[4 * q] = v.x;
+    z[4 * q + 1] = v.y;
+    z[4 * q + 2] = v.z;
+    z[4 * q + 3] = v.w;
+  }
+#pragma unroll
+  for (int j = 0; j < GP; ++j)
+    if (j < G) p = score_term(p, z[j], hm[j], hinv[j], inv_tau);
+  return p;
+}
 
 // ---------------------------------------------------------------------------
 // Eq. (2) score of the visual token at cache position pos of sequence b by one
-// thread (the same groups and order as the select kernel's lanes):
+// thread (the same order as the select kernel's lanes):
 // S = (1/Hq) sum_h 2^((z_h - m_h) / tau_score) / Ls_h from the spilled logits.
 // hm/hinv: per-head max and 1/Ls.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ float token_score(const MassArgs& a, int b, int pos, const float* hm, const float* hinv) {
-  const float* z = a.zs + static_cast<size_t>(b) * a.Hq * a.zs_stride + pos;
-  const ScoreGroups sg = score_groups(a.Hq);
+template <int GP>
+__device__ __forceinline__ float token_score_gp(const MassArgs& a, int b, int pos, const float* hm, const float* hinv) {
+  const float* zb = a.zs + static_cast<size_t>(b) * a.Hkv * a.zs_rows * GP + static_cast<size_t>(pos) * GP;
+  const int ng = score_lanes(a.Hkv);
   float total = 0.f;
-  for (int g = 0; g < sg.ng; ++g) {
-    const int h0 = g * sg.hpg;
-    const int h1 = min(a.Hq, h0 + sg.hpg);
-    float zz[kMaxHeadsPerGroup];
-#pragma unroll
-    for (int j = 0; j < kMaxHeadsPerGroup; ++j)
-      if (h0 + j < h1) zz[j] = z[static_cast<size_t>(h0 + j) * a.zs_stride];
+  for (int l = 0; l < ng; ++l) {
     float p = 0.f;
-#pragma unroll
-    for (int j = 0; j < kMaxHeadsPerGroup; ++j)
-      if (h0 + j < h1) p = score_term(p, zz[j], hm[h0 + j], hinv[h0 + j], a.inv_tau_s);
-    total = g == 0 ? p : total + p;
+    for (int g = l; g < a.Hkv; g += ng)
+      p = group_terms<GP>(p, zb + static_cast<size_t>(g) * a.zs_rows * GP, a.G, hm + g * a.G, hinv + g * a.G,
+                          a.inv_tau_s);
+    total = l == 0 ? p : total + p;
   }
   return total / static_cast<float>(a.Hq);
+}
+__device__ __forceinline__ float token_score(const MassArgs& a, int b, int pos, const float* hm, const float* hinv) {
+  return a.zs_gp == 8 ? token_score_gp<8>(a, b, pos, hm, hinv) : token_score_gp<16>(a, b, pos, hm, hinv);
 }
 
 // ---------------------------------------------------------------------------

@@ -20,8 +20,9 @@ struct Plan {
                 // the 32-row tiles p, p + nparts, p + 2 nparts, ...
   int split;    // kept rows per kept-pass work-group (multiple of 32)
   int nsplit;   // ceil(k_cap / split)
-  int zs_stride;  // floats per spill row: max_seq_len rounded up to 32 (128-byte rows)
-  size_t zs;      // float [B][Hq][zs_stride]   visual logits (log2 domain), by cache position
+  int zs_rows;    // rows per spill plane: max_seq_len rounded up to 32
+  int zs_gp;      // floats per spill row: the query group padded to 8 or 16
+  size_t zs;      // float [B][Hkv][zs_rows][zs_gp]  visual logits (log2 domain) by cache position
   size_t stats;   // float [B][Hq][nparts][8]   per-part statistics: visual rows
                   //   {m_v, Ls_v, Lm_v, -}, text rows {m_t, l_t, Lm_t, Ls_t}
   size_t acc;     // float [B][Hq][nparts][d]   per-part text value partials
@@ -65,7 +66,7 @@ struct AttendArgs {
   float thr_t;          // same for the attention partial
   int tau_s_one;        // tau_score == 1: the attention weight doubles as the score weight
   int nparts;
-  int zs_stride;
+  int zs_rows, zs_gp;
   float* zs;
   float* stats;
   float* acc;
@@ -90,7 +91,7 @@ struct MassArgs {
   const int32_t* seq_len;
   const int32_t* seg_off;
   const int32_t* seg;
-  int B, Hq, max_seq_len, max_vis, nparts, zs_stride;
+  int B, Hq, Hkv, G, max_seq_len, max_vis, nparts, zs_rows, zs_gp;
   float inv_tau_m, inv_tau_s;
   const float* stats;
   const float* zs;
@@ -120,7 +121,7 @@ struct SelectArgs {
 
 // visual ranks one select work-group scores per round (1024 lanes over the
 // lanes per token of the score order)
-int select_tokens_per_round(int n_q_heads);
+int select_tokens_per_round(int n_q_heads, int n_kv_heads);
 hipError_t launch_select(const SelectArgs& t, hipStream_t st);
 
 struct BudgetArgs {

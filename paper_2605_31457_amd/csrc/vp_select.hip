@@ -24,8 +24,8 @@
 namespace vp {
 namespace {
 
-// HB: heads per score group, rounded up (8 or 16)
-template <int HB>
+// GP: floats per spill row (the query group padded to 8 or 16)
+template <int GP>
 __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t, int lds_keys) {
   extern __shared__ __attribute__((aligned(16))) unsigned char dyn[];
   __shared__ SelectShared sh;
@@ -67,31 +67,26 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
   float* sc = a.scores + static_cast<size_t>(b) * a.max_vis;
 
   // ---- Eq. (2) scores of this chunk's visual ranks: ng lanes per token, lane
-  // g sums the heads of group g, the group sums are added in group order ----
-  const ScoreGroups sg = score_groups(a.Hq);
-  const int g = tid & (sg.ng - 1);
-  const int tpw = kSelThreads / sg.ng;  // tokens per round
-  const int h0 = g * sg.hpg;
-  const int h1 = min(a.Hq, h0 + sg.hpg);
+  // l takes the KV groups l, l + ng, ... (a 16-byte-aligned spill row each),
+  // the lane sums are added in lane order ----
+  const int ng = score_lanes(a.Hkv);
+  const int l = tid & (ng - 1);
+  const int tpw = kSelThreads / ng;  // tokens per round
   const int r0 = min(n, c * t.chunk);
   const int r1 = min(n, r0 + t.chunk);
-  const float* zb = a.zs + static_cast<size_t>(b) * a.Hq * a.zs_stride;
+  const float* zb = a.zs + static_cast<size_t>(b) * a.Hkv * a.zs_rows * GP;
   uint32_t kmin = 0xffffffffu, kmax = 0u;
   for (int base = r0; base < r1; base += tpw) {
-    const int i = base + tid / sg.ng;
+    const int i = base + tid / ng;
     const bool ok = i < r1;
     const int pos = ok ? rank_to_pos(tab, i) : 0;
-    float zz[HB];
-#pragma unroll
-    for (int j = 0; j < HB; ++j)
-      if (h0 + j < h1) zz[j] = zb[static_cast<size_t>(h0 + j) * a.zs_stride + pos];
     float p = 0.f;
-#pragma unroll
-    for (int j = 0; j < HB; ++j)
-      if (h0 + j < h1) p = score_term(p, zz[j], hs.hm[h0 + j], hs.hinv[h0 + j], a.inv_tau_s);
+    for (int g = l; g < a.Hkv; g += ng)
+      p = group_terms<GP>(p, zb + (static_cast<size_t>(g) * a.zs_rows + pos) * GP, a.G, hs.hm + g * a.G,
+                          hs.hinv + g * a.G, a.inv_tau_s);
     float total = p;
-    for (int j = 1; j < sg.ng; ++j) total = total + __shfl(p, (lane & ~(sg.ng - 1)) + j);
-    if (ok && g == 0) {
+    for (int j = 1; j < ng; ++j) total = total + __shfl(p, (lane & ~(ng - 1)) + j);
+    if (ok && l == 0) {
       const float S = total / static_cast<float>(a.Hq);
       sc[i] = S;
       const uint32_t u = order_key(S);
@@ -154,11 +149,11 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
 
 // LDS per work-group beyond the kernel's static arrays, and the keys it leaves
 // room for (one GPU model per process is assumed: computed once)
-template <int HB>
+template <int GP>
 int key_room(int Hq) {
   static const int stat = [] {
     hipFuncAttributes attr;
-    return hipFuncGetAttributes(&attr, reinterpret_cast<const void*>(select_kernel<HB>)) == hipSuccess
+    return hipFuncGetAttributes(&attr, reinterpret_cast<const void*>(select_kernel<GP>)) == hipSuccess
                ? static_cast<int>(attr.sharedSizeBytes)
                : 48 * 1024;
   }();
@@ -172,24 +167,24 @@ int key_room(int Hq) {
   return max(0, max_lds - stat - head_lds_bytes(Hq) - 64) / 4;
 }
 
-template <int HB>
-hipError_t launch_hb(const SelectArgs& t, hipStream_t st) {
-  const int room = key_room<HB>(t.m.Hq);
+template <int GP>
+hipError_t launch_gp(const SelectArgs& t, hipStream_t st) {
+  const int room = key_room<GP>(t.m.Hq);
   const int keys = min(room, t.m.max_vis);
   // one chunk keeps its keys in LDS: the launch plan guarantees they fit
   if (t.nchunks == 1 && keys < t.m.max_vis) return hipErrorInvalidValue;
   const size_t dyn = static_cast<size_t>(head_lds_bytes(t.m.Hq)) + static_cast<size_t>(keys) * 4;
-  hipLaunchKernelGGL((select_kernel<HB>), dim3(t.nchunks, t.m.B), dim3(kSelThreads), dyn, st, t, keys);
+  hipLaunchKernelGGL((select_kernel<GP>), dim3(t.nchunks, t.m.B), dim3(kSelThreads), dyn, st, t, keys);
   return hipGetLastError();
 }
 
 }  // namespace
 
-int select_tokens_per_round(int n_q_heads) { return kSelThreads / score_groups(n_q_heads).ng; }
+int select_tokens_per_round(int n_q_heads, int n_kv_heads) { return kSelThreads / score_lanes(n_kv_heads); }
 
 hipError_t launch_select(const SelectArgs& t, hipStream_t st) {
   if (t.m.Hq > kMaxSelectHeads || t.nchunks < 1 || t.chunk < 1) return hipErrorInvalidValue;
-  return score_groups(t.m.Hq).hpg <= 8 ? launch_hb<8>(t, st) : launch_hb<16>(t, st);
+  return t.m.zs_gp == 8 ? launch_gp<8>(t, st) : launch_gp<16>(t, st);
 }
 
 }  // namespace vp
