@@ -403,7 +403,7 @@ def main():
         "phases_ms": {"visual_pass": vis_ms, "text_pass": text_ms,
                       "mass_budget_scores_topk": tail_ms, "kept_pass_and_merge": attn_ms},
         "entry_point": "four calls" if args.calls else "vp_decode_step",
-        "plan": {"one_context_launch": one_launch, "fused_tail": bool(plan & vp.VP_PLAN_FUSED_TAIL)},
+        "plan": {"one_context_launch": one_launch, "select_in_one_group": bool(plan & vp.VP_PLAN_FUSED_TAIL)},
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the fp64 reference on the host", file=sys.stderr, flush=True)

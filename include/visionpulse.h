@@ -218,13 +218,13 @@ vp_status vp_sparse_decode_attn(const vp_shape* shape, const vp_layout* layout, 
  * vp_decode_step -- one whole decode step (Sec. 4.1-4.3): the results of
  *   vp_visual_mass(V) -> vp_budget -> vp_select_topk
  *     -> vp_sparse_decode_attn(VP_ATTN_TEXT_FROM_WORKSPACE)
- * on the same arguments, in fewer launches: where a sequence's visual tokens
- * fit one work-group's LDS (max_vis up to ~30 K, n_q_heads <= 256) and the
- * batch is small, the mass reduction, budget, scores and top-k of each
- * sequence run in one work-group. All outputs are written as by the four
- * calls (same arithmetic, same reduction order): mass_head [B, Hq],
- * mass_seq [B, 2], scores [B, max_vis], k [B], vis_idx [B, k_cap],
- * out [B, Hq, d]; V is required.
+ * on the same arguments, in fewer launches: the mass reduction, scores,
+ * budget and top-k of every sequence run in one launch (a sequence's visual
+ * ranks are scored in chunks on several work-groups, the last chunk to finish
+ * selects). All outputs are written as by the four calls (same arithmetic,
+ * same reduction order): mass_head [B, Hq], mass_seq [B, 2],
+ * scores [B, max_vis], k [B], vis_idx [B, k_cap], out [B, Hq, d]; V is
+ * required.
  *
  * events: optional caller-created hipEvent_t recorded on `stream`, i < n_events
  * (at most VP_STEP_EVENTS; NULL entries skipped):
@@ -250,9 +250,10 @@ vp_status vp_decode_step(const vp_shape* shape, const vp_layout* layout, const v
  *                               (small caches); events [0] and [1] are then
  *                               recorded together before it, so [1]..[2]
  *                               times the whole context pass;
- *   VP_PLAN_FUSED_TAIL          vp_decode_step runs the mass reduction,
- *                               budget, scores and top-k in one launch per
- *                               sequence (small visual sets).
+ *   VP_PLAN_FUSED_TAIL          vp_decode_step's select launch scores and
+ *                               selects each sequence in a single work-group
+ *                               (small visual sets; otherwise in chunks, the
+ *                               last chunk selecting).
  */
 #define VP_PLAN_ONE_CONTEXT_LAUNCH 1
 #define VP_PLAN_FUSED_TAIL 2
