@@ -152,7 +152,8 @@ def bench_layers(args, w, ds, bufs, loop, steps, warmup, sp, hip):
         seg0 = torch.zeros(2, dtype=torch.int32, device=ds.device)
         k0 = torch.zeros(w.B, dtype=torch.int32, device=ds.device)
         lay_dense = [vp.vp_layout(seq_len=(loop[2][t].seq_len if loop else ds.layout.seq_len),
-                                  vis_seg_off=seg_off0.data_ptr(), vis_seg=seg0.data_ptr())
+                                  vis_seg_off=seg_off0.data_ptr(), vis_seg=seg0.data_ptr(),
+                                  block_table=ds.layout.block_table)
                      for t in range(loop[0] if loop else 1)]
 
     def one(i):
@@ -219,6 +220,9 @@ def main():
                          "every other layer's attention over the anchor's kept set on its own KV cache")
     ap.add_argument("--dense", action="store_true",
                     help="with --layers: every layer attends to all of its cached tokens instead")
+    ap.add_argument("--paged", type=int, default=0, metavar="P",
+                    help="paged KV caches: blocks of P rows (a power of two) dealt to physical blocks in a "
+                         "seeded random order, addressed through a block table")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (3 times): the reference "
                          "for scaling the FETCH_SIZE / WRITE_SIZE counters")
@@ -267,16 +271,17 @@ def main():
             w.K[:, :, pos] = kr
             w.V[:, :, pos] = vr
             qs.append(q_t)
-        ds = S.DeviceStep(w)
+        ds = S.DeviceStep(w, block_size=args.paged)
         q_all = torch.from_numpy(np.ascontiguousarray(np.stack(qs)).view(np.int16)).view(torch.bfloat16).to(ds.device)
         lens = torch.tensor([[stream5.base_len + t + 1] * w.B for t in range(stream5.steps)], dtype=torch.int32,
                             device=ds.device)
         layouts = [vp.vp_layout(seq_len=lens[t].data_ptr(), vis_seg_off=ds.seg_off.data_ptr(),
-                                vis_seg=ds.seg.data_ptr()) for t in range(stream5.steps)]
+                                vis_seg=ds.seg.data_ptr(), block_table=ds.layout.block_table)
+                   for t in range(stream5.steps)]
         loop = (stream5.steps, q_all, layouts, [stream5.base_len + t + 1 for t in range(stream5.steps)])
     else:
         w = W.generate(cfg)
-        ds = S.DeviceStep(w)
+        ds = S.DeviceStep(w, block_size=args.paged)
     kv_bytes = ds.K.numel() * ds.K.element_size() * 2
     R = args.rotate or max(1, math.ceil(MALL_DEFEAT_BYTES / kv_bytes))
     layered = args.layers > 1 or args.dense
@@ -384,7 +389,8 @@ def main():
         "config": {"workload": f"config {cfg}: {WORKLOAD_NAMES[cfg]}", "batch": w.B, "q_heads": w.Hq,
                    "kv_heads": w.Hkv, "head_dim": w.d, "max_seq_len": w.S_cap, "visual_tokens": int(w.n_vis[0]),
                    "tau_mass": w.tau_mass, "retention_clamp_bp": [w.r_lo_bp, w.r_hi_bp],
-                   "kept_k": [int(x) for x in ks[:8]], "kv_rotation": R, "parallelism": "single GPU"},
+                   "kept_k": [int(x) for x in ks[:8]], "kv_rotation": R, "parallelism": "single GPU",
+                   "kv_block_size": args.paged or None},
         "step_algorithmic_bytes": step_bytes,
         "step_achieved_GBps": step_gbs,
         "step_frac_of_peak": step_gbs / PEAK_HBM_GBS,

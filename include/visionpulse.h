@@ -28,6 +28,13 @@
  *           base + b*kv_stride_b + h*kv_stride_h + s*kv_stride_s (elements) with
  *           the d elements of a row contiguous. Query head h reads KV head
  *           h / (Hq/Hkv) (grouped-query attention).
+ * Paged KV. With shape.block_size = P > 0 the caches are paged, as serving
+ *           engines keep them: token s of sequence b lives in physical block
+ *           blk = block_table[b * ceil(max_seq_len / P) + s / P] at
+ *           base + blk*kv_stride_b + h*kv_stride_h + (s % P)*kv_stride_s; P is a
+ *           power of two and kv_stride_b is the block stride. Block ids are
+ *           trusted like the rest of the layout (they must address blocks of
+ *           the caller's K and V).
  * Layout.   Each sequence b holds seq_len[b] cached tokens. Its visual tokens
  *           X_v (Sec. 4.2) are the union of the segments
  *           vis_seg[vis_seg_off[b] .. vis_seg_off[b+1]), each {start, length},
@@ -79,8 +86,8 @@ typedef struct vp_shape {
   int32_t max_vis;      /* >= N_v of every sequence; row stride of scores */
   int32_t max_segs;     /* >= visual segments of any sequence; <= 256 */
   int32_t k_cap;        /* row stride of vis_idx; >= every budget vp_budget can return */
-  int32_t reserved;     /* must be 0 */
-  int64_t kv_stride_b;  /* elements between sequences in K and V */
+  int32_t block_size;   /* 0: contiguous caches; P > 0 (a power of two <= 65536): paged caches of P rows per block */
+  int64_t kv_stride_b;  /* elements between sequences in K and V (paged: between physical blocks) */
   int64_t kv_stride_h;  /* elements between KV heads */
   int64_t kv_stride_s;  /* elements between token rows (>= head_dim) */
 } vp_shape;
@@ -90,6 +97,7 @@ typedef struct vp_layout {
   const int32_t* seq_len;      /* [B] cached tokens per sequence */
   const int32_t* vis_seg_off;  /* [B+1] CSR offsets into vis_seg */
   const int32_t* vis_seg;      /* [n_seg][2] {start, length} visual segments */
+  const int32_t* block_table;  /* [B][ceil(max_seq_len / block_size)] physical KV blocks (paged caches; else NULL) */
 } vp_layout;
 
 /* Method parameters (host-side). */

@@ -50,7 +50,8 @@ vp_status check_shape(const vp_shape* s) {
   if (s->max_vis < 1) return fail(VP_ERR_SHAPE, "max_vis %d < 1", s->max_vis);
   if (s->max_segs < 0 || s->max_segs > 256) return fail(VP_ERR_UNSUPPORTED, "max_segs %d outside [0, 256]", s->max_segs);
   if (s->k_cap < 1) return fail(VP_ERR_SHAPE, "k_cap %d < 1", s->k_cap);
-  if (s->reserved != 0) return fail(VP_ERR_SHAPE, "reserved field must be 0");
+  if (s->block_size < 0 || s->block_size > 65536 || (s->block_size & (s->block_size - 1)) != 0)
+    return fail(VP_ERR_SHAPE, "block_size %d: 0 (contiguous) or a power of two <= 65536", s->block_size);
   const int esz = s->dtype == VP_BF16 ? 2 : 4;
   const int64_t align_elems = 16 / esz;
   if (s->kv_stride_s < s->head_dim) return fail(VP_ERR_SHAPE, "kv_stride_s %lld < head_dim", (long long)s->kv_stride_s);
@@ -71,10 +72,11 @@ vp_status check_params(const vp_params* p) {
   return VP_OK;
 }
 
-vp_status check_layout(const vp_layout* l) {
+vp_status check_layout(const vp_shape* s, const vp_layout* l) {
   if (!l) return fail(VP_ERR_NULL, "layout is NULL");
   if (!l->seq_len || !l->vis_seg_off || !l->vis_seg)
     return fail(VP_ERR_NULL, "layout seq_len / vis_seg_off / vis_seg is NULL");
+  if (s->block_size > 0 && !l->block_table) return fail(VP_ERR_NULL, "paged caches (block_size > 0) need a block_table");
   return VP_OK;
 }
 
@@ -110,6 +112,14 @@ AttendArgs attend_args(const vp_shape* s, const vp_layout* l, const vp_params* p
   a.sb = s->kv_stride_b;
   a.sh = s->kv_stride_h;
   a.ss = s->kv_stride_s;
+  a.bs_log2 = -1;
+  a.nblk = 0;
+  a.block_table = nullptr;
+  if (s->block_size > 0) {
+    a.bs_log2 = __builtin_ctz(static_cast<unsigned>(s->block_size));
+    a.nblk = (s->max_seq_len + s->block_size - 1) / s->block_size;
+    a.block_table = l->block_table;
+  }
   a.seq_len = l->seq_len;
   a.seg_off = l->vis_seg_off;
   a.seg = l->vis_seg;
@@ -349,7 +359,7 @@ vp_status vp_visual_mass_timed(const vp_shape* shape, const vp_layout* layout, c
   if (n_events < 0 || n_events > VP_MASS_EVENTS) return fail(VP_ERR_RANGE, "n_events %d outside [0, %d]", n_events, VP_MASS_EVENTS);
   if (n_events > 0 && !events) return fail(VP_ERR_NULL, "events is NULL with n_events %d", n_events);
   if (vp_status e = check_shape(shape)) return e;
-  if (vp_status e = check_layout(layout)) return e;
+  if (vp_status e = check_layout(shape, layout)) return e;
   if (vp_status e = check_params(params)) return e;
   if (!q || !K || !mass_head || !mass_seq || !scores) return fail(VP_ERR_NULL, "q, K, mass_head, mass_seq, scores required");
   if (!aligned16(q) || !aligned16(K) || (V && !aligned16(V))) return fail(VP_ERR_SHAPE, "q, K, V must be 16-byte aligned");
@@ -393,7 +403,7 @@ vp_status vp_budget(const vp_shape* shape, const vp_layout* layout, const vp_par
                     int32_t* k, void* stream) {
   g_last_error.clear();
   if (vp_status e = check_shape(shape)) return e;
-  if (vp_status e = check_layout(layout)) return e;
+  if (vp_status e = check_layout(shape, layout)) return e;
   if (vp_status e = check_params(params)) return e;
   if (!mass_seq || !k) return fail(VP_ERR_NULL, "mass_seq and k required");
   if (vp_status e = check_budget_cap(shape, params)) return e;
@@ -406,7 +416,7 @@ vp_status vp_select_topk(const vp_shape* shape, const vp_layout* layout, const f
                          int32_t* vis_idx, void* stream) {
   g_last_error.clear();
   if (vp_status e = check_shape(shape)) return e;
-  if (vp_status e = check_layout(layout)) return e;
+  if (vp_status e = check_layout(shape, layout)) return e;
   if (!scores || !k || !vis_idx) return fail(VP_ERR_NULL, "scores, k, vis_idx required");
   if (hipError_t e = launch_topk(topk_args(shape, layout, scores, k, vis_idx), static_cast<hipStream_t>(stream)))
     return hip_fail(e, "top-k launch");
@@ -426,7 +436,7 @@ vp_status vp_budget_top_p(const vp_shape* shape, const vp_layout* layout, const 
                           void* stream) {
   g_last_error.clear();
   if (vp_status e = check_shape(shape)) return e;
-  if (vp_status e = check_layout(layout)) return e;
+  if (vp_status e = check_layout(shape, layout)) return e;
   if (!scores || !k) return fail(VP_ERR_NULL, "scores and k required");
   if (!(p >= 0.f && p <= 1.f)) return fail(VP_ERR_RANGE, "p %g outside [0, 1]", static_cast<double>(p));
   TopPArgs t{};
@@ -449,7 +459,7 @@ vp_status vp_sparse_decode_attn(const vp_shape* shape, const vp_layout* layout, 
                                 void* stream) {
   g_last_error.clear();
   if (vp_status e = check_shape(shape)) return e;
-  if (vp_status e = check_layout(layout)) return e;
+  if (vp_status e = check_layout(shape, layout)) return e;
   if (vp_status e = check_params(params)) return e;
   if (!q || !K || !V || !vis_idx || !k || !out) return fail(VP_ERR_NULL, "q, K, V, vis_idx, k, out required");
   if (!aligned16(q) || !aligned16(K) || !aligned16(V)) return fail(VP_ERR_SHAPE, "q, K, V must be 16-byte aligned");
@@ -481,7 +491,7 @@ vp_status vp_decode_step(const vp_shape* shape, const vp_layout* layout, const v
     return fail(VP_ERR_RANGE, "n_events %d outside [0, %d]", n_events, VP_STEP_EVENTS);
   if (n_events > 0 && !events) return fail(VP_ERR_NULL, "events is NULL with n_events %d", n_events);
   if (vp_status e = check_shape(shape)) return e;
-  if (vp_status e = check_layout(layout)) return e;
+  if (vp_status e = check_layout(shape, layout)) return e;
   if (vp_status e = check_params(params)) return e;
   if (!q || !K || !V || !mass_head || !mass_seq || !scores || !k || !vis_idx || !out)
     return fail(VP_ERR_NULL, "q, K, V, mass_head, mass_seq, scores, k, vis_idx, out required");

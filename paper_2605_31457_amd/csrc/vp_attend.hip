@@ -87,7 +87,10 @@ namespace {
 
 // waves per SIMD the register allocation is sized for (one wave per work-group)
 constexpr int attend_waves(int dt, int mode) {
-  return dt != VP_BF16 ? 1 : ((mode == MODE_VIS || mode == MODE_TEXT_STATS) ? VP_ATTEND_WAVES_LEAN : VP_ATTEND_WAVES);
+  return dt != VP_BF16 ? 1
+                       : (((mode & ~MODE_PAGED) == MODE_VIS || (mode & ~MODE_PAGED) == MODE_TEXT_STATS)
+                              ? VP_ATTEND_WAVES_LEAN
+                              : VP_ATTEND_WAVES);
 }
 
 // LDS floor per work-group: 20 KB keeps the bf16 passes that read V at 8
@@ -101,7 +104,10 @@ constexpr int attend_waves(int dt, int mode) {
 #endif
 constexpr int max_i(int x, int y) { return x > y ? x : y; }
 constexpr int lds_floor(int dt, int mode) {
-  return dt != VP_BF16 ? 0 : ((mode == MODE_VIS || mode == MODE_TEXT_STATS) ? VP_LDS_FLOOR_VIS : VP_LDS_FLOOR_TEXT);
+  return dt != VP_BF16 ? 0
+                       : (((mode & ~MODE_PAGED) == MODE_VIS || (mode & ~MODE_PAGED) == MODE_TEXT_STATS)
+                              ? VP_LDS_FLOOR_VIS
+                              : VP_LDS_FLOOR_TEXT);
 }
 
 template <int DT, int D>
@@ -270,6 +276,7 @@ struct Sub {
   int t0;       // first row of the 32-row sub-tile (cache position, or index into the kept list)
   int cls;      // TileClass (context pass)
   int kp;       // kept pass: lane r < 32 holds the cache position of row t0 + r (-1 past the list)
+  int blk;      // paged caches: lane r < 32 holds the physical block of row t0 + r
   SegWalker w;  // segment walker positioned at t0 (context pass)
 };
 
@@ -277,10 +284,12 @@ struct Sub {
 template <int DT, int D, int MODE>
 struct Pass {
   using C = Cfg<DT, D>;
-  static constexpr bool KEPT = MODE == MODE_KEPT;
-  static constexpr bool VIS = MODE == MODE_VIS;                  // visual rows: statistics + spill
-  static constexpr bool TSTATS = (MODE & MODE_TEXT_STATS) != 0;  // text rows: statistics
-  static constexpr bool ATTN = KEPT || (MODE & MODE_TEXT_ATTN) != 0;
+  static constexpr int BASE = MODE & ~MODE_PAGED;
+  static constexpr bool PAGED = (MODE & MODE_PAGED) != 0;        // rows through the block table
+  static constexpr bool KEPT = BASE == MODE_KEPT;
+  static constexpr bool VIS = BASE == MODE_VIS;                  // visual rows: statistics + spill
+  static constexpr bool TSTATS = (BASE & MODE_TEXT_STATS) != 0;  // text rows: statistics
+  static constexpr bool ATTN = KEPT || (BASE & MODE_TEXT_ATTN) != 0;
   static constexpr bool TEXT = !KEPT && !VIS;                    // a text-row pass
 
   const AttendArgs& a;
@@ -290,6 +299,9 @@ struct Pass {
   const char* Kb;
   const char* Vb;
   size_t rstride;
+  const int32_t* bt;  // paged caches: this sequence's block table (else null)
+  size_t bstride;     // paged caches: bytes per physical block
+  int bmask;          // paged caches: rows per block - 1
   float* zbase;  // spill plane of this KV group: row p holds the logits of its heads at position p
   QFrag<DT, D> qf;
   // visual pass: lane-local reference and sums (merged over a head's 4 lanes at the end)
@@ -334,6 +346,16 @@ struct Pass {
         n.cls = classify(n.w, t0, min(t0 + 32, r1));
       }
     }
+    if constexpr (PAGED) {
+      // the physical block of each of the tile's rows (the row that row_pos
+      // will read: clipped positions included)
+      if (lane < 32) {
+        int p;
+        if constexpr (KEPT) p = (n.kp < 0 || n.kp >= L) ? 0 : n.kp;
+        else p = min(t0 + lane, L - 1);
+        n.blk = bt[p >> __builtin_ctz(static_cast<unsigned>(bmask + 1))];
+      }
+    }
     return n;
   }
 
@@ -346,7 +368,13 @@ struct Pass {
     for (int j = 0; j < C::COPIES; ++j) {
       const int r = j * C::RPI + rr;
       const int piece = slot ^ (r & (C::PIECES - 1));
-      off[j] = static_cast<size_t>(row_pos(s, r)) * rstride + 16 * piece;
+      const int pos = row_pos(s, r);
+      if constexpr (PAGED) {
+        const int blk = __shfl(s.blk, r);
+        off[j] = static_cast<size_t>(blk) * bstride + static_cast<size_t>(pos & bmask) * rstride + 16 * piece;
+      } else {
+        off[j] = static_cast<size_t>(pos) * rstride + 16 * piece;
+      }
     }
   }
 
@@ -537,11 +565,16 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
 
   s.h = g * a.G + s.n16;
   s.hv = s.n16 < a.G;
-  s.Kb = static_cast<const char*>(a.K) + (static_cast<size_t>(b) * a.sb + static_cast<size_t>(g) * a.sh) * C::ESZ;
-  s.Vb = P::ATTN ? static_cast<const char*>(a.V) +
-                       (static_cast<size_t>(b) * a.sb + static_cast<size_t>(g) * a.sh) * C::ESZ
-                 : nullptr;
+  // contiguous caches: sequence b's rows from its base; paged caches: rows of
+  // physical blocks (the block offset is added per row)
+  constexpr bool paged = P::PAGED;
+  const size_t seq_off = paged ? 0 : static_cast<size_t>(b) * a.sb;
+  s.Kb = static_cast<const char*>(a.K) + (seq_off + static_cast<size_t>(g) * a.sh) * C::ESZ;
+  s.Vb = P::ATTN ? static_cast<const char*>(a.V) + (seq_off + static_cast<size_t>(g) * a.sh) * C::ESZ : nullptr;
   s.rstride = static_cast<size_t>(a.ss) * C::ESZ;
+  s.bt = paged ? a.block_table + static_cast<size_t>(b) * a.nblk : nullptr;
+  s.bstride = static_cast<size_t>(a.sb) * C::ESZ;
+  s.bmask = paged ? (1 << a.bs_log2) - 1 : 0;
   load_q<DT, D>(s.qf,
                 static_cast<const char*>(a.q) + (static_cast<size_t>(b) * a.Hq + (s.hv ? s.h : 0)) * C::ROWB,
                 s.hv, s.a4);
@@ -652,7 +685,7 @@ template <int DT, int D, int MODE>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(attend_waves(DT, MODE)))) void attend_kernel(
     const AttendArgs a) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[PassLds<DT, D, MODE>::BYTES];
-  if (MODE == MODE_VIS && static_cast<int>(blockIdx.x) == a.nparts) {
+  if ((MODE & ~MODE_PAGED) == MODE_VIS && static_cast<int>(blockIdx.x) == a.nparts) {
     step_setup(a, blockIdx.y, blockIdx.z);
     return;
   }
@@ -662,21 +695,21 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(attend_waves
 // Both context passes in one launch (grid.x = 2 parts): the first half of the
 // work-groups takes the visual role, the second the text role. Used where the
 // batch is small and launch latency, not bandwidth, bounds the step.
-template <int DT, int D>
+template <int DT, int D, int PG>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(attend_waves(DT, MODE_TEXT_BOTH)))) void
 attend_dual_kernel(const AttendArgs a) {
-  constexpr int BYTES = max_i(PassLds<DT, D, MODE_VIS>::BYTES, PassLds<DT, D, MODE_TEXT_BOTH>::BYTES);
+  constexpr int BYTES = max_i(PassLds<DT, D, MODE_VIS | PG>::BYTES, PassLds<DT, D, MODE_TEXT_BOTH | PG>::BYTES);
   __shared__ __attribute__((aligned(1024))) unsigned char lds[BYTES];
   const int x = blockIdx.x;
   if (x < a.nparts)
-    attend_body<DT, D, MODE_VIS>(a, lds, x, blockIdx.y, blockIdx.z);
+    attend_body<DT, D, MODE_VIS | PG>(a, lds, x, blockIdx.y, blockIdx.z);
   else if (x < 2 * a.nparts)
-    attend_body<DT, D, MODE_TEXT_BOTH>(a, lds, x - a.nparts, blockIdx.y, blockIdx.z);
+    attend_body<DT, D, MODE_TEXT_BOTH | PG>(a, lds, x - a.nparts, blockIdx.y, blockIdx.z);
   else
     step_setup(a, blockIdx.y, blockIdx.z);
 }
 
-template <int DT, int D>
+template <int DT, int D, int PG>
 hipError_t launch_dd(const AttendArgs& a, int mode, hipStream_t st) {
   // launches with the visual role carry one more work-group per sequence (step_setup)
   const int gx = mode == MODE_KEPT ? a.nsplit
@@ -685,22 +718,22 @@ hipError_t launch_dd(const AttendArgs& a, int mode, hipStream_t st) {
   const dim3 block(64);
   switch (mode) {
     case MODE_DUAL:
-      hipLaunchKernelGGL((attend_dual_kernel<DT, D>), grid, block, 0, st, a);
+      hipLaunchKernelGGL((attend_dual_kernel<DT, D, PG>), grid, block, 0, st, a);
       break;
     case MODE_VIS:
-      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_VIS>), grid, block, 0, st, a);
+      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_VIS | PG>), grid, block, 0, st, a);
       break;
     case MODE_TEXT_STATS:
-      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_TEXT_STATS>), grid, block, 0, st, a);
+      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_TEXT_STATS | PG>), grid, block, 0, st, a);
       break;
     case MODE_TEXT_ATTN:
-      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_TEXT_ATTN>), grid, block, 0, st, a);
+      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_TEXT_ATTN | PG>), grid, block, 0, st, a);
       break;
     case MODE_TEXT_BOTH:
-      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_TEXT_BOTH>), grid, block, 0, st, a);
+      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_TEXT_BOTH | PG>), grid, block, 0, st, a);
       break;
     case MODE_KEPT:
-      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_KEPT>), grid, block, 0, st, a);
+      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_KEPT | PG>), grid, block, 0, st, a);
       break;
     default:
       return hipErrorInvalidValue;
@@ -711,12 +744,13 @@ hipError_t launch_dd(const AttendArgs& a, int mode, hipStream_t st) {
 }  // namespace
 
 hipError_t launch_attend(const AttendArgs& a, int mode, int dtype, int head_dim, hipStream_t st) {
+  const bool paged = a.bs_log2 >= 0;
   if (dtype == VP_BF16) {
-    if (head_dim == 128) return launch_dd<VP_BF16, 128>(a, mode, st);
-    if (head_dim == 64) return launch_dd<VP_BF16, 64>(a, mode, st);
+    if (head_dim == 128) return paged ? launch_dd<VP_BF16, 128, MODE_PAGED>(a, mode, st) : launch_dd<VP_BF16, 128, 0>(a, mode, st);
+    if (head_dim == 64) return paged ? launch_dd<VP_BF16, 64, MODE_PAGED>(a, mode, st) : launch_dd<VP_BF16, 64, 0>(a, mode, st);
   } else if (dtype == VP_F32) {
-    if (head_dim == 128) return launch_dd<VP_F32, 128>(a, mode, st);
-    if (head_dim == 64) return launch_dd<VP_F32, 64>(a, mode, st);
+    if (head_dim == 128) return paged ? launch_dd<VP_F32, 128, MODE_PAGED>(a, mode, st) : launch_dd<VP_F32, 128, 0>(a, mode, st);
+    if (head_dim == 64) return paged ? launch_dd<VP_F32, 64, MODE_PAGED>(a, mode, st) : launch_dd<VP_F32, 64, 0>(a, mode, st);
   }
   return hipErrorInvalidValue;
 }

@@ -47,14 +47,18 @@ enum Mode : int {
   MODE_TEXT_ATTN = 4,   // text rows: attention partial (reads V)
   MODE_TEXT_BOTH = 6,
   MODE_KEPT = 8,        // kept visual rows: attention partial
-  MODE_DUAL = 16        // visual pass and text pass (statistics + attention) in one launch
+  MODE_DUAL = 16,       // visual pass and text pass (statistics + attention) in one launch
+  MODE_PAGED = 32       // flag: K and V rows addressed through a block table (paged caches)
 };
 
 struct AttendArgs {
   const void* q;
   const void* K;
   const void* V;
-  int64_t sb, sh, ss;   // KV strides (elements)
+  int64_t sb, sh, ss;   // KV strides (elements); paged caches: sb is the block stride
+  const int32_t* block_table;  // paged caches: [B][nblk] physical blocks (else null)
+  int bs_log2;          // paged caches: log2 of the rows per block; -1: contiguous
+  int nblk;             // row stride of block_table
   const int32_t* seq_len;
   const int32_t* seg_off;
   const int32_t* seg;

@@ -27,15 +27,43 @@ def make_params(w: Workload, sm_scale: float = 0.0) -> vp.vp_params:
                         r_lo_bp=w.r_lo_bp, r_hi_bp=w.r_hi_bp, clamp=int(w.clamp))
 
 
+def paged_cache(K: np.ndarray, V: np.ndarray, block_size: int, seed: int = 0):
+    """The caches [B][Hkv][S][d] as paged caches [NB][Hkv][block_size][d]:
+    block j of sequence b (rows j*block_size ...) goes to physical block
+    table[b, j], a seeded permutation of B*nblk + nblk//2 + 1 blocks (the spare
+    blocks stay zero). Returns (K_paged, V_paged, table int32 [B][nblk])."""
+    B, Hkv, S, d = K.shape
+    nblk = -(-S // block_size)
+    nb = B * nblk + nblk // 2 + 1
+    perm = np.random.default_rng(seed).permutation(nb)[:B * nblk].astype(np.int32)
+    table = perm.reshape(B, nblk)
+    Kp = np.zeros((nb, Hkv, block_size, d), K.dtype)
+    Vp = np.zeros((nb, Hkv, block_size, d), V.dtype)
+    for b in range(B):
+        for j in range(nblk):
+            r0, r1 = j * block_size, min(S, (j + 1) * block_size)
+            Kp[table[b, j], :, :r1 - r0] = K[b, :, r0:r1]
+            Vp[table[b, j], :, :r1 - r0] = V[b, :, r0:r1]
+    return Kp, Vp, np.ascontiguousarray(table)
+
+
 class DeviceStep:
     """Device-resident inputs, outputs and workspace of one step of workload ``w``."""
 
     def __init__(self, w: Workload, device="cuda:0", k_cap: int | None = None, max_vis: int | None = None,
-                 kv=None):
+                 kv=None, block_size: int = 0, block_seed: int = 0):
         self.w = w
         self.device = torch.device(device)
         self.q = _dev(w.q, self.device)
-        if kv is None:
+        self.block_size = block_size
+        self.block_table = None
+        if block_size:
+            # paged caches: the sequences' blocks of block_size rows dealt to
+            # physical blocks in a seeded random order (plus unused spare blocks)
+            Kp, Vp, table = paged_cache(w.K, w.V, block_size, block_seed)
+            self.K, self.V = _dev(Kp, self.device), _dev(Vp, self.device)
+            self.block_table = torch.from_numpy(table).to(self.device)
+        elif kv is None:
             self.K = _dev(w.K, self.device)
             self.V = _dev(w.V, self.device)
         else:
@@ -54,10 +82,11 @@ class DeviceStep:
         self.shape = vp.vp_shape(batch=B, n_q_heads=Hq, n_kv_heads=w.Hkv, head_dim=d,
                                  dtype=vp.VP_BF16 if w.dtype == "bf16" else vp.VP_F32,
                                  max_seq_len=w.S_cap, max_vis=self.max_vis, max_segs=w.max_segs,
-                                 k_cap=self.k_cap, reserved=0, kv_stride_b=st[0], kv_stride_h=st[1],
+                                 k_cap=self.k_cap, block_size=block_size, kv_stride_b=st[0], kv_stride_h=st[1],
                                  kv_stride_s=st[2])
         self.layout = vp.vp_layout(seq_len=self.seq_len.data_ptr(), vis_seg_off=self.seg_off.data_ptr(),
-                                   vis_seg=self.seg.data_ptr())
+                                   vis_seg=self.seg.data_ptr(),
+                                   block_table=self.block_table.data_ptr() if block_size else None)
         f32 = dict(dtype=torch.float32, device=self.device)
         i32 = dict(dtype=torch.int32, device=self.device)
         self.mass_head = torch.zeros(B, Hq, **f32)

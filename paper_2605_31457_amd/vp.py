@@ -31,12 +31,13 @@ class vp_shape(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32), ("max_seq_len", ctypes.c_int32),
                 ("max_vis", ctypes.c_int32), ("max_segs", ctypes.c_int32), ("k_cap", ctypes.c_int32),
-                ("reserved", ctypes.c_int32), ("kv_stride_b", ctypes.c_int64), ("kv_stride_h", ctypes.c_int64),
+                ("block_size", ctypes.c_int32), ("kv_stride_b", ctypes.c_int64), ("kv_stride_h", ctypes.c_int64),
                 ("kv_stride_s", ctypes.c_int64)]
 
 
 class vp_layout(ctypes.Structure):
-    _fields_ = [("seq_len", ctypes.c_void_p), ("vis_seg_off", ctypes.c_void_p), ("vis_seg", ctypes.c_void_p)]
+    _fields_ = [("seq_len", ctypes.c_void_p), ("vis_seg_off", ctypes.c_void_p), ("vis_seg", ctypes.c_void_p),
+                ("block_table", ctypes.c_void_p)]
 
 
 class vp_params(ctypes.Structure):

@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(L):
 
 def _shape(**kw):
     s = dict(batch=2, n_q_heads=28, n_kv_heads=4, head_dim=128, dtype=vp.VP_BF16, max_seq_len=4096,
-             max_vis=1296, max_segs=1, k_cap=64, reserved=0, kv_stride_b=4 * 4096 * 128,
+             max_vis=1296, max_segs=1, k_cap=64, block_size=0, kv_stride_b=4 * 4096 * 128,
              kv_stride_h=4096 * 128, kv_stride_s=128)
     s.update(kw)
     return vp.vp_shape(**s)
@@ -51,7 +51,8 @@ def _params(**kw):
 
 def test_struct_layout_matches_header(L):
     assert ctypes.sizeof(vp.vp_shape) == 64 and vp.vp_shape.kv_stride_b.offset == 40
-    assert ctypes.sizeof(vp.vp_params) == 24 and ctypes.sizeof(vp.vp_layout) == 24
+    assert ctypes.sizeof(vp.vp_params) == 24 and ctypes.sizeof(vp.vp_layout) == 32
+    assert vp.vp_shape.block_size.offset == 36 and vp.vp_layout.block_table.offset == 24
 
 
 def test_workspace_size_is_pure_and_scales(L):
@@ -72,7 +73,9 @@ def test_workspace_size_is_pure_and_scales(L):
     (dict(k_cap=0), "VP_ERR_SHAPE"),
     (dict(kv_stride_s=64), "VP_ERR_SHAPE"),
     (dict(kv_stride_s=130), "VP_ERR_SHAPE"),
-    (dict(reserved=1), "VP_ERR_SHAPE"),
+    (dict(block_size=3), "VP_ERR_SHAPE"),
+    (dict(block_size=-16), "VP_ERR_SHAPE"),
+    (dict(block_size=1 << 17), "VP_ERR_SHAPE"),
     (dict(max_segs=1000), "VP_ERR_UNSUPPORTED"),
 ])
 def test_shape_validation(L, kw, status):
@@ -105,6 +108,10 @@ def test_calls_reject_nulls_and_bad_params_before_launch(L):
         vp.vp_select_topk(s, lay, fake, None, fake, 0)
     with pytest.raises(vp.VPError, match="VP_ERR_NULL"):
         vp.vp_select_topk(s, vp.vp_layout(seq_len=0x1000, vis_seg_off=None, vis_seg=0x3000), fake, fake, fake, 0)
+    # paged caches need a block table
+    with pytest.raises(vp.VPError, match="VP_ERR_NULL"):
+        vp.vp_visual_mass(_shape(block_size=32), lay, p, fake, fake, None, fake, fake, fake, fake,
+                          vp.vp_workspace_size(_shape(block_size=32)), 0)
     with pytest.raises(vp.VPError, match="VP_ERR_RANGE"):
         vp.vp_sparse_decode_attn(s, lay, p, fake, fake, fake, fake, fake, fake, 8, fake, ws_bytes, 0)
     with pytest.raises(vp.VPError, match="VP_ERR_SHAPE"):
