@@ -142,6 +142,23 @@ def plant(w, params: O.OracleParams, seqs=None):
     return res, log
 
 
+def plant_kv_groups(w, params: O.OracleParams, seqs=None):
+    """plant() for the per-KV-group variant: every KV group of every sequence is
+    planted as the one-KV-head sequence it is in that variant (edits stay inside
+    the group's own KV head). Returns {b: GroupedResult}, log."""
+    res, log = {}, []
+    G = w.Hq // w.Hkv
+    for b in (range(w.B) if seqs is None else seqs):
+        for g in range(w.Hkv):
+            lg = []
+            _, edits = plant_sequence(w.q[b, g * G:(g + 1) * G], w.K[b, g:g + 1], w.V[b, g:g + 1],
+                                      int(w.seq_len[b]), w.segments[b], params, log=lg)
+            log.append({"seq": b, "group": g, **(lg[0] if lg else {}), "n_edits": len(edits)})
+        res[b] = O.decode_step_sequence_kv_groups(w.q[b], w.K[b], w.V[b], int(w.seq_len[b]),
+                                                  w.segments[b], params)
+    return res, log
+
+
 def params_of(w) -> O.OracleParams:
     return O.OracleParams(tau_mass=w.tau_mass, tau_score=w.tau_score,
                           r_lo_bp=w.r_lo_bp, r_hi_bp=w.r_hi_bp, clamp=w.clamp)

@@ -32,7 +32,12 @@ Readings where the paper is silent:
   A12 the pruned softmax is renormalised over the kept context only; an empty
      context yields a zero output;
   A18 the Top-p budget counts visual tokens in the Eq. (3) order until their
-     Eq. (2) scores sum to p (all of them if they never do).
+     Eq. (2) scores sum to p (all of them if they never do);
+  A19 the per-KV-group variant (an extension; the paper keeps one set per
+     sequence) runs the whole method on each KV group g as if it were a
+     sequence of its own: the G query heads that read KV head g give the head
+     mean and head max of Eq. (5)/(7), the head average of Eq. (2) and a budget
+     k_g, and those G heads attend over their group's own kept set.
 
 Parity status: every function below is pinned by tests/test_oracle_pins.py
 (closed forms, invariants, brute force, library cross-checks and the
@@ -49,7 +54,7 @@ __all__ = [
     "as_f64", "logits", "tempered_attention", "visual_mass", "retention_bounds",
     "budget", "budget_top_p", "importance_scores", "select_top_k", "pruned_attention",
     "OracleParams", "SequenceResult", "decode_step_sequence", "decode_step",
-    "visual_positions", "text_positions",
+    "visual_positions", "text_positions", "GroupedResult", "decode_step_sequence_kv_groups",
 ]
 
 
@@ -304,3 +309,42 @@ def decode_step(q, K, V, seq_len, segments, params: OracleParams,
     return {b: decode_step_sequence(q[b], K[b], V[b], int(seq_len[b]), segments[b],
                                     params, keep_logits=keep_logits)
             for b in seqs}
+
+
+# --------------------------------------------------------------------------
+# per-KV-group budgets and kept sets (reading A19)
+# --------------------------------------------------------------------------
+@dataclass
+class GroupedResult:
+    mass_head: np.ndarray        # [Hq] m^{vis}_{t,h} (the same as per sequence)
+    M_vis: np.ndarray            # [Hkv] mean of m^{vis} over the group's heads
+    M_vis_max: np.ndarray        # [Hkv] max over the group's heads
+    scores: np.ndarray           # [Hkv, N_v] S_{g,i} = (1/G) sum_{h in g} A_{t,h}(v_i)
+    k: np.ndarray                # [Hkv] K_{t,g}
+    vis_idx: list                # Hkv arrays of kept positions, ascending
+    out: np.ndarray | None       # [Hq, d]; head h attends over its group's kept set + text
+
+
+def decode_step_sequence_kv_groups(q: np.ndarray, K: np.ndarray, V: np.ndarray,
+                                   seq_len: int, segments, params: OracleParams,
+                                   with_output: bool = True) -> GroupedResult:
+    """The per-step path with one budget and one kept set per KV group (A19).
+
+    KV group g is the sub-problem made of query heads g*G .. (g+1)*G - 1 and KV
+    head g alone; each is solved by decode_step_sequence, which is the whole
+    definition of the variant.
+    """
+    Hq, d = q.shape
+    Hkv = K.shape[0]
+    assert Hq % Hkv == 0
+    G = Hq // Hkv
+    parts = [decode_step_sequence(q[g * G:(g + 1) * G], K[g:g + 1], V[g:g + 1], seq_len, segments,
+                                  params, with_output=with_output) for g in range(Hkv)]
+    return GroupedResult(
+        mass_head=np.concatenate([r.mass_head for r in parts]),
+        M_vis=np.array([r.M_vis for r in parts]),
+        M_vis_max=np.array([r.M_vis_max for r in parts]),
+        scores=np.stack([r.scores for r in parts]),
+        k=np.array([r.k for r in parts], dtype=np.int64),
+        vis_idx=[r.vis_idx for r in parts],
+        out=np.concatenate([r.out for r in parts]) if with_output else None)

@@ -362,3 +362,131 @@ def test_exact_rational_tiny_case():
     num = sum(Fraction(w[j]) * j for j in J)
     den = sum(Fraction(w[j]) for j in J)
     assert r.out[0, 0] == pytest.approx(float(num / den), rel=1e-14)
+
+
+# ---------------------------------------------------------------------------
+# per-KV-group budgets and kept sets (the variant with one Eq. (7) budget and one
+# Eq. (3) set per KV group; its reading of Eq. (2)/(5)/(7) is stated in the
+# reference's header)
+# ---------------------------------------------------------------------------
+def _brute_groups(q, K, V, L, segs, tau_mass, r_lo_bp, r_hi_bp):
+    """Pure-Python loops over a tiny case: for each KV group g, the tempered and
+    untempered softmax of each of its query heads over every token, the group's
+    head mean / head max of the visual mass, k_g = ceil(max * N_v) clamped to
+    [ceil(lo N_v), floor(hi N_v)], the group's score average, the top k_g by
+    (score desc, position asc) and each head's attention over kept + text."""
+    Hq, d = len(q), len(q[0])
+    Hkv = len(K)
+    G = Hq // Hkv
+    vis = [p for s, n in segs for p in range(s, s + n)]
+    nv = len(vis)
+    res = []
+    for g in range(Hkv):
+        masses, S = [], [0.0] * nv
+        outs = []
+        for j in range(G):
+            h = g * G + j
+            z = [sum(q[h][c] * K[g][t][c] for c in range(d)) / math.sqrt(d) for t in range(L)]
+            zt = max(z)
+            et = [math.exp((x - zt) / tau_mass) for x in z]
+            masses.append(sum(et[p] for p in vis) / sum(et))
+            e1 = [math.exp(x - zt) for x in z]
+            tot = sum(e1)
+            for i, p in enumerate(vis):
+                S[i] += e1[p] / tot / G
+        mean, mx = sum(masses) / G, max(masses)
+        k = math.ceil(mx * nv)
+        lo = -((-r_lo_bp * nv) // 10000)
+        hi = max((r_hi_bp * nv) // 10000, lo)
+        k = min(max(k, lo), hi, nv)
+        ranked = sorted(range(nv), key=lambda i: (-S[i], vis[i]))
+        kept = sorted(vis[i] for i in ranked[:k])
+        J = sorted(set(kept) | (set(range(L)) - set(vis)))
+        for j in range(G):
+            h = g * G + j
+            z = [sum(q[h][c] * K[g][t][c] for c in range(d)) / math.sqrt(d) for t in J]
+            zm = max(z)
+            e = [math.exp(x - zm) for x in z]
+            outs.append([sum(e[i] * V[g][t][c] for i, t in enumerate(J)) / sum(e) for c in range(d)])
+        res.append(dict(masses=masses, mean=mean, mx=mx, S=S, k=k, kept=kept, out=outs))
+    return res
+
+
+def test_kv_groups_brute_force_tiny():
+    rng = np.random.default_rng(31)
+    for trial in range(6):
+        Hkv = (1, 2, 3)[trial % 3]
+        G = 1 + trial % 2
+        q, K, V, L, segs = _rand_case(rng, Hq=Hkv * G, Hkv=Hkv, d=3, L=40, segs=((2, 15), (20, 12)), scale=2.0)
+        p = O.OracleParams(tau_mass=0.5, r_lo_bp=500, r_hi_bp=4000)
+        r = O.decode_step_sequence_kv_groups(q, K, V, L, segs, p)
+        bf = _brute_groups(q.tolist(), K.tolist(), V.tolist(), L, segs, 0.5, 500, 4000)
+        for g in range(Hkv):
+            np.testing.assert_allclose(r.mass_head[g * G:(g + 1) * G], bf[g]["masses"], rtol=1e-12)
+            assert r.M_vis[g] == pytest.approx(bf[g]["mean"], rel=1e-12)
+            assert r.M_vis_max[g] == pytest.approx(bf[g]["mx"], rel=1e-12)
+            np.testing.assert_allclose(r.scores[g], bf[g]["S"], rtol=1e-12)
+            assert r.k[g] == bf[g]["k"]
+            assert list(r.vis_idx[g]) == bf[g]["kept"]
+            np.testing.assert_allclose(r.out[g * G:(g + 1) * G], bf[g]["out"], rtol=1e-11, atol=1e-13)
+
+
+def test_kv_groups_aggregate_to_the_sequence_quantities():
+    """Equal group sizes: the head mean of Eq. (5) is the mean of the group means,
+    the head max is the max of the group maxima, and the Eq. (2) average is the
+    mean of the group averages."""
+    rng = np.random.default_rng(32)
+    q, K, V, L, segs = _rand_case(rng, Hq=12, Hkv=3, d=8, L=60, segs=((5, 30), (40, 10)))
+    p = O.OracleParams(clamp=False, tau_mass=0.3)
+    r = O.decode_step_sequence(q, K, V, L, segs, p)
+    gr = O.decode_step_sequence_kv_groups(q, K, V, L, segs, p)
+    np.testing.assert_allclose(gr.mass_head, r.mass_head, rtol=1e-13)
+    assert gr.M_vis.mean() == pytest.approx(r.M_vis, rel=1e-13)
+    assert gr.M_vis_max.max() == pytest.approx(r.M_vis_max, rel=1e-13)
+    np.testing.assert_allclose(gr.scores.mean(axis=0), r.scores, rtol=1e-12)
+    # the group whose head attains the sequence head max sets the largest budget
+    g_star = int(np.argmax(r.mass_head)) // 4
+    assert gr.k[g_star] == r.k == gr.k.max()
+
+
+def test_kv_groups_replicated_groups_match_the_sequence():
+    """Every KV group a copy of the same KV head and the same G query heads: each
+    group's budget, kept set and outputs are the per-sequence ones."""
+    rng = np.random.default_rng(33)
+    q1, K1, V1, L, segs = _rand_case(rng, Hq=2, Hkv=1, d=8, L=80, segs=((10, 50),))
+    q = np.tile(q1, (3, 1))
+    K = np.tile(K1, (3, 1, 1))
+    V = np.tile(V1, (3, 1, 1))
+    p = O.OracleParams(r_lo_bp=500, r_hi_bp=3000)
+    r = O.decode_step_sequence(q, K, V, L, segs, p)
+    gr = O.decode_step_sequence_kv_groups(q, K, V, L, segs, p)
+    for g in range(3):
+        assert gr.k[g] == r.k and list(gr.vis_idx[g]) == list(r.vis_idx)
+        np.testing.assert_allclose(gr.scores[g], r.scores, rtol=1e-12)
+    np.testing.assert_allclose(gr.out, r.out, rtol=1e-12)
+
+
+def test_kv_groups_permuting_groups_permutes_results():
+    rng = np.random.default_rng(34)
+    q, K, V, L, segs = _rand_case(rng, Hq=6, Hkv=3, d=8, L=70, segs=((0, 20), (30, 25)), scale=1.5)
+    p = O.OracleParams(tau_mass=0.2, r_lo_bp=200, r_hi_bp=4000)
+    perm = [2, 0, 1]
+    qp = np.concatenate([q[2 * g:2 * g + 2] for g in perm])
+    a = O.decode_step_sequence_kv_groups(q, K, V, L, segs, p)
+    b = O.decode_step_sequence_kv_groups(qp, K[perm], V[perm], L, segs, p)
+    assert list(b.k) == [a.k[g] for g in perm]
+    assert [list(x) for x in b.vis_idx] == [list(a.vis_idx[g]) for g in perm]
+    np.testing.assert_allclose(b.out, np.concatenate([a.out[2 * g:2 * g + 2] for g in perm]), rtol=1e-13)
+    # distinct groups really do pick different sets here (the test is not vacuous)
+    assert len({tuple(x) for x in a.vis_idx}) > 1
+
+
+def test_kv_groups_single_group_is_the_sequence_path():
+    rng = np.random.default_rng(35)
+    q, K, V, L, segs = _rand_case(rng, Hq=4, Hkv=1, d=8, L=50, segs=((5, 30),))
+    p = O.OracleParams()
+    r = O.decode_step_sequence(q, K, V, L, segs, p)
+    gr = O.decode_step_sequence_kv_groups(q, K, V, L, segs, p)
+    assert gr.k[0] == r.k and list(gr.vis_idx[0]) == list(r.vis_idx)
+    assert gr.M_vis[0] == r.M_vis and gr.M_vis_max[0] == r.M_vis_max
+    np.testing.assert_array_equal(gr.out, r.out)

@@ -36,3 +36,21 @@ def test_margin_detects_integer_crossing():
     p = O.OracleParams(clamp=False)
     assert not P.margin_ok(0.5, 256, p)          # 128 exactly: 127.99 vs 128.01
     assert P.margin_ok(0.502, 256, p)
+
+
+def test_plant_kv_groups_cfg2():
+    """Per-KV-group planting: every group's budget margin and score gap hold, and
+    the stored tensor is what the reference read."""
+    w = W.generate(2)
+    p = P.params_of(w)
+    res, log = P.plant_kv_groups(w, p)
+    r = res[0]
+    L = int(w.seq_len[0])
+    vis = O.visual_positions(L, w.segments[0])
+    assert len(log) == w.Hkv
+    for g in range(w.Hkv):
+        assert P.boundary_gap(r.scores[g], vis, int(r.k[g])) >= P.GAP
+        assert P.margin_ok(r.M_vis_max[g], len(vis), p)
+    r2 = O.decode_step_sequence_kv_groups(w.q[0], w.K[0], w.V[0], L, w.segments[0], p, with_output=False)
+    assert list(r2.k) == list(r.k)
+    assert all(list(a) == list(b) for a, b in zip(r2.vis_idx, r.vis_idx))
