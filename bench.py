@@ -63,14 +63,15 @@ class Hip:
         return t.value
 
 
-def algorithmic_bytes(w, ks, lens=None):
+def algorithmic_bytes(w, ks, lens=None, rows=1):
     """Bytes the method must move at least once per step, by kernel.
 
     Visual pass: the K rows of visual tokens (their Eq. (6) logits). Text pass:
     the K and V rows of text tokens. Kept pass: K and V rows of the k kept
     visual tokens. q, outputs, scores and indices are < 1% and not counted.
     lens: per-step sequence lengths of a decode loop (same for every sequence);
-    the figures are then averages over its steps."""
+    the figures are then averages over its steps. rows: selection rows per
+    sequence (Hkv with per-KV-group budgets: KV head g reads its own k_g rows)."""
     esz = 2 if w.dtype == "bf16" else 4
     row = w.Hkv * w.d * esz
     vis = text = kept = 0
@@ -79,7 +80,7 @@ def algorithmic_bytes(w, ks, lens=None):
         nv = sum(n for _, n in w.segments[b])
         vis += nv * row
         text += sum(2 * (L - nv) * row for L in Ls) / len(Ls)
-        kept += 2 * int(ks[b]) * row
+        kept += 2 * int(sum(ks[b * rows:(b + 1) * rows])) * row // rows  # a row covers Hkv/rows KV heads
     return {"visual": vis, "text": text, "kept": kept}
 
 
@@ -108,7 +109,7 @@ def counter_traffic(cfg: int, kernel: str):
     return entry["traffic_bytes"]
 
 
-def cpu_baseline(w, budget_s: float):
+def cpu_baseline(w, budget_s: float, kv_groups: bool = False):
     """fp64 reference on this host: whole sequences until about budget_s seconds."""
     import numpy as np
     from oracle import vp_oracle as O
@@ -119,7 +120,8 @@ def cpu_baseline(w, budget_s: float):
     n = 0
     while True:
         b = n % w.B
-        O.decode_step_sequence(w.q[b], w.K[b], w.V[b], int(w.seq_len[b]), w.segments[b], p)
+        run = O.decode_step_sequence_kv_groups if kv_groups else O.decode_step_sequence
+        run(w.q[b], w.K[b], w.V[b], int(w.seq_len[b]), w.segments[b], p)
         n += 1
         el = time.perf_counter() - t0
         if el >= budget_s and n >= 1:
@@ -183,7 +185,7 @@ def bench_layers(args, w, ds, bufs, loop, steps, warmup, sp, hip):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ks = ds.k.cpu().numpy()
-    nb = algorithmic_bytes(w, ks, None if loop is None else loop[3])
+    nb = algorithmic_bytes(w, ks, None if loop is None else loop[3], rows=ds.rows)
     esz = 2 if w.dtype == "bf16" else 4
     row = w.Hkv * w.d * esz
     if args.dense:
@@ -223,6 +225,8 @@ def main():
     ap.add_argument("--paged", type=int, default=0, metavar="P",
                     help="paged KV caches: blocks of P rows (a power of two) dealt to physical blocks in a "
                          "seeded random order, addressed through a block table")
+    ap.add_argument("--kv-groups", action="store_true",
+                    help="one budget and kept set per KV group (VP_SCOPE_KV_GROUP) instead of per sequence")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device-to-device copy of MIB MiB (3 times): the reference "
                          "for scaling the FETCH_SIZE / WRITE_SIZE counters")
@@ -271,7 +275,7 @@ def main():
             w.K[:, :, pos] = kr
             w.V[:, :, pos] = vr
             qs.append(q_t)
-        ds = S.DeviceStep(w, block_size=args.paged)
+        ds = S.DeviceStep(w, block_size=args.paged, kv_groups=args.kv_groups)
         q_all = torch.from_numpy(np.ascontiguousarray(np.stack(qs)).view(np.int16)).view(torch.bfloat16).to(ds.device)
         lens = torch.tensor([[stream5.base_len + t + 1] * w.B for t in range(stream5.steps)], dtype=torch.int32,
                             device=ds.device)
@@ -281,7 +285,7 @@ def main():
         loop = (stream5.steps, q_all, layouts, [stream5.base_len + t + 1 for t in range(stream5.steps)])
     else:
         w = W.generate(cfg)
-        ds = S.DeviceStep(w, block_size=args.paged)
+        ds = S.DeviceStep(w, block_size=args.paged, kv_groups=args.kv_groups)
     kv_bytes = ds.K.numel() * ds.K.element_size() * 2
     R = args.rotate or max(1, math.ceil(MALL_DEFEAT_BYTES / kv_bytes))
     layered = args.layers > 1 or args.dense
@@ -362,7 +366,7 @@ def main():
     if loop is None:
         assert np.array_equal(ds.k.cpu().numpy(), ks), "budget changed between warm-up and timed steps"
 
-    nb = algorithmic_bytes(w, ks, None if loop is None else loop[3])
+    nb = algorithmic_bytes(w, ks, None if loop is None else loop[3], rows=ds.rows)
     step_bytes = nb["visual"] + nb["text"] + nb["kept"]
     ms_per_step = wall * 1e3 / steps
     plan = vp.vp_step_plan(ds.shape, ds.params)
@@ -390,7 +394,8 @@ def main():
                    "kv_heads": w.Hkv, "head_dim": w.d, "max_seq_len": w.S_cap, "visual_tokens": int(w.n_vis[0]),
                    "tau_mass": w.tau_mass, "retention_clamp_bp": [w.r_lo_bp, w.r_hi_bp],
                    "kept_k": [int(x) for x in ks[:8]], "kv_rotation": R, "parallelism": "single GPU",
-                   "kv_block_size": args.paged or None},
+                   "kv_block_size": args.paged or None,
+                   "budget_scope": "per KV group" if args.kv_groups else "per sequence"},
         "step_algorithmic_bytes": step_bytes,
         "step_achieved_GBps": step_gbs,
         "step_frac_of_peak": step_gbs / PEAK_HBM_GBS,
@@ -413,7 +418,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         print("[bench] timing the fp64 reference on the host", file=sys.stderr, flush=True)
-        res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds)
+        res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, args.kv_groups)
     print(json.dumps(res), flush=True)
 
 

@@ -48,6 +48,17 @@
  * Errors.   Host-checkable problems (null pointers, unsupported shapes, small
  *           workspace, bad parameters) return an error before anything is
  *           enqueued. A failed kernel launch returns VP_ERR_HIP.
+ * Scope.    shape.scope chooses where the budget and the kept set live.
+ *           VP_SCOPE_SEQUENCE (the paper's method, Sec. 4.2/4.3): one k and one
+ *           kept set per sequence, from the mean and max over all Hq query
+ *           heads, shared by every head. VP_SCOPE_KV_GROUP (a per-KV-group
+ *           variant): each KV group g (query heads g*G .. g*G+G-1, G = Hq/Hkv)
+ *           is treated as a sequence of its own: Eq. (5)/(7) take the mean and
+ *           max over the group's G heads, Eq. (2) averages over them, and the
+ *           group's heads attend over the group's own kept set. Per-sequence
+ *           results are then held in R = Hkv "selection rows" per sequence
+ *           (row b*Hkv + g), else R = 1 (row b): below, mass_seq is [B*R, 2],
+ *           scores [B*R, max_vis], k [B*R] and vis_idx [B*R, k_cap].
  * Dtypes.   VP_BF16: q, K, V, out are bfloat16; VP_F32: all float32. Logits,
  *           softmax statistics, masses and scores are float32; accumulation is
  *           float32 (bf16 products are exact in float32).
@@ -75,6 +86,9 @@ typedef enum vp_status {
 
 typedef enum vp_dtype { VP_F32 = 0, VP_BF16 = 1 } vp_dtype;
 
+/* Where budgets and kept sets live (see "Scope" above). */
+typedef enum vp_scope { VP_SCOPE_SEQUENCE = 0, VP_SCOPE_KV_GROUP = 1 } vp_scope;
+
 /* Host-side description of one step's tensors (validated synchronously). */
 typedef struct vp_shape {
   int32_t batch;        /* B >= 1 */
@@ -87,6 +101,8 @@ typedef struct vp_shape {
   int32_t max_segs;     /* >= visual segments of any sequence; <= 256 */
   int32_t k_cap;        /* row stride of vis_idx; >= every budget vp_budget can return */
   int32_t block_size;   /* 0: contiguous caches; P > 0 (a power of two <= 65536): paged caches of P rows per block */
+  int32_t scope;        /* vp_scope: selection rows per sequence R = 1 (VP_SCOPE_SEQUENCE) or Hkv (VP_SCOPE_KV_GROUP) */
+  int32_t reserved;     /* must be 0 */
   int64_t kv_stride_b;  /* elements between sequences in K and V (paged: between physical blocks) */
   int64_t kv_stride_h;  /* elements between KV heads */
   int64_t kv_stride_s;  /* elements between token rows (>= head_dim) */
@@ -130,9 +146,10 @@ vp_status vp_workspace_size(const vp_shape* shape, size_t* bytes);
  *
  *   Z_{h,j}      = sm_scale * <q_h, K_{g(h), j}>                j < seq_len
  *   mass_head    = sum_{j visual} softmax_j(Z_h / tau_mass)      [B, Hq]
- *   mass_seq     = {mean_h mass_head, max_h mass_head}           [B, 2]
- *   scores[b, i] = (1/Hq) sum_h softmax_j(Z_h / tau_score)_{v_i} [B, max_vis], rank order;
+ *   mass_seq     = {mean_h mass_head, max_h mass_head}           [B*R, 2]
+ *   scores[b, i] = (1/Hq) sum_h softmax_j(Z_h / tau_score)_{v_i} [B*R, max_vis], rank order;
  *                  entries i >= N_v of the sequence are not written.
+ * (VP_SCOPE_KV_GROUP: row b*Hkv + g, with h over group g's G heads and 1/G.)
  *
  * q: [B, Hq, d]; K: cache; V: cache or NULL. When V is non-NULL the same pass
  * over K also accumulates the softmax-weighted text-token values (the text
@@ -172,7 +189,8 @@ vp_status vp_visual_mass_timed(const vp_shape* shape, const vp_layout* layout, c
  * and to [0, N_v]. The product is formed in double from the float mass, so the
  * rounding decision is exact. N_v = 0 gives 0.
  *
- * mass_seq: [B, 2] device (column 1 = M_vis,max); k: [B] int32 device.
+ * mass_seq: [B*R, 2] device (column 1 = M_vis,max); k: [B*R] int32 device
+ * (one budget per selection row; N_v is the row's sequence's).
  */
 vp_status vp_budget(const vp_shape* shape, const vp_layout* layout, const vp_params* params,
                     const float* mass_seq, int32_t* k, void* stream);
@@ -186,29 +204,31 @@ vp_status vp_budget(const vp_shape* shape, const vp_layout* layout, const vp_par
  * fp32 score rounded down), so the count is deterministic. Feed k to
  * vp_select_topk (which clamps it to k_cap).
  *
- * scores: [B, max_vis] float (from vp_visual_mass); k: [B] int32 device.
+ * scores: [B*R, max_vis] float (from vp_visual_mass); k: [B*R] int32 device.
  * VP_ERR_RANGE unless 0 <= p <= 1.
  */
 vp_status vp_budget_top_p(const vp_shape* shape, const vp_layout* layout, const float* scores, float p,
                           int32_t* k, void* stream);
 
 /*
- * vp_select_topk -- Eq. (3): for every sequence, the k[b] visual tokens with the
- * largest score, ties to the lower position; written as absolute cache
- * positions in ascending order to vis_idx[b, 0 .. k[b]) and -1 in
- * vis_idx[b, k[b] .. k_cap). k[b] is clamped to [0, min(N_v, k_cap)].
+ * vp_select_topk -- Eq. (3): for every selection row r (of sequence b), the
+ * k[r] visual tokens with the largest score, ties to the lower position;
+ * written as absolute cache positions in ascending order to
+ * vis_idx[r, 0 .. k[r]) and -1 in vis_idx[r, k[r] .. k_cap). k[r] is clamped
+ * to [0, min(N_v, k_cap)].
  *
- * scores: [B, max_vis] float (from vp_visual_mass); k: [B] int32 device;
- * vis_idx: [B, k_cap] int32 device.
+ * scores: [B*R, max_vis] float (from vp_visual_mass); k: [B*R] int32 device;
+ * vis_idx: [B*R, k_cap] int32 device.
  */
 vp_status vp_select_topk(const vp_shape* shape, const vp_layout* layout,
                          const float* scores, const int32_t* k, int32_t* vis_idx, void* stream);
 
 /*
  * vp_sparse_decode_attn -- the step's attention over the pruned context
- * J_b = {vis_idx[b, 0 .. k[b])} U {text positions of b} (Sec. 4.1/4.2; the
+ * J_b = {vis_idx[r, 0 .. k[r])} U {text positions of b} (Sec. 4.1/4.2; the
  * dropped visual tokens are absent from the softmax, which is renormalised
- * over J_b at temperature 1):
+ * over J_b at temperature 1), r the selection row of head h (b, or
+ * b*Hkv + g(h) with VP_SCOPE_KV_GROUP):
  *
  *   out[b, h] = sum_{j in J_b} softmax_{J_b}(Z_{h, j}) V_{g(h), j}      [B, Hq, d]
  *
@@ -230,8 +250,8 @@ vp_status vp_sparse_decode_attn(const vp_shape* shape, const vp_layout* layout, 
  * budget and top-k of every sequence run in one launch (a sequence's visual
  * ranks are scored in chunks on several work-groups, the last chunk to finish
  * selects). All outputs are written as by the four calls (same arithmetic,
- * same reduction order): mass_head [B, Hq], mass_seq [B, 2],
- * scores [B, max_vis], k [B], vis_idx [B, k_cap], out [B, Hq, d]; V is
+ * same reduction order): mass_head [B, Hq], mass_seq [B*R, 2],
+ * scores [B*R, max_vis], k [B*R], vis_idx [B*R, k_cap], out [B, Hq, d]; V is
  * required.
  *
  * events: optional caller-created hipEvent_t recorded on `stream`, i < n_events

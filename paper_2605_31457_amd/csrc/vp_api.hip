@@ -35,6 +35,9 @@ constexpr int kMaxBatch = 65535;
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
+// selection rows per sequence: one, or one per KV group
+int rows_per_seq(const vp_shape& s) { return s.scope == VP_SCOPE_KV_GROUP ? s.n_kv_heads : 1; }
+
 vp_status check_shape(const vp_shape* s) {
   if (!s) return fail(VP_ERR_NULL, "shape is NULL");
   if (s->dtype != VP_F32 && s->dtype != VP_BF16) return fail(VP_ERR_DTYPE, "dtype %d", s->dtype);
@@ -52,6 +55,12 @@ vp_status check_shape(const vp_shape* s) {
   if (s->k_cap < 1) return fail(VP_ERR_SHAPE, "k_cap %d < 1", s->k_cap);
   if (s->block_size < 0 || s->block_size > 65536 || (s->block_size & (s->block_size - 1)) != 0)
     return fail(VP_ERR_SHAPE, "block_size %d: 0 (contiguous) or a power of two <= 65536", s->block_size);
+  if (s->scope != VP_SCOPE_SEQUENCE && s->scope != VP_SCOPE_KV_GROUP)
+    return fail(VP_ERR_RANGE, "scope %d: VP_SCOPE_SEQUENCE or VP_SCOPE_KV_GROUP", s->scope);
+  if (s->reserved != 0) return fail(VP_ERR_RANGE, "reserved field %d must be 0", s->reserved);
+  if (static_cast<int64_t>(s->batch) * rows_per_seq(*s) > kMaxBatch)
+    return fail(VP_ERR_UNSUPPORTED, "batch x selection rows %lld > %d",
+                static_cast<long long>(s->batch) * rows_per_seq(*s), kMaxBatch);
   const int esz = s->dtype == VP_BF16 ? 2 : 4;
   const int64_t align_elems = 16 / esz;
   if (s->kv_stride_s < s->head_dim) return fail(VP_ERR_SHAPE, "kv_stride_s %lld < head_dim", (long long)s->kv_stride_s);
@@ -129,6 +138,7 @@ AttendArgs attend_args(const vp_shape* s, const vp_layout* l, const vp_params* p
   a.G = s->n_q_heads / s->n_kv_heads;
   a.max_seq_len = s->max_seq_len;
   a.max_vis = s->max_vis;
+  a.U = rows_per_seq(*s);
   a.zscale = zscale_of(s, p);
   a.inv_tau_m = 1.0f / p->tau_mass;
   a.inv_tau_s = 1.0f / p->tau_score;
@@ -176,6 +186,7 @@ MassArgs mass_args(const vp_shape* s, const vp_layout* l, const Plan& plan, cons
   m.nparts = plan.nparts;
   m.Hkv = s->n_kv_heads;
   m.G = s->n_q_heads / s->n_kv_heads;
+  m.U = rows_per_seq(*s);
   m.zs_rows = plan.zs_rows;
   m.zs_gp = plan.zs_gp;
   m.inv_tau_m = a.inv_tau_m;
@@ -195,6 +206,7 @@ BudgetArgs budget_args(const vp_shape* s, const vp_layout* l, const vp_params* p
   b.seg_off = l->vis_seg_off;
   b.seg = l->vis_seg;
   b.B = s->batch;
+  b.U = rows_per_seq(*s);
   b.max_seq_len = s->max_seq_len;
   b.r_lo_bp = p->r_lo_bp;
   b.r_hi_bp = p->r_hi_bp;
@@ -210,6 +222,7 @@ TopkArgs topk_args(const vp_shape* s, const vp_layout* l, const float* scores, c
   t.seg_off = l->vis_seg_off;
   t.seg = l->vis_seg;
   t.B = s->batch;
+  t.U = rows_per_seq(*s);
   t.max_seq_len = s->max_seq_len;
   t.max_vis = s->max_vis;
   t.k_cap = s->k_cap;
@@ -226,6 +239,7 @@ MergeArgs merge_args(const vp_shape* s, const vp_layout* l, const Plan& plan, co
   m.kk = k;
   m.B = s->batch;
   m.Hq = s->n_q_heads;
+  m.U = rows_per_seq(*s);
   m.max_seq_len = s->max_seq_len;
   m.k_cap = s->k_cap;
   m.nparts = plan.nparts;
@@ -298,16 +312,17 @@ Plan make_plan(const vp_shape& s) {
   off = align256(off + B * Hq * p.nsplit * 2 * 4);
   p.kacc = off;
   off = align256(off + B * Hq * p.nsplit * d * 4);
+  const size_t rows = B * static_cast<size_t>(rows_per_seq(s));
   p.sync = off;
-  off = align256(off + B * 4);
+  off = align256(off + rows * 4);
   p.segtab = off;
   off = align256(off + B * kSegTableBytes);
   p.total = off;
   // Select kernel: chunks of whole rounds (a round scores 1024 / lanes-per-token
   // visual ranks), enough rounds per chunk that the launch has about
   // VP_SELECT_WGS work-groups, so the spilled logits stream through many CUs.
-  const int64_t tpr = select_tokens_per_round(s.n_q_heads, s.n_kv_heads);
-  const int64_t want = static_cast<int64_t>(s.batch) * s.max_vis;
+  const int64_t tpr = select_tokens_per_round(s.n_kv_heads, rows_per_seq(s));
+  const int64_t want = static_cast<int64_t>(rows) * s.max_vis;
   int64_t rounds = (want + tpr * VP_SELECT_WGS - 1) / (tpr * VP_SELECT_WGS);
   if (rounds < 1) rounds = 1;
   const int64_t chunk = tpr * rounds;
@@ -444,6 +459,7 @@ vp_status vp_budget_top_p(const vp_shape* shape, const vp_layout* layout, const 
   t.seg_off = layout->vis_seg_off;
   t.seg = layout->vis_seg;
   t.B = shape->batch;
+  t.U = rows_per_seq(*shape);
   t.max_seq_len = shape->max_seq_len;
   t.max_vis = shape->max_vis;
   t.p = p;

@@ -550,12 +550,13 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
   s.kept = nullptr;
   if constexpr (P::KEPT) {
     if (s.L == 0) return;
-    int kb = a.kk[b];
+    const size_t row = static_cast<size_t>(b) * a.U + g / (a.Hkv / a.U);  // the KV head's selection row
+    int kb = a.kk[row];
     kb = kb < 0 ? 0 : (kb > a.k_cap ? a.k_cap : kb);
     s.r0 = part * a.split;
     s.r1 = min(s.r0 + a.split, kb);
     s.step = 32;
-    s.kept = a.vis_idx + static_cast<size_t>(b) * a.k_cap;
+    s.kept = a.vis_idx + row * a.k_cap;
   } else {
     s.r0 = 32 * part;
     s.r1 = s.L;
@@ -666,13 +667,14 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
   }
 }
 
-// The extra work-group of a launch with the visual role (x = its last index,
-// KV head 0): the sequence's clipped segment table (positions and visual
-// ranks) for the select kernel, and a new step's arrival counter at zero.
+// The extra work-group of a launch with the visual role (x = its last index):
+// for KV head g < U, a new step's arrival counter of selection row (b, g) at
+// zero; for KV head 0, also the sequence's clipped segment table (positions and
+// visual ranks) for the select kernel.
 __device__ __forceinline__ void step_setup(const AttendArgs& a, int g, int b) {
-  if (g != 0) return;
   const int lane = threadIdx.x;
-  if (a.sync && lane == 0) a.sync[b] = 0u;
+  if (a.sync && lane == 0 && g < a.U) a.sync[b * a.U + g] = 0u;
+  if (g != 0) return;
   if (a.segtab) {
     const int L = clamp_len(a.seq_len[b], a.max_seq_len);
     const int o0 = a.seg_off[b];

@@ -47,19 +47,20 @@ __device__ __forceinline__ int lanes_per_head(int Hq, int nparts) {
 }
 
 // Merges the per-part statistics of sequence b (visual and text rows, kept
-// apart by the context pass) for every head onto the head's maximum, in
+// apart by the context pass) for every head of selection row u of the
+// sequence (heads [u Hq/U, (u+1) Hq/U)) onto the head's maximum, in
 // double with fixed-order reductions, by a kSelThreads block (every thread
 // calls it; two block barriers). Every head gets a group of lanes (a power of
-// two, lanes_per_head; one round of heads since Hq <= kSelThreads) that
+// two, lanes_per_head of the row's head count; one round of heads since Hq <= kSelThreads) that
 // strides over the parts and reduces on the DPP network. When the part capacity allows, each lane's (up to four) parts are
 // requested at entry at addresses that do not depend on the sequence length,
 // `between()` runs while they are in flight (the caller's other independent
 // loads), and the maximum and the sums then come from registers; more parts
 // take two sweeps with the same arithmetic order. The head mean and head max
-// are summed by one wave in a fixed order.
-// L is the sequence's clamped length. Fills `hs`; with `write_out` also writes
-// m^vis_{t,h} (mass_head), the per-head (max, Eq. (2) normaliser) (head) and
-// (M_vis, M_vis,max) (mass_seq).
+// over the row's heads are summed by one wave in a fixed order.
+// L is the sequence's clamped length. Fills `hs` for the row's heads; with
+// `write_out` also writes their m^vis_{t,h} (mass_head), per-head (max, Eq. (2)
+// normaliser) (head) and the row's (M_vis, M_vis,max) (mass_seq).
 namespace detail {
 constexpr int kPartsPerLane = 4;
 // parts c0, c0 + step, ... of one head (slots past `cap` read as empty parts)
@@ -110,17 +111,18 @@ __device__ __forceinline__ void sum_parts(double& Ls, double& Lm, double& Vm, co
 }  // namespace detail
 
 template <typename Between>
-__device__ __forceinline__ void reduce_heads(const MassArgs& a, int b, int L, int tid, const HeadLds& hs,
+__device__ __forceinline__ void reduce_heads(const MassArgs& a, int b, int u, int L, int tid, const HeadLds& hs,
                                              bool write_out, Between between) {
   using namespace detail;
-  const int lph = lanes_per_head(a.Hq, a.nparts);
+  const int Hu = a.Hq / a.U;  // heads of the row
+  const int h0 = u * Hu;
+  const int lph = lanes_per_head(Hu, a.nparts);
   const int sub = tid % lph;
-  const int h = tid / lph;
-  const bool on = h < a.Hq;
+  const bool on = tid / lph < Hu;
+  const int h = h0 + (on ? tid / lph : 0);
   constexpr int U = kPartsPerLane;
   // per part: [0] visual {m, Ls, Lm, -}, [1] text {m, l, Lm, Ls}
-  const float4* st =
-      reinterpret_cast<const float4*>(a.stats + (static_cast<size_t>(b) * a.Hq + (on ? h : 0)) * a.nparts * 8);
+  const float4* st = reinterpret_cast<const float4*>(a.stats + (static_cast<size_t>(b) * a.Hq + h) * a.nparts * 8);
   const bool one_round = a.nparts <= U * lph;
   float4 v[U], t[U];
   if (one_round) load_parts(v, t, st, on, sub, lph, a.nparts);
@@ -158,23 +160,25 @@ __device__ __forceinline__ void reduce_heads(const MassArgs& a, int b, int L, in
     }
   }
   __syncthreads();
-  // head mean and head max: lane j takes heads j, j + 64, ... in order, then a fixed butterfly
+  // head mean and head max of the row: lane j takes heads h0 + j, h0 + j + 64,
+  // ... in order, then a fixed butterfly
   if (tid < 64) {
     double msum = 0.0, mmax = 0.0;
-    for (int hh = tid; hh < a.Hq; hh += 64) {
+    for (int hh = h0 + tid; hh < h0 + Hu; hh += 64) {
       msum += hs.mass[hh];
       mmax = hs.mass[hh] > mmax ? hs.mass[hh] : mmax;
     }
     msum = group_sum_f64(msum, 64);
     mmax = group_max_f64(mmax, 64);
     if (tid == 0) {
-      const float mv = static_cast<float>(msum / a.Hq);
+      const float mv = static_cast<float>(msum / Hu);
       const float mx = static_cast<float>(mmax);
       hs.mseq[0] = mv;
       hs.mseq[1] = mx;
       if (write_out) {
-        a.mass_seq[2 * b + 0] = mv;
-        a.mass_seq[2 * b + 1] = mx;
+        const size_t row = static_cast<size_t>(b) * a.U + u;
+        a.mass_seq[2 * row + 0] = mv;
+        a.mass_seq[2 * row + 1] = mx;
       }
     }
   }
@@ -189,9 +193,11 @@ __device__ __forceinline__ float score_term(float s, float z, float hm, float hi
 }
 
 // Summation order of the Eq. (2) head sum, shared by every kernel that scores:
-// lane slot l of ng = min(64, Hkv rounded up to a power of two) sums, in order,
-// the KV groups g = l, l + ng, ..., each group's G heads in head order, from
-// zero; the lane sums are then added in lane order and the total divided by Hq.
+// over the Gu = Hkv/U KV groups g0 .. g0 + Gu - 1 of a selection row, lane slot l
+// of ng = min(64, Gu rounded up to a power of two) sums, in order, the KV groups
+// g0 + l, g0 + l + ng, ..., each group's G heads in head order, from zero; the
+// lane sums are then added in lane order and the total divided by the row's
+// head count Hq/U.
 __host__ __device__ inline int score_lanes(int Hkv) {
   int ng = 1;
   while (ng < 64 && ng < Hkv) ng <<= 1;
@@ -219,27 +225,31 @@ __device__ __forceinline__ float group_terms(float p, const float* row, int G, c
 }
 
 // ---------------------------------------------------------------------------
-// Eq. (2) score of the visual token at cache position pos of sequence b by one
-// thread (the same order as the select kernel's lanes):
-// S = (1/Hq) sum_h 2^((z_h - m_h) / tau_score) / Ls_h from the spilled logits.
-// hm/hinv: per-head max and 1/Ls.
+// Eq. (2) score of the visual token at cache position pos of sequence b for
+// selection row u, by one thread (the same order as the select kernel's lanes):
+// S = (1/Hu) sum_h 2^((z_h - m_h) / tau_score) / Ls_h over the row's heads,
+// from the spilled logits. hm/hinv: per-head max and 1/Ls (by head index).
 // ---------------------------------------------------------------------------
 template <int GP>
-__device__ __forceinline__ float token_score_gp(const MassArgs& a, int b, int pos, const float* hm, const float* hinv) {
+__device__ __forceinline__ float token_score_gp(const MassArgs& a, int b, int u, int pos, const float* hm,
+                                                const float* hinv) {
   const float* zb = a.zs + static_cast<size_t>(b) * a.Hkv * a.zs_rows * GP + static_cast<size_t>(pos) * GP;
-  const int ng = score_lanes(a.Hkv);
+  const int Gu = a.Hkv / a.U;
+  const int g0 = u * Gu;
+  const int ng = score_lanes(Gu);
   float total = 0.f;
   for (int l = 0; l < ng; ++l) {
     float p = 0.f;
-    for (int g = l; g < a.Hkv; g += ng)
+    for (int g = g0 + l; g < g0 + Gu; g += ng)
       p = group_terms<GP>(p, zb + static_cast<size_t>(g) * a.zs_rows * GP, a.G, hm + g * a.G, hinv + g * a.G,
                           a.inv_tau_s);
     total = l == 0 ? p : total + p;
   }
-  return total / static_cast<float>(a.Hq);
+  return total / static_cast<float>(a.Hq / a.U);
 }
-__device__ __forceinline__ float token_score(const MassArgs& a, int b, int pos, const float* hm, const float* hinv) {
-  return a.zs_gp == 8 ? token_score_gp<8>(a, b, pos, hm, hinv) : token_score_gp<16>(a, b, pos, hm, hinv);
+__device__ __forceinline__ float token_score(const MassArgs& a, int b, int u, int pos, const float* hm,
+                                             const float* hinv) {
+  return a.zs_gp == 8 ? token_score_gp<8>(a, b, u, pos, hm, hinv) : token_score_gp<16>(a, b, u, pos, hm, hinv);
 }
 
 // ---------------------------------------------------------------------------

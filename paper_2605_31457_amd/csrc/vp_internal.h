@@ -29,10 +29,10 @@ struct Plan {
   size_t head;    // float [B][Hq][2]           merged (max, score normaliser)
   size_t kstats;  // float [B][Hq][nsplit][2]   kept-row (max, sum)
   size_t kacc;    // float [B][Hq][nsplit][d]   kept-row value partials
-  size_t sync;    // uint32 [B]                 select-kernel arrival counters
+  size_t sync;    // uint32 [B][U]              select-kernel arrival counters (per selection row)
   size_t segtab;  // SegTable [B]               clipped segment tables (positions, ranks)
   int sel_chunk;  // visual ranks scored per select work-group
-  int sel_chunks; // select work-groups per sequence
+  int sel_chunks; // select work-groups per selection row
   size_t total;
 };
 
@@ -63,6 +63,7 @@ struct AttendArgs {
   const int32_t* seg_off;
   const int32_t* seg;
   int B, Hq, Hkv, G, max_seq_len, max_vis;
+  int U;                // selection rows per sequence: 1, or Hkv (one per KV group)
   float zscale;         // sm_scale * log2(e)
   float inv_tau_m;      // 1 / tau_mass
   float inv_tau_s;      // 1 / tau_score
@@ -79,7 +80,7 @@ struct AttendArgs {
   int k_cap, split, nsplit;
   float* kstats;
   float* kacc;
-  uint32_t* sync;       // [B] arrival counters of the select kernel (may be null)
+  uint32_t* sync;       // [B][U] arrival counters of the select kernel (may be null)
   void* segtab;         // [B] segment tables (SegTable) for the select kernel (may be null)
 };
 
@@ -96,6 +97,8 @@ struct MassArgs {
   const int32_t* seg_off;
   const int32_t* seg;
   int B, Hq, Hkv, G, max_seq_len, max_vis, nparts, zs_rows, zs_gp;
+  int U;  // selection rows per sequence (1 or Hkv); row b*U + u covers query heads
+          // [u Hq/U, (u+1) Hq/U) and KV groups [u Hkv/U, (u+1) Hkv/U)
   float inv_tau_m, inv_tau_s;
   const float* stats;
   const float* zs;
@@ -109,7 +112,7 @@ hipError_t launch_mass_finalize(const MassArgs& a, hipStream_t st);
 hipError_t launch_scores(const MassArgs& a, hipStream_t st);
 
 // Everything between the context pass and the kept-row pass of a decode step
-// (mass reduction, scores, budget, top-k) in one launch: grid (nchunks, B).
+// (mass reduction, scores, budget, top-k) in one launch: grid (nchunks, B*U).
 constexpr int kMaxSelectHeads = 1024;
 struct SelectArgs {
   MassArgs m;
@@ -118,21 +121,21 @@ struct SelectArgs {
   int32_t* k;
   int32_t* vis_idx;
   int chunk;       // visual ranks scored per work-group
-  int nchunks;     // work-groups per sequence
-  uint32_t* sync;  // [B] arrival counters (nchunks > 1), zeroed by the context pass
+  int nchunks;     // work-groups per selection row
+  uint32_t* sync;  // [B*U] arrival counters (nchunks > 1), zeroed by the context pass
   const void* segtab;  // [B] segment tables written by the context pass
 };
 
 // visual ranks one select work-group scores per round (1024 lanes over the
 // lanes per token of the score order)
-int select_tokens_per_round(int n_q_heads, int n_kv_heads);
+int select_tokens_per_round(int n_kv_heads, int rows_per_seq);
 hipError_t launch_select(const SelectArgs& t, hipStream_t st);
 
 struct BudgetArgs {
   const int32_t* seq_len;
   const int32_t* seg_off;
   const int32_t* seg;
-  int B, max_seq_len;
+  int B, U, max_seq_len;
   int r_lo_bp, r_hi_bp, clamp;
   const float* mass_seq;
   int32_t* k;
@@ -144,7 +147,7 @@ struct TopkArgs {
   const int32_t* seq_len;
   const int32_t* seg_off;
   const int32_t* seg;
-  int B, max_seq_len, max_vis, k_cap;
+  int B, U, max_seq_len, max_vis, k_cap;
   const float* scores;
   const int32_t* k;
   int32_t* vis_idx;
@@ -161,7 +164,7 @@ struct TopPArgs {
   const int32_t* seq_len;
   const int32_t* seg_off;
   const int32_t* seg;
-  int B, max_seq_len, max_vis;
+  int B, U, max_seq_len, max_vis;
   float p;
   const float* scores;
   int32_t* k;
@@ -172,7 +175,7 @@ hipError_t launch_top_p(const TopPArgs& a, hipStream_t st);
 struct MergeArgs {
   const int32_t* seq_len;
   const int32_t* kk;
-  int B, Hq, max_seq_len, k_cap, nparts, split, nsplit, dtype;
+  int B, Hq, U, max_seq_len, k_cap, nparts, split, nsplit, dtype;
   const float* stats;
   const float* acc;
   const float* kstats;

@@ -30,7 +30,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a)
   const int r = tid / COLS;
   const int L = clamp_len(a.seq_len[b], a.max_seq_len);
   const int nc = parts_used(L, a.nparts);
-  int kb = a.kk[b];
+  int kb = a.kk[static_cast<size_t>(b) * a.U + h / (a.Hq / a.U)];  // the head's selection row
   kb = kb < 0 ? 0 : (kb > a.k_cap ? a.k_cap : kb);
   const int ns = L > 0 ? (kb + a.split - 1) / a.split : 0;
   const int np = nc + ns;

@@ -3,15 +3,16 @@
 // head max (Sec. 4.3), the Eq. (2) score of every visual token (Sec. 4.2), the
 // Eq. (7) budget with the Sec. 5.2 clamp and the Eq. (3) top-k.
 //
-// grid = (chunks, B), 1024 threads per work-group. Work-group c of sequence b
-// reduces the sequence's per-part statistics (every work-group of the sequence
-// does, so none waits for another), scores the visual ranks
-// [c * chunk, (c + 1) * chunk) from the spilled logits and writes them. With
-// one chunk per sequence the keys stay in LDS and the same work-group selects;
-// with several, each work-group publishes its scores (device-scope release)
-// and counts itself in on the sequence's arrival counter (zeroed by the
+// grid = (chunks, B*U), 1024 threads per work-group, one row of work-groups per
+// selection row (b, u): the sequence (U = 1), or one KV group of it (U = Hkv).
+// Work-group c of row (b, u) reduces the per-part statistics of the row's heads
+// (every work-group of the row does, so none waits for another), scores the
+// visual ranks [c * chunk, (c + 1) * chunk) from the spilled logits and writes
+// them. With one chunk per row the keys stay in LDS and the same work-group
+// selects; with several, each work-group publishes its scores (device-scope
+// release) and counts itself in on the row's arrival counter (zeroed by the
 // context pass of the same step); the last to arrive reads every score of the
-// sequence back and selects. No work-group ever waits for another.
+// row back and selects. No work-group ever waits for another.
 //
 // Latency: the statistics and the segment table (built by the context pass)
 // are requested at once at entry; the spilled logits of a thread's tokens (all heads) are one
@@ -34,7 +35,9 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
 
   const MassArgs& a = t.m;
   const int c = blockIdx.x;
-  const int b = blockIdx.y;
+  const int row = blockIdx.y;
+  const int b = row / a.U;
+  const int u = row % a.U;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wid = tid >> 6;
@@ -46,7 +49,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
 
   // ---- per-head statistics; wave 0 builds the segment table while the
   // statistics are in flight (the reduction's barriers publish it) ----
-  reduce_heads(a, b, L, tid, hs, c == 0, [&] {
+  reduce_heads(a, b, u, L, tid, hs, c == 0, [&] {
     if (wid == 0) {
       // the context pass left the clipped table in the workspace: one round of loads
       const uint4* src = reinterpret_cast<const uint4*>(static_cast<const SegTable*>(t.segtab) + b);
@@ -64,12 +67,14 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
   const int n = min(nvis, a.max_vis);
   const bool single = t.nchunks == 1;
   const bool in_lds = n <= lds_keys;
-  float* sc = a.scores + static_cast<size_t>(b) * a.max_vis;
+  float* sc = a.scores + static_cast<size_t>(row) * a.max_vis;
 
   // ---- Eq. (2) scores of this chunk's visual ranks: ng lanes per token, lane
-  // l takes the KV groups l, l + ng, ... (a 16-byte-aligned spill row each),
-  // the lane sums are added in lane order ----
-  const int ng = score_lanes(a.Hkv);
+  // l takes the row's KV groups g0 + l, g0 + l + ng, ... (a 16-byte-aligned
+  // spill row each), the lane sums are added in lane order ----
+  const int Gu = a.Hkv / a.U;
+  const int g0 = u * Gu;
+  const int ng = score_lanes(Gu);
   const int l = tid & (ng - 1);
   const int tpw = kSelThreads / ng;  // tokens per round
   const int r0 = min(n, c * t.chunk);
@@ -81,13 +86,13 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
     const bool ok = i < r1;
     const int pos = ok ? rank_to_pos(tab, i) : 0;
     float p = 0.f;
-    for (int g = l; g < a.Hkv; g += ng)
+    for (int g = g0 + l; g < g0 + Gu; g += ng)
       p = group_terms<GP>(p, zb + (static_cast<size_t>(g) * a.zs_rows + pos) * GP, a.G, hs.hm + g * a.G,
                           hs.hinv + g * a.G, a.inv_tau_s);
     float total = p;
     for (int j = 1; j < ng; ++j) total = total + __shfl(p, (lane & ~(ng - 1)) + j);
     if (ok && l == 0) {
-      const float S = total / static_cast<float>(a.Hq);
+      const float S = total / static_cast<float>(a.Hq / a.U);
       sc[i] = S;
       const uint32_t u = order_key(S);
       if (single && in_lds) s_keys[i] = u;
@@ -98,12 +103,12 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
 
   if (!single) {
     // publish this chunk's scores and count in; the last work-group of the
-    // sequence selects. The barrier orders the block's stores before thread 0's
+    // row selects. The barrier orders the block's stores before thread 0's
     // device-scope release; the last arrival alone takes the acquire, which makes
     // the other work-groups' scores visible to the block after the second barrier.
     __syncthreads();
     if (tid == 0) {
-      const bool last = __hip_atomic_fetch_add(t.sync + b, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT) ==
+      const bool last = __hip_atomic_fetch_add(t.sync + row, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT) ==
                         static_cast<unsigned>(t.nchunks - 1);
       if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
       s_last = last;
@@ -132,10 +137,10 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
 
   // ---- Eq. (7) budget, then Eq. (3) selection ----
   const int kb = budget_rule(static_cast<double>(hs.mseq[1]), nvis, t.r_lo_bp, t.r_hi_bp, t.clamp);
-  if (tid == 0) t.k[b] = kb;
+  if (tid == 0) t.k[row] = kb;
   int k = kb > n ? n : kb;
   k = k > t.k_cap ? t.k_cap : k;
-  int32_t* out = t.vis_idx + static_cast<size_t>(b) * t.k_cap;
+  int32_t* out = t.vis_idx + static_cast<size_t>(row) * t.k_cap;
   for (int i = k + tid; i < t.k_cap; i += kSelThreads) out[i] = -1;
   if (k == 0) return;
   auto key_at = [&](int i) -> uint32_t { return in_lds ? s_keys[i] : order_key(sc[i]); };
@@ -174,13 +179,15 @@ hipError_t launch_gp(const SelectArgs& t, hipStream_t st) {
   // one chunk keeps its keys in LDS: the launch plan guarantees they fit
   if (t.nchunks == 1 && keys < t.m.max_vis) return hipErrorInvalidValue;
   const size_t dyn = static_cast<size_t>(head_lds_bytes(t.m.Hq)) + static_cast<size_t>(keys) * 4;
-  hipLaunchKernelGGL((select_kernel<GP>), dim3(t.nchunks, t.m.B), dim3(kSelThreads), dyn, st, t, keys);
+  hipLaunchKernelGGL((select_kernel<GP>), dim3(t.nchunks, t.m.B * t.m.U), dim3(kSelThreads), dyn, st, t, keys);
   return hipGetLastError();
 }
 
 }  // namespace
 
-int select_tokens_per_round(int n_q_heads, int n_kv_heads) { return kSelThreads / score_lanes(n_kv_heads); }
+int select_tokens_per_round(int n_kv_heads, int rows_per_seq) {
+  return kSelThreads / score_lanes(n_kv_heads / rows_per_seq);
+}
 
 hipError_t launch_select(const SelectArgs& t, hipStream_t st) {
   if (t.m.Hq > kMaxSelectHeads || t.nchunks < 1 || t.chunk < 1) return hipErrorInvalidValue;

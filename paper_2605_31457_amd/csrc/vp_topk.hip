@@ -29,7 +29,8 @@ __global__ __launch_bounds__(kSelThreads) void topk_kernel(const TopkArgs a, int
   __shared__ SelectShared sh;
   __shared__ SegTable tab;
 
-  const int b = blockIdx.x;
+  const int row = blockIdx.x;  // selection row of sequence b
+  const int b = row / a.U;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wid = tid >> 6;
@@ -40,18 +41,18 @@ __global__ __launch_bounds__(kSelThreads) void topk_kernel(const TopkArgs a, int
   const int n = min(tab.rk[tab.n], a.max_vis);
   int k;
   if (a.mass_seq) {
-    k = budget_rule(static_cast<double>(a.mass_seq[2 * b + 1]), tab.rk[tab.n], a.r_lo_bp, a.r_hi_bp, a.clamp);
-    if (tid == 0) a.k_out[b] = k;
+    k = budget_rule(static_cast<double>(a.mass_seq[2 * row + 1]), tab.rk[tab.n], a.r_lo_bp, a.r_hi_bp, a.clamp);
+    if (tid == 0) a.k_out[row] = k;
   } else {
-    k = a.k[b];
+    k = a.k[row];
   }
   k = k < 0 ? 0 : k;
   k = k > n ? n : k;
   k = k > a.k_cap ? a.k_cap : k;
-  int32_t* out = a.vis_idx + static_cast<size_t>(b) * a.k_cap;
+  int32_t* out = a.vis_idx + static_cast<size_t>(row) * a.k_cap;
   for (int i = k + tid; i < a.k_cap; i += kSelThreads) out[i] = -1;
   if (k == 0) return;
-  const float* sc = a.scores + static_cast<size_t>(b) * a.max_vis;
+  const float* sc = a.scores + static_cast<size_t>(row) * a.max_vis;
   const bool in_lds = n <= lds_keys;
   const bool take_all = k >= n;
   auto key_at = [&](int i) -> uint32_t { return in_lds ? s_keys[i] : order_key(sc[i]); };
@@ -123,7 +124,8 @@ __global__ __launch_bounds__(kSelThreads) void top_p_kernel(const TopPArgs a, in
   __shared__ unsigned long long s_above_m;
   __shared__ int s_above_c;
 
-  const int b = blockIdx.x;
+  const int row = blockIdx.x;  // selection row of sequence b
+  const int b = row / a.U;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wid = tid >> 6;
@@ -133,10 +135,10 @@ __global__ __launch_bounds__(kSelThreads) void top_p_kernel(const TopPArgs a, in
   __syncthreads();
   const int n = min(tab.rk[tab.n], a.max_vis);
   if (!(a.p > 0.f) || n == 0) {
-    if (tid == 0) a.k[b] = 0;
+    if (tid == 0) a.k[row] = 0;
     return;
   }
-  const float* sc = a.scores + static_cast<size_t>(b) * a.max_vis;
+  const float* sc = a.scores + static_cast<size_t>(row) * a.max_vis;
   const bool in_lds = n <= lds_keys;
   auto key_at = [&](int i) -> uint32_t { return in_lds ? s_keys[i] : order_key(sc[i]); };
   // target in fixed point, rounded up: sum >= p  <=>  fixed sum >= ceil(p 2^40)
@@ -187,7 +189,7 @@ __global__ __launch_bounds__(kSelThreads) void top_p_kernel(const TopPArgs a, in
     tot += s_wm[v];
   }
   if (tot < target) {  // every visual token together stays below p
-    if (tid == 0) a.k[b] = n;
+    if (tid == 0) a.k[row] = n;
     return;
   }
 
@@ -269,7 +271,7 @@ __global__ __launch_bounds__(kSelThreads) void top_p_kernel(const TopPArgs a, in
   if (tid == 0) {
     const uint64_t m = fixed_mass(lo);
     const uint64_t j = m > 0 ? (need + m - 1) / m : 0;
-    a.k[b] = min(n, above + static_cast<int>(j));
+    a.k[row] = min(n, above + static_cast<int>(j));
   }
 }
 
@@ -288,7 +290,7 @@ hipError_t launch_top_p(const TopPArgs& a, hipStream_t st) {
     return max(0, max_lds - stat - 64);
   }();
   const int keys = min(lds_room / 4, a.max_vis);
-  hipLaunchKernelGGL(top_p_kernel, dim3(a.B), dim3(kSelThreads), static_cast<size_t>(keys) * 4, st, a, keys);
+  hipLaunchKernelGGL(top_p_kernel, dim3(a.B * a.U), dim3(kSelThreads), static_cast<size_t>(keys) * 4, st, a, keys);
   return hipGetLastError();
 }
 
@@ -307,7 +309,7 @@ hipError_t launch_topk(const TopkArgs& a, hipStream_t st) {
     return max(0, max_lds - stat - 64);
   }();
   const int keys = min(lds_room / 4, a.max_vis);
-  hipLaunchKernelGGL(topk_kernel, dim3(a.B), dim3(kSelThreads), static_cast<size_t>(keys) * 4, st, a, keys);
+  hipLaunchKernelGGL(topk_kernel, dim3(a.B * a.U), dim3(kSelThreads), static_cast<size_t>(keys) * 4, st, a, keys);
   return hipGetLastError();
 }
 

@@ -48,11 +48,17 @@ def paged_cache(K: np.ndarray, V: np.ndarray, block_size: int, seed: int = 0):
 
 
 class DeviceStep:
-    """Device-resident inputs, outputs and workspace of one step of workload ``w``."""
+    """Device-resident inputs, outputs and workspace of one step of workload ``w``.
+
+    ``kv_groups``: one budget and kept set per KV group (VP_SCOPE_KV_GROUP);
+    results() then returns mass_seq [B, Hkv, 2], scores [B, Hkv, max_vis],
+    k [B, Hkv] and vis_idx [B, Hkv, k_cap].
+    """
 
     def __init__(self, w: Workload, device="cuda:0", k_cap: int | None = None, max_vis: int | None = None,
-                 kv=None, block_size: int = 0, block_seed: int = 0):
+                 kv=None, block_size: int = 0, block_seed: int = 0, kv_groups: bool = False):
         self.w = w
+        self.rows = w.Hkv if kv_groups else 1
         self.device = torch.device(device)
         self.q = _dev(w.q, self.device)
         self.block_size = block_size
@@ -82,18 +88,20 @@ class DeviceStep:
         self.shape = vp.vp_shape(batch=B, n_q_heads=Hq, n_kv_heads=w.Hkv, head_dim=d,
                                  dtype=vp.VP_BF16 if w.dtype == "bf16" else vp.VP_F32,
                                  max_seq_len=w.S_cap, max_vis=self.max_vis, max_segs=w.max_segs,
-                                 k_cap=self.k_cap, block_size=block_size, kv_stride_b=st[0], kv_stride_h=st[1],
-                                 kv_stride_s=st[2])
+                                 k_cap=self.k_cap, block_size=block_size,
+                                 scope=vp.VP_SCOPE_KV_GROUP if kv_groups else vp.VP_SCOPE_SEQUENCE,
+                                 kv_stride_b=st[0], kv_stride_h=st[1], kv_stride_s=st[2])
         self.layout = vp.vp_layout(seq_len=self.seq_len.data_ptr(), vis_seg_off=self.seg_off.data_ptr(),
                                    vis_seg=self.seg.data_ptr(),
                                    block_table=self.block_table.data_ptr() if block_size else None)
         f32 = dict(dtype=torch.float32, device=self.device)
         i32 = dict(dtype=torch.int32, device=self.device)
         self.mass_head = torch.zeros(B, Hq, **f32)
-        self.mass_seq = torch.zeros(B, 2, **f32)
-        self.scores = torch.zeros(B, self.max_vis, **f32)
-        self.k = torch.zeros(B, **i32)
-        self.vis_idx = torch.full((B, self.k_cap), -7, **i32)
+        R = B * self.rows  # selection rows
+        self.mass_seq = torch.zeros(R, 2, **f32)
+        self.scores = torch.zeros(R, self.max_vis, **f32)
+        self.k = torch.zeros(R, **i32)
+        self.vis_idx = torch.full((R, self.k_cap), -7, **i32)
         self.out = torch.zeros(B, Hq, d, dtype=self.q.dtype, device=self.device)
         self.ws_bytes = vp.vp_workspace_size(self.shape)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
@@ -128,6 +136,7 @@ class DeviceStep:
     def results(self) -> dict:
         torch.cuda.synchronize(self.device)
         out = self.out.float().cpu().numpy()
-        return dict(mass_head=self.mass_head.cpu().numpy(), mass_seq=self.mass_seq.cpu().numpy(),
-                    scores=self.scores.cpu().numpy(), k=self.k.cpu().numpy(),
-                    vis_idx=self.vis_idx.cpu().numpy(), out=out)
+        lead = (self.w.B, self.rows) if self.rows > 1 else (self.w.B,)
+        rows = lambda t: t.cpu().numpy().reshape(lead + tuple(t.shape[1:]))
+        return dict(mass_head=self.mass_head.cpu().numpy(), mass_seq=rows(self.mass_seq),
+                    scores=rows(self.scores), k=rows(self.k), vis_idx=rows(self.vis_idx), out=out)

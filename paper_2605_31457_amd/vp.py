@@ -16,6 +16,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.environ.get("VP_LIB") or os.path.join(PKG, "libvisionpulse.so")
 
 VP_F32, VP_BF16 = 0, 1
+VP_SCOPE_SEQUENCE, VP_SCOPE_KV_GROUP = 0, 1
 VP_ATTN_TEXT_FROM_WORKSPACE = 1
 STATUS = ["VP_OK", "VP_ERR_NULL", "VP_ERR_SHAPE", "VP_ERR_RANGE", "VP_ERR_DTYPE",
           "VP_ERR_UNSUPPORTED", "VP_ERR_WORKSPACE", "VP_ERR_HIP"]
@@ -31,7 +32,8 @@ class vp_shape(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32), ("max_seq_len", ctypes.c_int32),
                 ("max_vis", ctypes.c_int32), ("max_segs", ctypes.c_int32), ("k_cap", ctypes.c_int32),
-                ("block_size", ctypes.c_int32), ("kv_stride_b", ctypes.c_int64), ("kv_stride_h", ctypes.c_int64),
+                ("block_size", ctypes.c_int32), ("scope", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("kv_stride_b", ctypes.c_int64), ("kv_stride_h", ctypes.c_int64),
                 ("kv_stride_s", ctypes.c_int64)]
 
 

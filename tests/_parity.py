@@ -67,3 +67,24 @@ def small_workload(seed, B, Hq, Hkv, d, lens, segs, dtype="bf16", S_cap=None, sp
     return W.Workload(name=f"small-{seed}", dtype=dtype, B=B, Hq=Hq, Hkv=Hkv, d=d, S_cap=S_cap,
                       seq_len=np.array(lens, np.int32), segments=[list(s) for s in segs], q=q, K=K, V=V,
                       tau_mass=tau_mass, r_lo_bp=r_lo_bp, r_hi_bp=r_hi_bp, clamp=clamp)
+
+
+def check_groups(tag, w, gpu, b, r: O.GroupedResult):
+    """Compare GPU outputs of sequence b (per-KV-group selection rows) with the
+    reference result r of the per-KV-group variant."""
+    ctx = f"{tag} seq {b}"
+    np.testing.assert_allclose(gpu["mass_head"][b], r.mass_head, rtol=MASS_RTOL, atol=MASS_ATOL,
+                               err_msg=f"{ctx}: mass_head")
+    np.testing.assert_allclose(gpu["mass_seq"][b], np.stack([r.M_vis, r.M_vis_max], axis=1), rtol=MASS_RTOL,
+                               atol=MASS_ATOL, err_msg=f"{ctx}: group M_vis / M_vis_max")
+    nv = r.scores.shape[1]
+    np.testing.assert_allclose(gpu["scores"][b, :, :nv], r.scores, rtol=MASS_RTOL, atol=MASS_ATOL,
+                               err_msg=f"{ctx}: group scores")
+    assert np.array_equal(gpu["k"][b], r.k), f"{ctx}: k {gpu['k'][b]} != {r.k}"
+    for g in range(w.Hkv):
+        idx = gpu["vis_idx"][b, g]
+        k = int(r.k[g])
+        assert np.array_equal(idx[:k], r.vis_idx[g]), f"{ctx} group {g}: kept index set differs"
+        assert np.all(idx[k:] == -1), f"{ctx} group {g}: padding"
+    atol, rtol = OUT_TOL[w.dtype]
+    np.testing.assert_allclose(gpu["out"][b], r.out, atol=atol, rtol=rtol, err_msg=f"{ctx}: out")

@@ -50,9 +50,10 @@ def _params(**kw):
 
 
 def test_struct_layout_matches_header(L):
-    assert ctypes.sizeof(vp.vp_shape) == 64 and vp.vp_shape.kv_stride_b.offset == 40
+    assert ctypes.sizeof(vp.vp_shape) == 72 and vp.vp_shape.kv_stride_b.offset == 48
     assert ctypes.sizeof(vp.vp_params) == 24 and ctypes.sizeof(vp.vp_layout) == 32
     assert vp.vp_shape.block_size.offset == 36 and vp.vp_layout.block_table.offset == 24
+    assert vp.vp_shape.scope.offset == 40 and vp.vp_shape.reserved.offset == 44
 
 
 def test_workspace_size_is_pure_and_scales(L):
@@ -77,11 +78,23 @@ def test_workspace_size_is_pure_and_scales(L):
     (dict(block_size=-16), "VP_ERR_SHAPE"),
     (dict(block_size=1 << 17), "VP_ERR_SHAPE"),
     (dict(max_segs=1000), "VP_ERR_UNSUPPORTED"),
+    (dict(scope=2), "VP_ERR_RANGE"),
+    (dict(scope=-1), "VP_ERR_RANGE"),
+    (dict(reserved=1), "VP_ERR_RANGE"),
+    (dict(scope=1, batch=20000), "VP_ERR_UNSUPPORTED"),  # 80000 selection rows
 ])
 def test_shape_validation(L, kw, status):
     with pytest.raises(vp.VPError) as e:
         vp.vp_workspace_size(_shape(**kw))
     assert status in str(e.value)
+
+
+def test_kv_group_scope_sizes_the_arrival_counters(L):
+    """One arrival counter per selection row: the workspace grows by at most a
+    few 256-byte pieces, never by a per-token amount."""
+    a = vp.vp_workspace_size(_shape(batch=64))
+    b = vp.vp_workspace_size(_shape(batch=64, scope=vp.VP_SCOPE_KV_GROUP))
+    assert a <= b <= a + 1024
 
 
 def _layout():
