@@ -159,6 +159,43 @@ def plant_kv_groups(w, params: O.OracleParams, seqs=None):
     return res, log
 
 
+def plant_queries(w, params: O.OracleParams, seqs=None, kv_groups=False, rounds=4):
+    """plant() for T queries per sequence (w.q: [B, T, Hq, d]): each query is
+    planted as the step it is (its visible prefix, visual segments cut at
+    L - T + 1), in rounds until every query of the sequence holds its margin
+    and gap at once (an edit for one query moves the others' scores too).
+    Returns {b: [T results]}, {b: True when every query holds}."""
+    res, ok = {}, {}
+    T = w.q.shape[1]
+    G = w.Hq // w.Hkv
+    for b in (range(w.B) if seqs is None else seqs):
+        L = int(w.seq_len[b])
+        L0 = L - T + 1
+        segs = O.clip_segments(w.segments[b], max(L0, 0))
+        vis = O.visual_positions(max(L0, 0), segs)
+        good = False
+        for _ in range(rounds):
+            good = True
+            for t in range(T):
+                n = max(L0 + t, 0)
+                units = ([(w.q[b, t], w.K[b], w.V[b])] if not kv_groups else
+                         [(w.q[b, t, g * G:(g + 1) * G], w.K[b, g:g + 1], w.V[b, g:g + 1]) for g in range(w.Hkv)])
+                for (qq, KK, VV) in units:
+                    r = O.decode_step_sequence(qq, KK, VV, n, segs, params, with_output=False)
+                    if margin_ok(r.M_vis_max, len(vis), params) and boundary_gap(r.scores, vis, r.k) >= GAP:
+                        continue
+                    good = False
+                    try:
+                        plant_sequence(qq, KK, VV, n, segs, params)
+                    except RuntimeError:
+                        pass
+            if good:
+                break
+        ok[b] = good
+        res[b] = O.decode_step_queries(w.q[b], w.K[b], w.V[b], L, w.segments[b], params, kv_groups=kv_groups)
+    return res, ok
+
+
 def params_of(w) -> O.OracleParams:
     return O.OracleParams(tau_mass=w.tau_mass, tau_score=w.tau_score,
                           r_lo_bp=w.r_lo_bp, r_hi_bp=w.r_hi_bp, clamp=w.clamp)

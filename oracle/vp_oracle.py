@@ -37,7 +37,12 @@ Readings where the paper is silent:
      sequence) runs the whole method on each KV group g as if it were a
      sequence of its own: the G query heads that read KV head g give the head
      mean and head max of Eq. (5)/(7), the head average of Eq. (2) and a budget
-     k_g, and those G heads attend over their group's own kept set.
+     k_g, and those G heads attend over their group's own kept set;
+  A20 several queries per sequence (an extension: speculative or multi-token
+     decoding): the T queries are the last T positions of the sequence, query t
+     sees the positions before L - T + 1 + t (itself included) and is a decode
+     step of its own (its own masses, budget, kept set and output); the other
+     queries' positions are text, so the visual segments are cut at L - T + 1.
 
 Parity status: every function below is pinned by tests/test_oracle_pins.py
 (closed forms, invariants, brute force, library cross-checks and the
@@ -55,6 +60,7 @@ __all__ = [
     "budget", "budget_top_p", "importance_scores", "select_top_k", "pruned_attention",
     "OracleParams", "SequenceResult", "decode_step_sequence", "decode_step",
     "visual_positions", "text_positions", "GroupedResult", "decode_step_sequence_kv_groups",
+    "clip_segments", "decode_step_queries",
 ]
 
 
@@ -348,3 +354,36 @@ def decode_step_sequence_kv_groups(q: np.ndarray, K: np.ndarray, V: np.ndarray,
         k=np.array([r.k for r in parts], dtype=np.int64),
         vis_idx=[r.vis_idx for r in parts],
         out=np.concatenate([r.out for r in parts]) if with_output else None)
+
+
+# --------------------------------------------------------------------------
+# several queries per sequence (reading A20)
+# --------------------------------------------------------------------------
+def clip_segments(segments, n: int):
+    """The visual segments cut to the first n positions (empty pieces dropped)."""
+    out = []
+    for (st, ln) in segments:
+        ln = min(ln, n - st)
+        if ln > 0:
+            out.append((st, ln))
+    return out
+
+
+def decode_step_queries(q: np.ndarray, K: np.ndarray, V: np.ndarray, seq_len: int, segments,
+                        params: OracleParams, kv_groups: bool = False, with_output: bool = True):
+    """T queries of one sequence (q: [T, Hq, d]), each a decode step of its own (A20).
+
+    Query t sees the first L0 + t positions, L0 = seq_len - T + 1; positions from
+    L0 on are never visual. Returns a list of T results (SequenceResult, or
+    GroupedResult with ``kv_groups``).
+    """
+    T = q.shape[0]
+    L0 = seq_len - T + 1
+    segs = clip_segments(segments, max(L0, 0))
+    # a sequence shorter than T leaves the first queries without positions
+    n = [max(L0 + t, 0) for t in range(T)]
+    if kv_groups:
+        return [decode_step_sequence_kv_groups(q[t], K, V, n[t], segs, params, with_output=with_output)
+                for t in range(T)]
+    return [decode_step_sequence(q[t], K, V, n[t], segs, params, with_output=with_output)
+            for t in range(T)]

@@ -23,7 +23,7 @@ from dataclasses import dataclass, field
 import numpy as np
 
 __all__ = ["Workload", "CONFIGS", "generate", "bf16_round", "bf16_to_f32",
-           "Cfg5Stream", "layout_arrays"]
+           "Cfg5Stream", "layout_arrays", "with_queries"]
 
 
 # --------------------------------------------------------------------------
@@ -99,7 +99,7 @@ def layout_arrays(segments):
 # --------------------------------------------------------------------------
 # seeded streams: one independent stream per (config, sequence, purpose)
 # --------------------------------------------------------------------------
-_STREAMS = {"q": 0, "K": 1, "V": 2, "spike": 3, "lengths": 4, "offset": 5, "steps": 6}
+_STREAMS = {"q": 0, "K": 1, "V": 2, "spike": 3, "lengths": 4, "offset": 5, "steps": 6, "queries": 7}
 
 
 def _rng(cfg: int, stream: str, b: int = 0, seed: int | None = None) -> np.random.Generator:
@@ -265,3 +265,28 @@ class Cfg5Stream:
         kr = _normal(rng, (w.B, w.Hkv, w.d), 0.5)
         vr = _normal(rng, (w.B, w.Hkv, w.d), 0.5)
         return bf16_round(self._q), bf16_round(kr), bf16_round(vr), self.base_len + t
+
+
+# --------------------------------------------------------------------------
+# several queries per sequence (speculative / multi-token decoding)
+# --------------------------------------------------------------------------
+def with_queries(w: Workload, T: int, seed: int = 0) -> Workload:
+    """A copy of ``w`` whose q holds T queries per sequence, [B, T, Hq, d]:
+    query 0 is w's query and q_t = 0.9 q_{t-1} + 0.1 eps_t (eps ~ N(0, 1)), the
+    drift of the decode loop, carried in float32 and rounded to the stored
+    dtype. The queries stand for the last T positions of each sequence (whose
+    K/V rows are the text rows the generator already wrote there)."""
+    f32 = w.dtype == "f32"
+    q = (w.q if f32 else bf16_to_f32(w.q)).astype(np.float32)
+    qs = [q]
+    cur = q.copy()
+    for t in range(1, T):
+        eps = _normal(_rng(0, "queries", t, 7000 + seed), q.shape)
+        cur = np.float32(0.9) * cur + np.float32(0.1) * eps
+        qs.append(cur.copy())
+    qt = np.stack(qs, axis=1)
+    return Workload(name=f"{w.name}-q{T}", dtype=w.dtype, B=w.B, Hq=w.Hq, Hkv=w.Hkv, d=w.d, S_cap=w.S_cap,
+                    seq_len=w.seq_len.copy(), segments=[list(x) for x in w.segments],
+                    q=qt if f32 else bf16_round(qt), K=w.K.copy(), V=w.V.copy(), tau_mass=w.tau_mass,
+                    tau_score=w.tau_score, r_lo_bp=w.r_lo_bp, r_hi_bp=w.r_hi_bp, clamp=w.clamp,
+                    meta=dict(w.meta, queries=T))

@@ -490,3 +490,112 @@ def test_kv_groups_single_group_is_the_sequence_path():
     assert gr.k[0] == r.k and list(gr.vis_idx[0]) == list(r.vis_idx)
     assert gr.M_vis[0] == r.M_vis and gr.M_vis_max[0] == r.M_vis_max
     np.testing.assert_array_equal(gr.out, r.out)
+
+
+# ---------------------------------------------------------------------------
+# several queries per sequence (each query a decode step of its own over the
+# positions before it; the reading is stated in the reference's header)
+# ---------------------------------------------------------------------------
+def _brute_queries(q, K, V, L, segs, tau_mass, r_lo_bp, r_hi_bp):
+    """Pure-Python loops: query t sees positions < L - T + 1 + t; positions from
+    L - T + 1 on are text whatever the segments say; per query the per-head
+    tempered visual mass, head max, budget, head-averaged scores, top-k and
+    attention over kept + visible text."""
+    T, Hq, d = len(q), len(q[0]), len(q[0][0])
+    Hkv = len(K)
+    G = Hq // Hkv
+    L0 = L - T + 1
+    vis = sorted(p for s, n in segs for p in range(s, s + n) if p < L0)
+    nv = len(vis)
+    res = []
+    for t in range(T):
+        n = L0 + t
+        masses, S = [], [0.0] * nv
+        for h in range(Hq):
+            z = [sum(q[t][h][c] * K[h // G][j][c] for c in range(d)) / math.sqrt(d) for j in range(n)]
+            zt = max(z)
+            et = [math.exp((x - zt) / tau_mass) for x in z]
+            masses.append(sum(et[p] for p in vis) / sum(et))
+            e1 = [math.exp(x - zt) for x in z]
+            for i, p in enumerate(vis):
+                S[i] += e1[p] / sum(e1) / Hq
+        k = math.ceil(max(masses) * nv)
+        lo = -((-r_lo_bp * nv) // 10000)
+        hi = max((r_hi_bp * nv) // 10000, lo)
+        k = min(max(k, lo), hi, nv)
+        kept = sorted(vis[i] for i in sorted(range(nv), key=lambda i: (-S[i], vis[i]))[:k])
+        J = sorted(set(kept) | (set(range(n)) - set(vis)))
+        out = []
+        for h in range(Hq):
+            z = [sum(q[t][h][c] * K[h // G][j][c] for c in range(d)) / math.sqrt(d) for j in J]
+            zm = max(z)
+            e = [math.exp(x - zm) for x in z]
+            out.append([sum(e[i] * V[h // G][j][c] for i, j in enumerate(J)) / sum(e) for c in range(d)])
+        res.append(dict(masses=masses, k=k, S=S, kept=kept, out=out))
+    return res
+
+
+def test_queries_brute_force_tiny():
+    rng = np.random.default_rng(41)
+    for trial, (T, segs) in enumerate([(3, ((2, 14), (20, 9))), (2, ((0, 10), (25, 15))), (4, ((5, 30),))]):
+        # the last segment of the second and third cases runs into the other queries' positions
+        L, Hq, Hkv, d = 40, 4, 2, 3
+        q = rng.standard_normal((T, Hq, d))
+        K = rng.standard_normal((Hkv, L, d)) * 2.0
+        V = rng.standard_normal((Hkv, L, d))
+        p = O.OracleParams(tau_mass=0.5, r_lo_bp=500, r_hi_bp=4000)
+        rs = O.decode_step_queries(q, K, V, L, [tuple(x) for x in segs], p)
+        bf = _brute_queries(q.tolist(), K.tolist(), V.tolist(), L, segs, 0.5, 500, 4000)
+        for t in range(T):
+            np.testing.assert_allclose(rs[t].mass_head, bf[t]["masses"], rtol=1e-12)
+            assert rs[t].k == bf[t]["k"]
+            np.testing.assert_allclose(rs[t].scores, bf[t]["S"], rtol=1e-12)
+            assert list(rs[t].vis_idx) == bf[t]["kept"]
+            np.testing.assert_allclose(rs[t].out, bf[t]["out"], rtol=1e-11, atol=1e-13)
+
+
+def test_queries_single_query_is_the_step():
+    rng = np.random.default_rng(42)
+    q, K, V, L, segs = _rand_case(rng, Hq=4, Hkv=2, d=8, L=60, segs=((4, 40),))
+    p = O.OracleParams()
+    r = O.decode_step_sequence(q, K, V, L, segs, p)
+    (r1,) = O.decode_step_queries(q[None], K, V, L, segs, p)
+    assert r1.k == r.k and list(r1.vis_idx) == list(r.vis_idx)
+    np.testing.assert_array_equal(r1.out, r.out)
+    np.testing.assert_array_equal(r1.mass_head, r.mass_head)
+
+
+def test_queries_are_causal():
+    """Rows at or after query t's successor positions never change query t's
+    results, and do change the later queries'."""
+    rng = np.random.default_rng(43)
+    T, L, Hq, Hkv, d = 3, 50, 4, 1, 8
+    q = rng.standard_normal((T, Hq, d))
+    K = rng.standard_normal((Hkv, L, d))
+    V = rng.standard_normal((Hkv, L, d))
+    p = O.OracleParams(clamp=False, tau_mass=1.0)
+    segs = [(3, 30)]
+    a = O.decode_step_queries(q, K, V, L, segs, p)
+    K2, V2 = K.copy(), V.copy()
+    K2[:, L - 1] += 3.0   # the last query's own row
+    V2[:, L - 1] -= 2.0
+    b = O.decode_step_queries(q, K2, V2, L, segs, p)
+    for t in range(T - 1):
+        np.testing.assert_array_equal(a[t].out, b[t].out)
+        np.testing.assert_array_equal(a[t].mass_head, b[t].mass_head)
+    assert not np.allclose(a[T - 1].out, b[T - 1].out)
+    assert not np.allclose(a[T - 1].mass_head, b[T - 1].mass_head)
+
+
+def test_queries_shorter_than_the_batch_of_queries():
+    """A sequence of 2 tokens with 4 queries: the first two queries see nothing
+    (zero output, no budget), the others see 1 and 2 text tokens."""
+    rng = np.random.default_rng(44)
+    q = rng.standard_normal((4, 2, 4))
+    K = rng.standard_normal((1, 2, 4))
+    V = rng.standard_normal((1, 2, 4))
+    rs = O.decode_step_queries(q, K, V, 2, [(0, 2)], O.OracleParams())
+    assert [r.k for r in rs] == [0, 0, 0, 0]
+    np.testing.assert_array_equal(rs[0].out, 0.0)
+    np.testing.assert_array_equal(rs[1].out, 0.0)
+    np.testing.assert_allclose(rs[2].out, np.tile(V[0, 0], (2, 1)), rtol=1e-15)

@@ -54,3 +54,20 @@ def test_plant_kv_groups_cfg2():
     r2 = O.decode_step_sequence_kv_groups(w.q[0], w.K[0], w.V[0], L, w.segments[0], p, with_output=False)
     assert list(r2.k) == list(r.k)
     assert all(list(a) == list(b) for a, b in zip(r2.vis_idx, r.vis_idx))
+
+
+def test_plant_queries_cfg2_two_queries():
+    """Two queries per sequence: both hold margin and gap at once after planting,
+    and each query's reference sees its own prefix."""
+    w = W.with_queries(W.generate(2), 2)
+    p = P.params_of(w)
+    res, ok = P.plant_queries(w, p)
+    assert ok[0]
+    L = int(w.seq_len[0])
+    segs = O.clip_segments(w.segments[0], L - 1)
+    vis = O.visual_positions(L - 1, segs)
+    for t, r in enumerate(res[0]):
+        assert P.margin_ok(r.M_vis_max, len(vis), p)
+        assert P.boundary_gap(r.scores, vis, r.k) >= P.GAP
+        r2 = O.decode_step_sequence(w.q[0, t], w.K[0], w.V[0], L - 1 + t, segs, p, with_output=False)
+        assert r2.k == r.k and list(r2.vis_idx) == list(r.vis_idx)

@@ -72,3 +72,16 @@ def test_cfg5_stream_appends_and_drifts():
         assert pos == 10496 + t and q.shape == (2, 64, 128) and kr.shape == (2, 8, 128)
         rms.append(float(np.sqrt((W.bf16_to_f32(q) ** 2).mean())))
     assert rms[7] < rms[0]          # 0.9 decay dominates the 0.1 innovation
+
+
+def test_with_queries_drift_and_determinism():
+    w = W.generate(1)
+    a = W.with_queries(w, 3)
+    b = W.with_queries(w, 3)
+    assert a.q.shape == (w.B, 3, w.Hq, w.d) and a.q.dtype == w.q.dtype
+    np.testing.assert_array_equal(a.q, b.q)
+    np.testing.assert_array_equal(a.q[:, 0], w.q)          # query 0 is the workload's own
+    assert not np.array_equal(a.q[:, 1], a.q[:, 2])
+    # the drift keeps consecutive queries close: 0.9 q + 0.1 eps
+    c = np.corrcoef(a.q[:, 0].ravel(), a.q[:, 1].ravel())[0, 1]
+    assert c > 0.95
