@@ -24,7 +24,7 @@
  *           call only enqueues kernels on that stream and returns; none
  *           synchronises. k and the kept indices stay on the device, so a step
  *           never waits for the host.
- * Shapes.   q and out are [B, Hq, d] contiguous. K and V caches are addressed as
+ * Shapes.   q and out are [B, T, Hq, d] contiguous (T = 1 by default). K and V caches are addressed as
  *           base + b*kv_stride_b + h*kv_stride_h + s*kv_stride_s (elements) with
  *           the d elements of a row contiguous. Query head h reads KV head
  *           h / (Hq/Hkv) (grouped-query attention).
@@ -55,10 +55,20 @@
  *           variant): each KV group g (query heads g*G .. g*G+G-1, G = Hq/Hkv)
  *           is treated as a sequence of its own: Eq. (5)/(7) take the mean and
  *           max over the group's G heads, Eq. (2) averages over them, and the
- *           group's heads attend over the group's own kept set. Per-sequence
- *           results are then held in R = Hkv "selection rows" per sequence
- *           (row b*Hkv + g), else R = 1 (row b): below, mass_seq is [B*R, 2],
- *           scores [B*R, max_vis], k [B*R] and vis_idx [B*R, k_cap].
+ *           group's heads attend over the group's own kept set. Per-query
+ *           results are then held in U = Hkv "selection rows" (row u = g),
+ *           else U = 1.
+ * Queries.  shape.n_queries = T > 1 runs T queries per sequence in one step
+ *           (speculative or multi-token decoding; an extension of the paper's
+ *           one query per step): the queries are the sequence's last T
+ *           positions, query t sees the positions before L - T + 1 + t, and
+ *           each is a decode step of its own (own masses, budget, kept set,
+ *           output); the positions from L - T + 1 on are text whatever the
+ *           segments say. The K/V rows are read once for all T queries.
+ *           q and out are then [B, T, Hq, d] and mass_head [B, T, Hq].
+ * Rows.     With R = T*U selection rows per sequence, row (b*T + t)*U + u:
+ *           mass_seq is [B*R, 2], scores [B*R, max_vis], k [B*R] and vis_idx
+ *           [B*R, k_cap] (R = 1 by default: row b).
  * Dtypes.   VP_BF16: q, K, V, out are bfloat16; VP_F32: all float32. Logits,
  *           softmax statistics, masses and scores are float32; accumulation is
  *           float32 (bf16 products are exact in float32).
@@ -102,7 +112,7 @@ typedef struct vp_shape {
   int32_t k_cap;        /* row stride of vis_idx; >= every budget vp_budget can return */
   int32_t block_size;   /* 0: contiguous caches; P > 0 (a power of two <= 65536): paged caches of P rows per block */
   int32_t scope;        /* vp_scope: selection rows per sequence R = 1 (VP_SCOPE_SEQUENCE) or Hkv (VP_SCOPE_KV_GROUP) */
-  int32_t reserved;     /* must be 0 */
+  int32_t n_queries;    /* T: queries per sequence (0 is read as 1); T * Hq / Hkv <= 16 */
   int64_t kv_stride_b;  /* elements between sequences in K and V (paged: between physical blocks) */
   int64_t kv_stride_h;  /* elements between KV heads */
   int64_t kv_stride_s;  /* elements between token rows (>= head_dim) */
@@ -145,11 +155,12 @@ vp_status vp_workspace_size(const vp_shape* shape, size_t* bytes);
  * (Sec. 4.3), and the Eq. (2) importance score of every visual token (Sec. 4.2).
  *
  *   Z_{h,j}      = sm_scale * <q_h, K_{g(h), j}>                j < seq_len
- *   mass_head    = sum_{j visual} softmax_j(Z_h / tau_mass)      [B, Hq]
+ *   mass_head    = sum_{j visual} softmax_j(Z_h / tau_mass)      [B, T, Hq]
  *   mass_seq     = {mean_h mass_head, max_h mass_head}           [B*R, 2]
  *   scores[b, i] = (1/Hq) sum_h softmax_j(Z_h / tau_score)_{v_i} [B*R, max_vis], rank order;
  *                  entries i >= N_v of the sequence are not written.
- * (VP_SCOPE_KV_GROUP: row b*Hkv + g, with h over group g's G heads and 1/G.)
+ * (per query t, j < its visible length; VP_SCOPE_KV_GROUP: row per KV group g,
+ * with h over the group's G heads and 1/G.)
  *
  * q: [B, Hq, d]; K: cache; V: cache or NULL. When V is non-NULL the same pass
  * over K also accumulates the softmax-weighted text-token values (the text
@@ -227,10 +238,10 @@ vp_status vp_select_topk(const vp_shape* shape, const vp_layout* layout,
  * vp_sparse_decode_attn -- the step's attention over the pruned context
  * J_b = {vis_idx[r, 0 .. k[r])} U {text positions of b} (Sec. 4.1/4.2; the
  * dropped visual tokens are absent from the softmax, which is renormalised
- * over J_b at temperature 1), r the selection row of head h (b, or
- * b*Hkv + g(h) with VP_SCOPE_KV_GROUP):
+ * over J_b at temperature 1), r the selection row of head h (per query t, the
+ * text positions of J_b are those query t sees):
  *
- *   out[b, h] = sum_{j in J_b} softmax_{J_b}(Z_{h, j}) V_{g(h), j}      [B, Hq, d]
+ *   out[b, h] = sum_{j in J_b} softmax_{J_b}(Z_{h, j}) V_{g(h), j}      [B, T, Hq, d]
  *
  * An empty J_b yields zeros. Kept indices outside [0, seq_len) or equal to -1
  * are skipped. With flags & VP_ATTN_TEXT_FROM_WORKSPACE the text part is taken
@@ -250,8 +261,8 @@ vp_status vp_sparse_decode_attn(const vp_shape* shape, const vp_layout* layout, 
  * budget and top-k of every sequence run in one launch (a sequence's visual
  * ranks are scored in chunks on several work-groups, the last chunk to finish
  * selects). All outputs are written as by the four calls (same arithmetic,
- * same reduction order): mass_head [B, Hq], mass_seq [B*R, 2],
- * scores [B*R, max_vis], k [B*R], vis_idx [B*R, k_cap], out [B, Hq, d]; V is
+ * same reduction order): mass_head [B, T, Hq], mass_seq [B*R, 2],
+ * scores [B*R, max_vis], k [B*R], vis_idx [B*R, k_cap], out [B, T, Hq, d]; V is
  * required.
  *
  * events: optional caller-created hipEvent_t recorded on `stream`, i < n_events

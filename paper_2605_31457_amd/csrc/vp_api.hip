@@ -35,8 +35,10 @@ constexpr int kMaxBatch = 65535;
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
-// selection rows per sequence: one, or one per KV group
-int rows_per_seq(const vp_shape& s) { return s.scope == VP_SCOPE_KV_GROUP ? s.n_kv_heads : 1; }
+// queries per sequence, and selection rows per query: one, or one per KV group
+int queries(const vp_shape& s) { return s.n_queries > 1 ? s.n_queries : 1; }
+int rows_per_query(const vp_shape& s) { return s.scope == VP_SCOPE_KV_GROUP ? s.n_kv_heads : 1; }
+int rows_per_seq(const vp_shape& s) { return queries(s) * rows_per_query(s); }
 
 vp_status check_shape(const vp_shape* s) {
   if (!s) return fail(VP_ERR_NULL, "shape is NULL");
@@ -57,9 +59,12 @@ vp_status check_shape(const vp_shape* s) {
     return fail(VP_ERR_SHAPE, "block_size %d: 0 (contiguous) or a power of two <= 65536", s->block_size);
   if (s->scope != VP_SCOPE_SEQUENCE && s->scope != VP_SCOPE_KV_GROUP)
     return fail(VP_ERR_RANGE, "scope %d: VP_SCOPE_SEQUENCE or VP_SCOPE_KV_GROUP", s->scope);
-  if (s->reserved != 0) return fail(VP_ERR_RANGE, "reserved field %d must be 0", s->reserved);
+  if (s->n_queries < 0) return fail(VP_ERR_RANGE, "n_queries %d < 0", s->n_queries);
+  if (queries(*s) * (s->n_q_heads / s->n_kv_heads) > kMaxGroup)
+    return fail(VP_ERR_UNSUPPORTED, "n_queries %d x query group %d > %d rows per KV head", queries(*s),
+                s->n_q_heads / s->n_kv_heads, kMaxGroup);
   if (static_cast<int64_t>(s->batch) * rows_per_seq(*s) > kMaxBatch)
-    return fail(VP_ERR_UNSUPPORTED, "batch x selection rows %lld > %d",
+    return fail(VP_ERR_UNSUPPORTED, "batch x queries x selection rows %lld > %d",
                 static_cast<long long>(s->batch) * rows_per_seq(*s), kMaxBatch);
   const int esz = s->dtype == VP_BF16 ? 2 : 4;
   const int64_t align_elems = 16 / esz;
@@ -138,7 +143,8 @@ AttendArgs attend_args(const vp_shape* s, const vp_layout* l, const vp_params* p
   a.G = s->n_q_heads / s->n_kv_heads;
   a.max_seq_len = s->max_seq_len;
   a.max_vis = s->max_vis;
-  a.U = rows_per_seq(*s);
+  a.T = queries(*s);
+  a.U = rows_per_query(*s);
   a.zscale = zscale_of(s, p);
   a.inv_tau_m = 1.0f / p->tau_mass;
   a.inv_tau_s = 1.0f / p->tau_score;
@@ -186,7 +192,8 @@ MassArgs mass_args(const vp_shape* s, const vp_layout* l, const Plan& plan, cons
   m.nparts = plan.nparts;
   m.Hkv = s->n_kv_heads;
   m.G = s->n_q_heads / s->n_kv_heads;
-  m.U = rows_per_seq(*s);
+  m.T = queries(*s);
+  m.U = rows_per_query(*s);
   m.zs_rows = plan.zs_rows;
   m.zs_gp = plan.zs_gp;
   m.inv_tau_m = a.inv_tau_m;
@@ -206,7 +213,8 @@ BudgetArgs budget_args(const vp_shape* s, const vp_layout* l, const vp_params* p
   b.seg_off = l->vis_seg_off;
   b.seg = l->vis_seg;
   b.B = s->batch;
-  b.U = rows_per_seq(*s);
+  b.R = rows_per_seq(*s);
+  b.T = queries(*s);
   b.max_seq_len = s->max_seq_len;
   b.r_lo_bp = p->r_lo_bp;
   b.r_hi_bp = p->r_hi_bp;
@@ -222,7 +230,8 @@ TopkArgs topk_args(const vp_shape* s, const vp_layout* l, const float* scores, c
   t.seg_off = l->vis_seg_off;
   t.seg = l->vis_seg;
   t.B = s->batch;
-  t.U = rows_per_seq(*s);
+  t.R = rows_per_seq(*s);
+  t.T = queries(*s);
   t.max_seq_len = s->max_seq_len;
   t.max_vis = s->max_vis;
   t.k_cap = s->k_cap;
@@ -239,7 +248,9 @@ MergeArgs merge_args(const vp_shape* s, const vp_layout* l, const Plan& plan, co
   m.kk = k;
   m.B = s->batch;
   m.Hq = s->n_q_heads;
-  m.U = rows_per_seq(*s);
+  m.G = s->n_q_heads / s->n_kv_heads;
+  m.T = queries(*s);
+  m.U = rows_per_query(*s);
   m.max_seq_len = s->max_seq_len;
   m.k_cap = s->k_cap;
   m.nparts = plan.nparts;
@@ -293,12 +304,13 @@ Plan make_plan(const vp_shape& s) {
 #ifdef VP_KEPT_SPLIT
   p.split = VP_KEPT_SPLIT;
 #else
-  p.split = static_cast<int64_t>(s.batch) * s.n_kv_heads * ((s.k_cap + 63) / 64) >= 1024 ? 64 : 32;
+  p.split = static_cast<int64_t>(s.batch) * s.n_kv_heads * queries(s) * ((s.k_cap + 63) / 64) >= 1024 ? 64 : 32;
 #endif
   p.nsplit = (s.k_cap + p.split - 1) / p.split;
-  const size_t B = s.batch, Hq = s.n_q_heads, d = s.head_dim;
+  // per-head arrays hold one entry per query row (virtual head): T*Hq per sequence
+  const size_t B = s.batch, Hq = static_cast<size_t>(s.n_q_heads) * queries(s), d = s.head_dim;
   p.zs_rows = ((s.max_seq_len + 31) / 32) * 32;
-  p.zs_gp = s.n_q_heads / s.n_kv_heads <= 8 ? 8 : 16;
+  p.zs_gp = queries(s) * (s.n_q_heads / s.n_kv_heads) <= 8 ? 8 : 16;
   size_t off = 0;
   p.zs = off;
   off = align256(off + B * static_cast<size_t>(s.n_kv_heads) * p.zs_rows * static_cast<size_t>(p.zs_gp) * 4);
@@ -321,7 +333,7 @@ Plan make_plan(const vp_shape& s) {
   // Select kernel: chunks of whole rounds (a round scores 1024 / lanes-per-token
   // visual ranks), enough rounds per chunk that the launch has about
   // VP_SELECT_WGS work-groups, so the spilled logits stream through many CUs.
-  const int64_t tpr = select_tokens_per_round(s.n_kv_heads, rows_per_seq(s));
+  const int64_t tpr = select_tokens_per_round(s.n_kv_heads, rows_per_query(s));
   const int64_t want = static_cast<int64_t>(rows) * s.max_vis;
   int64_t rounds = (want + tpr * VP_SELECT_WGS - 1) / (tpr * VP_SELECT_WGS);
   if (rounds < 1) rounds = 1;
@@ -459,7 +471,8 @@ vp_status vp_budget_top_p(const vp_shape* shape, const vp_layout* layout, const 
   t.seg_off = layout->vis_seg_off;
   t.seg = layout->vis_seg;
   t.B = shape->batch;
-  t.U = rows_per_seq(*shape);
+  t.R = rows_per_seq(*shape);
+  t.T = queries(*shape);
   t.max_seq_len = shape->max_seq_len;
   t.max_vis = shape->max_vis;
   t.p = p;

@@ -25,8 +25,11 @@
 // 16-byte pieces are XOR-swizzled by the row index (slot = piece ^ row), which
 // keeps the operand reads below free of bank conflicts.
 //
-// Per 32-row sub-tile the grouped query heads of this KV head (G <= 16, padded
-// to 16) are scored against the key rows on the matrix cores:
+// Per 32-row sub-tile the query rows of this KV head -- its G grouped heads for
+// each of the sequence's T queries, T*G <= 16, padded to 16 -- are scored
+// against the key rows on the matrix cores (with several queries per sequence
+// the K/V rows are read once for all of them; query t sees the positions
+// before L - T + 1 + t):
 //   C'[token][head] = K_tile[token][:] . q[head][:]
 // bf16: v_mfma_f32_16x16x32_bf16 (two 16-row halves x d/32 k-steps);
 // fp32: v_mfma_f32_16x16x4_f32. Lane l then holds head l%16 for tokens
@@ -293,7 +296,8 @@ struct Pass {
   static constexpr bool TEXT = !KEPT && !VIS;                    // a text-row pass
 
   const AttendArgs& a;
-  int lane, n16, a4, L, r0, r1, step, h;  // rows [r0, r1) in tiles `step` apart
+  int lane, n16, a4, L, r0, r1, step, h;  // rows [r0, r1) in tiles `step` apart; h: virtual head
+  int L0, lim;  // rows from L0 on are the queries' own; this lane's query sees rows < lim
   bool hv;
   const int32_t* kept;
   const char* Kb;
@@ -412,6 +416,12 @@ struct Pass {
 #pragma unroll
         for (int i = 0; i < 8; ++i)
           if (t0 + 16 * (i >> 2) + 4 * a4 + (i & 3) >= t_end) valid &= ~(1u << i);
+      }
+      if (t_end > L0) {
+        // several queries: the rows after a query's own position are hidden from it
+#pragma unroll
+        for (int i = 0; i < 8; ++i)
+          if (t0 + 16 * (i >> 2) + 4 * a4 + (i & 3) >= lim) valid &= ~(1u << i);
       }
       if (cls == TILE_VIS) {
         vis = valid;
@@ -532,9 +542,10 @@ struct PassLds {
   static constexpr int BYTES = max_i(NSUB * SUB, lds_floor(DT, MODE));
 };
 
-// The work of one work-group (part `part` of KV head g of sequence b).
+// The work of one work-group (part `part` of KV head g of sequence b; in the
+// kept pass gy = g*T + t also names the query t whose kept list it reads).
 template <int DT, int D, int MODE>
-__device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* lds, int part, int g, int b) {
+__device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* lds, int part, int gy, int b) {
   using C = Cfg<DT, D>;
   using P = Pass<DT, D, MODE>;
   using Q = PassLds<DT, D, MODE>;
@@ -548,9 +559,12 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
   s.a4 = s.lane >> 4;
   s.L = clamp_len(a.seq_len[b], a.max_seq_len);
   s.kept = nullptr;
+  const int qk = P::KEPT ? gy % a.T : 0;  // kept pass: the query
+  const int g = P::KEPT ? gy / a.T : gy;   // KV head
   if constexpr (P::KEPT) {
     if (s.L == 0) return;
-    const size_t row = static_cast<size_t>(b) * a.U + g / (a.Hkv / a.U);  // the KV head's selection row
+    // the selection row of query qk that KV head g belongs to
+    const size_t row = (static_cast<size_t>(b) * a.T + qk) * a.U + g / (a.Hkv / a.U);
     int kb = a.kk[row];
     kb = kb < 0 ? 0 : (kb > a.k_cap ? a.k_cap : kb);
     s.r0 = part * a.split;
@@ -564,8 +578,13 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
   }
   if (s.r0 >= s.r1) return;
 
-  s.h = g * a.G + s.n16;
-  s.hv = s.n16 < a.G;
+  // lane row n16 <-> virtual head vh of this KV head: query vh / G, head g*G + vh % G
+  const int vh = P::KEPT ? qk * a.G + s.n16 : s.n16;
+  s.hv = s.n16 < (P::KEPT ? a.G : a.T * a.G);
+  const int tq = s.hv ? vh / a.G : 0;
+  s.h = g * a.T * a.G + vh;
+  s.L0 = s.L - a.T + 1;
+  s.lim = s.L0 + tq;
   // contiguous caches: sequence b's rows from its base; paged caches: rows of
   // physical blocks (the block offset is added per row)
   constexpr bool paged = P::PAGED;
@@ -576,9 +595,8 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
   s.bt = paged ? a.block_table + static_cast<size_t>(b) * a.nblk : nullptr;
   s.bstride = static_cast<size_t>(a.sb) * C::ESZ;
   s.bmask = paged ? (1 << a.bs_log2) - 1 : 0;
-  load_q<DT, D>(s.qf,
-                static_cast<const char*>(a.q) + (static_cast<size_t>(b) * a.Hq + (s.hv ? s.h : 0)) * C::ROWB,
-                s.hv, s.a4);
+  const size_t qrow = s.hv ? (static_cast<size_t>(b) * a.T + tq) * a.Hq + g * a.G + (vh - tq * a.G) : 0;
+  load_q<DT, D>(s.qf, static_cast<const char*>(a.q) + qrow * C::ROWB, s.hv, s.a4);
   s.m_v = kNegInf;
   s.Ls_v = s.Lm_v = 0.f;
   s.m_t = kNegInf;
@@ -592,7 +610,7 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
   cur.cls = TILE_TEXT;
   if constexpr (!P::KEPT) {
     const int o0 = a.seg_off[b];
-    cur.w.start(a.seg + 2 * static_cast<long>(o0), a.seg_off[b + 1] - o0, s.L);
+    cur.w.start(a.seg + 2 * static_cast<long>(o0), a.seg_off[b + 1] - o0, vis_len(s.L, a.T));
   }
   cur = s.sub_at(cur, s.r0);
 
@@ -641,7 +659,7 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
     const float s_ls = sum_over_quads(s.Ls_v * fs);
     const float s_lm = sum_over_quads(s.Lm_v * fm);
     if (s.hv && s.a4 == 0) {
-      float* st = a.stats + ((static_cast<size_t>(b) * a.Hq + s.h) * a.nparts + part) * 8;
+      float* st = a.stats + ((static_cast<size_t>(b) * a.T * a.Hq + s.h) * a.nparts + part) * 8;
       *reinterpret_cast<float4*>(st) = make_float4(M, s_ls, s_lm, 0.f);
     }
   } else {
@@ -650,11 +668,11 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
     const float s_ls = P::TSTATS ? (a.tau_s_one ? s_lt : sum_over_quads(s.Ls_t)) : 0.f;
     if (s.hv) {
       if constexpr (P::KEPT) {
-        const size_t row = (static_cast<size_t>(b) * a.Hq + s.h) * a.nsplit + part;
+        const size_t row = (static_cast<size_t>(b) * a.T * a.Hq + s.h) * a.nsplit + part;
         if (s.a4 == 0) *reinterpret_cast<float2*>(a.kstats + row * 2) = make_float2(s.m_t, s_lt);
         store_acc<DT, D, C::ACC_N>(a.kacc + row * D, s.acc, s.a4);
       } else {
-        const size_t row = (static_cast<size_t>(b) * a.Hq + s.h) * a.nparts + part;
+        const size_t row = (static_cast<size_t>(b) * a.T * a.Hq + s.h) * a.nparts + part;
         if (s.a4 == 0) {
           if constexpr (P::TSTATS)
             *reinterpret_cast<float4*>(a.stats + row * 8 + 4) = make_float4(s.m_t, s_lt, s_lm, s_ls);
@@ -667,16 +685,17 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
   }
 }
 
-// The extra work-group of a launch with the visual role (x = its last index):
-// for KV head g < U, a new step's arrival counter of selection row (b, g) at
-// zero; for KV head 0, also the sequence's clipped segment table (positions and
-// visual ranks) for the select kernel.
+// The extra work-group of a launch with the visual role (x = its last index,
+// KV head 0): a new step's arrival counters of the sequence's T*U selection
+// rows at zero, and the sequence's clipped segment table (positions and visual
+// ranks) for the select kernel.
 __device__ __forceinline__ void step_setup(const AttendArgs& a, int g, int b) {
-  const int lane = threadIdx.x;
-  if (a.sync && lane == 0 && g < a.U) a.sync[b * a.U + g] = 0u;
   if (g != 0) return;
+  const int lane = threadIdx.x;
+  if (a.sync)
+    for (int i = lane; i < a.T * a.U; i += 64) a.sync[static_cast<size_t>(b) * a.T * a.U + i] = 0u;
   if (a.segtab) {
-    const int L = clamp_len(a.seq_len[b], a.max_seq_len);
+    const int L = vis_len(clamp_len(a.seq_len[b], a.max_seq_len), a.T);
     const int o0 = a.seg_off[b];
     load_segments(static_cast<SegTable*>(a.segtab)[b], a.seg + 2 * static_cast<long>(o0), a.seg_off[b + 1] - o0, L,
                   lane);
@@ -716,7 +735,7 @@ hipError_t launch_dd(const AttendArgs& a, int mode, hipStream_t st) {
   // launches with the visual role carry one more work-group per sequence (step_setup)
   const int gx = mode == MODE_KEPT ? a.nsplit
                                    : (mode == MODE_DUAL ? 2 * a.nparts + 1 : (mode == MODE_VIS ? a.nparts + 1 : a.nparts));
-  const dim3 grid(gx, a.Hkv, a.B);
+  const dim3 grid(gx, mode == MODE_KEPT ? a.Hkv * a.T : a.Hkv, a.B);
   const dim3 block(64);
   switch (mode) {
     case MODE_DUAL:

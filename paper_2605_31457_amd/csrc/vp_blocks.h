@@ -46,9 +46,9 @@ __device__ __forceinline__ int lanes_per_head(int Hq, int nparts) {
   return l;
 }
 
-// Merges the per-part statistics of sequence b (visual and text rows, kept
-// apart by the context pass) for every head of selection row u of the
-// sequence (heads [u Hq/U, (u+1) Hq/U)) onto the head's maximum, in
+// Merges the per-part statistics of query qt of sequence b (visual and text
+// rows, kept apart by the context pass) for every head of selection row u of
+// the query (heads [u Hq/U, (u+1) Hq/U)) onto the head's maximum, in
 // double with fixed-order reductions, by a kSelThreads block (every thread
 // calls it; two block barriers). Every head gets a group of lanes (a power of
 // two, lanes_per_head of the row's head count; one round of heads since Hq <= kSelThreads) that
@@ -58,7 +58,7 @@ __device__ __forceinline__ int lanes_per_head(int Hq, int nparts) {
 // loads), and the maximum and the sums then come from registers; more parts
 // take two sweeps with the same arithmetic order. The head mean and head max
 // over the row's heads are summed by one wave in a fixed order.
-// L is the sequence's clamped length. Fills `hs` for the row's heads; with
+// L is the sequence's clamped length. Fills `hs` (by head index) for the row's heads; with
 // `write_out` also writes their m^vis_{t,h} (mass_head), per-head (max, Eq. (2)
 // normaliser) (head) and the row's (M_vis, M_vis,max) (mass_seq).
 namespace detail {
@@ -111,8 +111,8 @@ __device__ __forceinline__ void sum_parts(double& Ls, double& Lm, double& Vm, co
 }  // namespace detail
 
 template <typename Between>
-__device__ __forceinline__ void reduce_heads(const MassArgs& a, int b, int u, int L, int tid, const HeadLds& hs,
-                                             bool write_out, Between between) {
+__device__ __forceinline__ void reduce_heads(const MassArgs& a, int b, int qt, int u, int L, int tid,
+                                             const HeadLds& hs, bool write_out, Between between) {
   using namespace detail;
   const int Hu = a.Hq / a.U;  // heads of the row
   const int h0 = u * Hu;
@@ -120,9 +120,11 @@ __device__ __forceinline__ void reduce_heads(const MassArgs& a, int b, int u, in
   const int sub = tid % lph;
   const bool on = tid / lph < Hu;
   const int h = h0 + (on ? tid / lph : 0);
+  // the head's statistics and merged results sit at its virtual head for query qt
+  const size_t vh = static_cast<size_t>(b) * a.T * a.Hq + vhead(h, qt, a.G, a.T);
   constexpr int U = kPartsPerLane;
   // per part: [0] visual {m, Ls, Lm, -}, [1] text {m, l, Lm, Ls}
-  const float4* st = reinterpret_cast<const float4*>(a.stats + (static_cast<size_t>(b) * a.Hq + h) * a.nparts * 8);
+  const float4* st = reinterpret_cast<const float4*>(a.stats + vh * a.nparts * 8);
   const bool one_round = a.nparts <= U * lph;
   float4 v[U], t[U];
   if (one_round) load_parts(v, t, st, on, sub, lph, a.nparts);
@@ -155,8 +157,8 @@ __device__ __forceinline__ void reduce_heads(const MassArgs& a, int b, int u, in
     hs.hinv[h] = ls > 0.f ? 1.0f / ls : 0.f;
     hs.mass[h] = mass;
     if (write_out) {
-      a.mass_head[static_cast<size_t>(b) * a.Hq + h] = static_cast<float>(mass);
-      *reinterpret_cast<float2*>(a.head + (static_cast<size_t>(b) * a.Hq + h) * 2) = make_float2(m, ls);
+      a.mass_head[(static_cast<size_t>(b) * a.T + qt) * a.Hq + h] = static_cast<float>(mass);
+      *reinterpret_cast<float2*>(a.head + vh * 2) = make_float2(m, ls);
     }
   }
   __syncthreads();
@@ -176,7 +178,7 @@ __device__ __forceinline__ void reduce_heads(const MassArgs& a, int b, int u, in
       hs.mseq[0] = mv;
       hs.mseq[1] = mx;
       if (write_out) {
-        const size_t row = static_cast<size_t>(b) * a.U + u;
+        const size_t row = (static_cast<size_t>(b) * a.T + qt) * a.U + u;
         a.mass_seq[2 * row + 0] = mv;
         a.mass_seq[2 * row + 1] = mx;
       }
@@ -204,11 +206,12 @@ __host__ __device__ inline int score_lanes(int Hkv) {
   return ng;
 }
 
-// p plus the score terms of one KV group's G heads for one token, from its
-// spill row (GP floats, 16-byte aligned); hm/hinv point at the group's first head
+// p plus the score terms of one KV group's G heads of query t for one token,
+// from its spill row (GP floats, 16-byte aligned; the query's heads are
+// columns o .. o + G - 1, o = t*G); hm/hinv point at the group's first head
 template <int GP>
-__device__ __forceinline__ float group_terms(float p, const float* row, int G, const float* hm, const float* hinv,
-                                             float inv_tau) {
+__device__ __forceinline__ float group_terms(float p, const float* row, int G, int o, const float* hm,
+                                             const float* hinv, float inv_tau) {
   float z[GP];
 #pragma unroll
   for (int q = 0; q < GP / 4; ++q) {
@@ -220,18 +223,18 @@ __device__ __forceinline__ float group_terms(float p, const float* row, int G, c
   }
 #pragma unroll
   for (int j = 0; j < GP; ++j)
-    if (j < G) p = score_term(p, z[j], hm[j], hinv[j], inv_tau);
+    if (j >= o && j < o + G) p = score_term(p, z[j], hm[j - o], hinv[j - o], inv_tau);
   return p;
 }
 
 // ---------------------------------------------------------------------------
 // Eq. (2) score of the visual token at cache position pos of sequence b for
-// selection row u, by one thread (the same order as the select kernel's lanes):
+// query t's selection row u, by one thread (the same order as the select kernel's lanes):
 // S = (1/Hu) sum_h 2^((z_h - m_h) / tau_score) / Ls_h over the row's heads,
 // from the spilled logits. hm/hinv: per-head max and 1/Ls (by head index).
 // ---------------------------------------------------------------------------
 template <int GP>
-__device__ __forceinline__ float token_score_gp(const MassArgs& a, int b, int u, int pos, const float* hm,
+__device__ __forceinline__ float token_score_gp(const MassArgs& a, int b, int t, int u, int pos, const float* hm,
                                                 const float* hinv) {
   const float* zb = a.zs + static_cast<size_t>(b) * a.Hkv * a.zs_rows * GP + static_cast<size_t>(pos) * GP;
   const int Gu = a.Hkv / a.U;
@@ -241,15 +244,15 @@ __device__ __forceinline__ float token_score_gp(const MassArgs& a, int b, int u,
   for (int l = 0; l < ng; ++l) {
     float p = 0.f;
     for (int g = g0 + l; g < g0 + Gu; g += ng)
-      p = group_terms<GP>(p, zb + static_cast<size_t>(g) * a.zs_rows * GP, a.G, hm + g * a.G, hinv + g * a.G,
-                          a.inv_tau_s);
+      p = group_terms<GP>(p, zb + static_cast<size_t>(g) * a.zs_rows * GP, a.G, t * a.G, hm + g * a.G,
+                          hinv + g * a.G, a.inv_tau_s);
     total = l == 0 ? p : total + p;
   }
   return total / static_cast<float>(a.Hq / a.U);
 }
-__device__ __forceinline__ float token_score(const MassArgs& a, int b, int u, int pos, const float* hm,
+__device__ __forceinline__ float token_score(const MassArgs& a, int b, int t, int u, int pos, const float* hm,
                                              const float* hinv) {
-  return a.zs_gp == 8 ? token_score_gp<8>(a, b, u, pos, hm, hinv) : token_score_gp<16>(a, b, u, pos, hm, hinv);
+  return a.zs_gp == 8 ? token_score_gp<8>(a, b, t, u, pos, hm, hinv) : token_score_gp<16>(a, b, t, u, pos, hm, hinv);
 }
 
 // ---------------------------------------------------------------------------

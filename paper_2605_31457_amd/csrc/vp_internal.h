@@ -14,6 +14,15 @@ constexpr int kMaxHq_ = 1024;  // query heads supported
 // bytes of one sequence's segment table (SegTable: 256 starts, 256 ends, 257 ranks, count; 16-byte aligned)
 constexpr size_t kSegTableBytes = 3088;
 
+// Several queries per sequence (T >= 1): the T*G query rows that read one KV
+// head are "virtual heads" of that KV head, in the order (query t, head j of
+// the group), so one pass over a KV head's rows serves all of them. Per-head
+// workspace arrays are indexed by virtual head: b*T*Hq + g*T*G + t*G + j.
+__host__ __device__ inline int vhead(int h, int t, int G, int T) { return (h / G) * (T * G) + t * G + h % G; }
+// positions visible as visual to the queries of a sequence of length L: the
+// last T - 1 positions are the other queries' tokens (text)
+__host__ __device__ inline int vis_len(int L, int T) { return L - T + 1 > 0 ? L - T + 1 : 0; }
+
 // Work decomposition and workspace carving, a pure function of the shape.
 struct Plan {
   int nparts;   // context-pass work-groups per (sequence, KV head); part p takes
@@ -23,13 +32,13 @@ struct Plan {
   int zs_rows;    // rows per spill plane: max_seq_len rounded up to 32
   int zs_gp;      // floats per spill row: the query group padded to 8 or 16
   size_t zs;      // float [B][Hkv][zs_rows][zs_gp]  visual logits (log2 domain) by cache position
-  size_t stats;   // float [B][Hq][nparts][8]   per-part statistics: visual rows
+  size_t stats;   // float [B][T*Hq][nparts][8] per-part statistics (by virtual head): visual rows
                   //   {m_v, Ls_v, Lm_v, -}, text rows {m_t, l_t, Lm_t, Ls_t}
-  size_t acc;     // float [B][Hq][nparts][d]   per-part text value partials
-  size_t head;    // float [B][Hq][2]           merged (max, score normaliser)
-  size_t kstats;  // float [B][Hq][nsplit][2]   kept-row (max, sum)
-  size_t kacc;    // float [B][Hq][nsplit][d]   kept-row value partials
-  size_t sync;    // uint32 [B][U]              select-kernel arrival counters (per selection row)
+  size_t acc;     // float [B][T*Hq][nparts][d] per-part text value partials
+  size_t head;    // float [B][T*Hq][2]         merged (max, score normaliser)
+  size_t kstats;  // float [B][T*Hq][nsplit][2] kept-row (max, sum)
+  size_t kacc;    // float [B][T*Hq][nsplit][d] kept-row value partials
+  size_t sync;    // uint32 [B][T][U]           select-kernel arrival counters (per selection row)
   size_t segtab;  // SegTable [B]               clipped segment tables (positions, ranks)
   int sel_chunk;  // visual ranks scored per select work-group
   int sel_chunks; // select work-groups per selection row
@@ -63,7 +72,8 @@ struct AttendArgs {
   const int32_t* seg_off;
   const int32_t* seg;
   int B, Hq, Hkv, G, max_seq_len, max_vis;
-  int U;                // selection rows per sequence: 1, or Hkv (one per KV group)
+  int T;                // queries per sequence (q, out: [B][T][Hq][d])
+  int U;                // selection rows per query: 1, or Hkv (one per KV group)
   float zscale;         // sm_scale * log2(e)
   float inv_tau_m;      // 1 / tau_mass
   float inv_tau_s;      // 1 / tau_score
@@ -80,7 +90,7 @@ struct AttendArgs {
   int k_cap, split, nsplit;
   float* kstats;
   float* kacc;
-  uint32_t* sync;       // [B][U] arrival counters of the select kernel (may be null)
+  uint32_t* sync;       // [B][T][U] arrival counters of the select kernel (may be null)
   void* segtab;         // [B] segment tables (SegTable) for the select kernel (may be null)
 };
 
@@ -97,8 +107,9 @@ struct MassArgs {
   const int32_t* seg_off;
   const int32_t* seg;
   int B, Hq, Hkv, G, max_seq_len, max_vis, nparts, zs_rows, zs_gp;
-  int U;  // selection rows per sequence (1 or Hkv); row b*U + u covers query heads
-          // [u Hq/U, (u+1) Hq/U) and KV groups [u Hkv/U, (u+1) Hkv/U)
+  int T;  // queries per sequence
+  int U;  // selection rows per query (1 or Hkv); row (b*T + t)*U + u covers query t's
+          // heads [u Hq/U, (u+1) Hq/U) and KV groups [u Hkv/U, (u+1) Hkv/U)
   float inv_tau_m, inv_tau_s;
   const float* stats;
   const float* zs;
@@ -112,7 +123,7 @@ hipError_t launch_mass_finalize(const MassArgs& a, hipStream_t st);
 hipError_t launch_scores(const MassArgs& a, hipStream_t st);
 
 // Everything between the context pass and the kept-row pass of a decode step
-// (mass reduction, scores, budget, top-k) in one launch: grid (nchunks, B*U).
+// (mass reduction, scores, budget, top-k) in one launch: grid (nchunks, B*T*U).
 constexpr int kMaxSelectHeads = 1024;
 struct SelectArgs {
   MassArgs m;
@@ -122,7 +133,7 @@ struct SelectArgs {
   int32_t* vis_idx;
   int chunk;       // visual ranks scored per work-group
   int nchunks;     // work-groups per selection row
-  uint32_t* sync;  // [B*U] arrival counters (nchunks > 1), zeroed by the context pass
+  uint32_t* sync;  // [B*T*U] arrival counters (nchunks > 1), zeroed by the context pass
   const void* segtab;  // [B] segment tables written by the context pass
 };
 
@@ -135,7 +146,7 @@ struct BudgetArgs {
   const int32_t* seq_len;
   const int32_t* seg_off;
   const int32_t* seg;
-  int B, U, max_seq_len;
+  int B, R, T, max_seq_len;  // R: selection rows per sequence (T*U); row b*R + r
   int r_lo_bp, r_hi_bp, clamp;
   const float* mass_seq;
   int32_t* k;
@@ -147,7 +158,7 @@ struct TopkArgs {
   const int32_t* seq_len;
   const int32_t* seg_off;
   const int32_t* seg;
-  int B, U, max_seq_len, max_vis, k_cap;
+  int B, R, T, max_seq_len, max_vis, k_cap;  // R: selection rows per sequence
   const float* scores;
   const int32_t* k;
   int32_t* vis_idx;
@@ -164,7 +175,7 @@ struct TopPArgs {
   const int32_t* seq_len;
   const int32_t* seg_off;
   const int32_t* seg;
-  int B, U, max_seq_len, max_vis;
+  int B, R, T, max_seq_len, max_vis;  // R: selection rows per sequence
   float p;
   const float* scores;
   int32_t* k;
@@ -175,7 +186,7 @@ hipError_t launch_top_p(const TopPArgs& a, hipStream_t st);
 struct MergeArgs {
   const int32_t* seq_len;
   const int32_t* kk;
-  int B, Hq, U, max_seq_len, k_cap, nparts, split, nsplit, dtype;
+  int B, Hq, G, T, U, max_seq_len, k_cap, nparts, split, nsplit, dtype;
   const float* stats;
   const float* acc;
   const float* kstats;

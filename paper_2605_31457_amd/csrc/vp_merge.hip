@@ -1,9 +1,9 @@
 // Split-K reduction of the pruned attention (Sec. 4.1/4.2): merges the text
 // partials of the context pass (one per context-pass part) and the kept-row partials
-// (one per split of the kept list) of every (sequence, query head):
+// (one per split of the kept list) of every (sequence, query, query head):
 //   out = sum_i 2^(m_i - M) acc_i / sum_i 2^(m_i - M) l_i,  M = max_i m_i,
 // over the partials with l_i > 0; an empty context gives zeros.
-// grid = (Hq, B); 256 threads = (D/4 float4 columns) x R partial lanes, so the
+// grid = (T*Hq, B); 256 threads = (D/4 float4 columns) x R partial lanes, so the
 // partials are read in parallel (R at a time, each row as coalesced float4s)
 // rather than one after another.
 #include "vp_common.h"
@@ -21,7 +21,9 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a)
   __shared__ float s_red[kMergeThreads / 64];
   __shared__ float4 s_num[R][COLS];
   __shared__ float s_den[R];
-  const int h = blockIdx.x;
+  const int x = blockIdx.x;  // t*Hq + h: query t, head h
+  const int qt = x / a.Hq;
+  const int h = x - qt * a.Hq;
   const int b = blockIdx.y;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -30,11 +32,12 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a)
   const int r = tid / COLS;
   const int L = clamp_len(a.seq_len[b], a.max_seq_len);
   const int nc = parts_used(L, a.nparts);
-  int kb = a.kk[static_cast<size_t>(b) * a.U + h / (a.Hq / a.U)];  // the head's selection row
+  int kb = a.kk[(static_cast<size_t>(b) * a.T + qt) * a.U + h / (a.Hq / a.U)];  // the head's selection row
   kb = kb < 0 ? 0 : (kb > a.k_cap ? a.k_cap : kb);
   const int ns = L > 0 ? (kb + a.split - 1) / a.split : 0;
   const int np = nc + ns;
-  const size_t bh = static_cast<size_t>(b) * a.Hq + h;
+  const size_t bh = static_cast<size_t>(b) * a.T * a.Hq + vhead(h, qt, a.G, a.T);  // partials: virtual head
+  const size_t ob = static_cast<size_t>(b) * a.T * a.Hq + x;  // out [B][T][Hq][D]
   const float* st = a.stats + bh * a.nparts * 8;
   const float* ks = a.kstats + bh * a.nsplit * 2;
   const float4* ac = reinterpret_cast<const float4*>(a.acc + bh * a.nparts * D) + col;
@@ -95,9 +98,9 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a)
       uint2 packed;
       packed.x = f32_to_bf16_bits(o.x) | (static_cast<uint32_t>(f32_to_bf16_bits(o.y)) << 16);
       packed.y = f32_to_bf16_bits(o.z) | (static_cast<uint32_t>(f32_to_bf16_bits(o.w)) << 16);
-      reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + bh * D)[col] = packed;
+      reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + ob * D)[col] = packed;
     } else {
-      reinterpret_cast<float4*>(static_cast<float*>(a.out) + bh * D)[col] = o;
+      reinterpret_cast<float4*>(static_cast<float*>(a.out) + ob * D)[col] = o;
     }
   }
 }
@@ -105,7 +108,7 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a)
 }  // namespace
 
 hipError_t launch_merge(const MergeArgs& a, int head_dim, hipStream_t st) {
-  const dim3 grid(a.Hq, a.B);
+  const dim3 grid(a.T * a.Hq, a.B);
   if (head_dim == 128)
     hipLaunchKernelGGL(merge_kernel<128>, grid, dim3(kMergeThreads), 0, st, a);
   else if (head_dim == 64)

@@ -3,8 +3,9 @@
 // head max (Sec. 4.3), the Eq. (2) score of every visual token (Sec. 4.2), the
 // Eq. (7) budget with the Sec. 5.2 clamp and the Eq. (3) top-k.
 //
-// grid = (chunks, B*U), 1024 threads per work-group, one row of work-groups per
-// selection row (b, u): the sequence (U = 1), or one KV group of it (U = Hkv).
+// grid = (chunks, B*T*U), 1024 threads per work-group, one row of work-groups per
+// selection row (b, t, u): query t of the sequence (U = 1), or one KV group of
+// it (U = Hkv).
 // Work-group c of row (b, u) reduces the per-part statistics of the row's heads
 // (every work-group of the row does, so none waits for another), scores the
 // visual ranks [c * chunk, (c + 1) * chunk) from the spilled logits and writes
@@ -36,7 +37,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
   const MassArgs& a = t.m;
   const int c = blockIdx.x;
   const int row = blockIdx.y;
-  const int b = row / a.U;
+  const int b = row / (a.T * a.U);
+  const int qt = (row / a.U) % a.T;  // query of the row
   const int u = row % a.U;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -49,7 +51,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
 
   // ---- per-head statistics; wave 0 builds the segment table while the
   // statistics are in flight (the reduction's barriers publish it) ----
-  reduce_heads(a, b, u, L, tid, hs, c == 0, [&] {
+  reduce_heads(a, b, qt, u, L, tid, hs, c == 0, [&] {
     if (wid == 0) {
       // the context pass left the clipped table in the workspace: one round of loads
       const uint4* src = reinterpret_cast<const uint4*>(static_cast<const SegTable*>(t.segtab) + b);
@@ -87,7 +89,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
     const int pos = ok ? rank_to_pos(tab, i) : 0;
     float p = 0.f;
     for (int g = g0 + l; g < g0 + Gu; g += ng)
-      p = group_terms<GP>(p, zb + (static_cast<size_t>(g) * a.zs_rows + pos) * GP, a.G, hs.hm + g * a.G,
+      p = group_terms<GP>(p, zb + (static_cast<size_t>(g) * a.zs_rows + pos) * GP, a.G, qt * a.G, hs.hm + g * a.G,
                           hs.hinv + g * a.G, a.inv_tau_s);
     float total = p;
     for (int j = 1; j < ng; ++j) total = total + __shfl(p, (lane & ~(ng - 1)) + j);
@@ -179,7 +181,8 @@ hipError_t launch_gp(const SelectArgs& t, hipStream_t st) {
   // one chunk keeps its keys in LDS: the launch plan guarantees they fit
   if (t.nchunks == 1 && keys < t.m.max_vis) return hipErrorInvalidValue;
   const size_t dyn = static_cast<size_t>(head_lds_bytes(t.m.Hq)) + static_cast<size_t>(keys) * 4;
-  hipLaunchKernelGGL((select_kernel<GP>), dim3(t.nchunks, t.m.B * t.m.U), dim3(kSelThreads), dyn, st, t, keys);
+  hipLaunchKernelGGL((select_kernel<GP>), dim3(t.nchunks, t.m.B * t.m.T * t.m.U), dim3(kSelThreads), dyn, st, t,
+                     keys);
   return hipGetLastError();
 }
 

@@ -30,11 +30,11 @@ __global__ __launch_bounds__(kSelThreads) void topk_kernel(const TopkArgs a, int
   __shared__ SegTable tab;
 
   const int row = blockIdx.x;  // selection row of sequence b
-  const int b = row / a.U;
+  const int b = row / a.R;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wid = tid >> 6;
-  const int L = clamp_len(a.seq_len[b], a.max_seq_len);
+  const int L = vis_len(clamp_len(a.seq_len[b], a.max_seq_len), a.T);
   const int o0 = a.seg_off[b];
   if (wid == 0) load_segments(tab, a.seg + 2 * static_cast<long>(o0), a.seg_off[b + 1] - o0, L, lane);
   __syncthreads();
@@ -125,11 +125,11 @@ __global__ __launch_bounds__(kSelThreads) void top_p_kernel(const TopPArgs a, in
   __shared__ int s_above_c;
 
   const int row = blockIdx.x;  // selection row of sequence b
-  const int b = row / a.U;
+  const int b = row / a.R;
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wid = tid >> 6;
-  const int L = clamp_len(a.seq_len[b], a.max_seq_len);
+  const int L = vis_len(clamp_len(a.seq_len[b], a.max_seq_len), a.T);
   const int o0 = a.seg_off[b];
   if (wid == 0) load_segments(tab, a.seg + 2 * static_cast<long>(o0), a.seg_off[b + 1] - o0, L, lane);
   __syncthreads();
@@ -290,7 +290,7 @@ hipError_t launch_top_p(const TopPArgs& a, hipStream_t st) {
     return max(0, max_lds - stat - 64);
   }();
   const int keys = min(lds_room / 4, a.max_vis);
-  hipLaunchKernelGGL(top_p_kernel, dim3(a.B * a.U), dim3(kSelThreads), static_cast<size_t>(keys) * 4, st, a, keys);
+  hipLaunchKernelGGL(top_p_kernel, dim3(a.B * a.R), dim3(kSelThreads), static_cast<size_t>(keys) * 4, st, a, keys);
   return hipGetLastError();
 }
 
@@ -309,7 +309,7 @@ hipError_t launch_topk(const TopkArgs& a, hipStream_t st) {
     return max(0, max_lds - stat - 64);
   }();
   const int keys = min(lds_room / 4, a.max_vis);
-  hipLaunchKernelGGL(topk_kernel, dim3(a.B * a.U), dim3(kSelThreads), static_cast<size_t>(keys) * 4, st, a, keys);
+  hipLaunchKernelGGL(topk_kernel, dim3(a.B * a.R), dim3(kSelThreads), static_cast<size_t>(keys) * 4, st, a, keys);
   return hipGetLastError();
 }
 

@@ -52,13 +52,17 @@ class DeviceStep:
 
     ``kv_groups``: one budget and kept set per KV group (VP_SCOPE_KV_GROUP);
     results() then returns mass_seq [B, Hkv, 2], scores [B, Hkv, max_vis],
-    k [B, Hkv] and vis_idx [B, Hkv, k_cap].
+    k [B, Hkv] and vis_idx [B, Hkv, k_cap]. A workload whose q is
+    [B, T, Hq, d] runs T queries per sequence (n_queries = T); results() then
+    has a query axis after the batch axis (mass_head [B, T, Hq], out
+    [B, T, Hq, d], k [B, T] or [B, T, Hkv], ...).
     """
 
     def __init__(self, w: Workload, device="cuda:0", k_cap: int | None = None, max_vis: int | None = None,
                  kv=None, block_size: int = 0, block_seed: int = 0, kv_groups: bool = False):
         self.w = w
-        self.rows = w.Hkv if kv_groups else 1
+        self.T = w.q.shape[1] if w.q.ndim == 4 else 1
+        self.rows = w.Hkv if kv_groups else 1  # selection rows per query
         self.device = torch.device(device)
         self.q = _dev(w.q, self.device)
         self.block_size = block_size
@@ -90,19 +94,21 @@ class DeviceStep:
                                  max_seq_len=w.S_cap, max_vis=self.max_vis, max_segs=w.max_segs,
                                  k_cap=self.k_cap, block_size=block_size,
                                  scope=vp.VP_SCOPE_KV_GROUP if kv_groups else vp.VP_SCOPE_SEQUENCE,
+                                 n_queries=self.T,
                                  kv_stride_b=st[0], kv_stride_h=st[1], kv_stride_s=st[2])
         self.layout = vp.vp_layout(seq_len=self.seq_len.data_ptr(), vis_seg_off=self.seg_off.data_ptr(),
                                    vis_seg=self.seg.data_ptr(),
                                    block_table=self.block_table.data_ptr() if block_size else None)
         f32 = dict(dtype=torch.float32, device=self.device)
         i32 = dict(dtype=torch.int32, device=self.device)
-        self.mass_head = torch.zeros(B, Hq, **f32)
-        R = B * self.rows  # selection rows
+        T = self.T
+        self.mass_head = torch.zeros(B * T, Hq, **f32)
+        R = B * T * self.rows  # selection rows
         self.mass_seq = torch.zeros(R, 2, **f32)
         self.scores = torch.zeros(R, self.max_vis, **f32)
         self.k = torch.zeros(R, **i32)
         self.vis_idx = torch.full((R, self.k_cap), -7, **i32)
-        self.out = torch.zeros(B, Hq, d, dtype=self.q.dtype, device=self.device)
+        self.out = torch.zeros(B * T, Hq, d, dtype=self.q.dtype, device=self.device)
         self.ws_bytes = vp.vp_workspace_size(self.shape)
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=self.device)
 
@@ -135,8 +141,11 @@ class DeviceStep:
 
     def results(self) -> dict:
         torch.cuda.synchronize(self.device)
-        out = self.out.float().cpu().numpy()
-        lead = (self.w.B, self.rows) if self.rows > 1 else (self.w.B,)
+        B, T = self.w.B, self.T
+        qlead = (B, T) if T > 1 else (B,)
+        lead = qlead + ((self.rows,) if self.rows > 1 else ())
         rows = lambda t: t.cpu().numpy().reshape(lead + tuple(t.shape[1:]))
-        return dict(mass_head=self.mass_head.cpu().numpy(), mass_seq=rows(self.mass_seq),
-                    scores=rows(self.scores), k=rows(self.k), vis_idx=rows(self.vis_idx), out=out)
+        per_query = lambda t: t.cpu().numpy().reshape(qlead + tuple(t.shape[1:]))
+        return dict(mass_head=per_query(self.mass_head), mass_seq=rows(self.mass_seq),
+                    scores=rows(self.scores), k=rows(self.k), vis_idx=rows(self.vis_idx),
+                    out=per_query(self.out.float()))

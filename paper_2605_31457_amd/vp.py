@@ -32,7 +32,7 @@ class vp_shape(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32),
                 ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32), ("max_seq_len", ctypes.c_int32),
                 ("max_vis", ctypes.c_int32), ("max_segs", ctypes.c_int32), ("k_cap", ctypes.c_int32),
-                ("block_size", ctypes.c_int32), ("scope", ctypes.c_int32), ("reserved", ctypes.c_int32),
+                ("block_size", ctypes.c_int32), ("scope", ctypes.c_int32), ("n_queries", ctypes.c_int32),
                 ("kv_stride_b", ctypes.c_int64), ("kv_stride_h", ctypes.c_int64),
                 ("kv_stride_s", ctypes.c_int64)]
 

@@ -53,7 +53,7 @@ def test_struct_layout_matches_header(L):
     assert ctypes.sizeof(vp.vp_shape) == 72 and vp.vp_shape.kv_stride_b.offset == 48
     assert ctypes.sizeof(vp.vp_params) == 24 and ctypes.sizeof(vp.vp_layout) == 32
     assert vp.vp_shape.block_size.offset == 36 and vp.vp_layout.block_table.offset == 24
-    assert vp.vp_shape.scope.offset == 40 and vp.vp_shape.reserved.offset == 44
+    assert vp.vp_shape.scope.offset == 40 and vp.vp_shape.n_queries.offset == 44
 
 
 def test_workspace_size_is_pure_and_scales(L):
@@ -80,7 +80,9 @@ def test_workspace_size_is_pure_and_scales(L):
     (dict(max_segs=1000), "VP_ERR_UNSUPPORTED"),
     (dict(scope=2), "VP_ERR_RANGE"),
     (dict(scope=-1), "VP_ERR_RANGE"),
-    (dict(reserved=1), "VP_ERR_RANGE"),
+    (dict(n_queries=-1), "VP_ERR_RANGE"),
+    (dict(n_queries=3), "VP_ERR_UNSUPPORTED"),  # 3 queries x 7 heads > 16 rows per KV head
+    (dict(n_queries=17, n_q_heads=4, n_kv_heads=4), "VP_ERR_UNSUPPORTED"),
     (dict(scope=1, batch=20000), "VP_ERR_UNSUPPORTED"),  # 80000 selection rows
 ])
 def test_shape_validation(L, kw, status):
@@ -95,6 +97,14 @@ def test_kv_group_scope_sizes_the_arrival_counters(L):
     a = vp.vp_workspace_size(_shape(batch=64))
     b = vp.vp_workspace_size(_shape(batch=64, scope=vp.VP_SCOPE_KV_GROUP))
     assert a <= b <= a + 1024
+
+
+def test_queries_scale_the_per_head_workspace(L):
+    """T queries: per-head partials for T*Hq query rows; n_queries 0 and 1 agree."""
+    one = vp.vp_workspace_size(_shape())
+    assert vp.vp_workspace_size(_shape(n_queries=1)) == one
+    two = vp.vp_workspace_size(_shape(n_queries=2))
+    assert one < two < 2 * one + 4096
 
 
 def _layout():
