@@ -63,7 +63,7 @@ class Hip:
         return t.value
 
 
-def algorithmic_bytes(w, ks, lens=None, rows=1):
+def algorithmic_bytes(w, ks, lens=None, rows=1, kv_per_row=None):
     """Bytes the method must move at least once per step, by kernel.
 
     Visual pass: the K rows of visual tokens (their Eq. (6) logits). Text pass:
@@ -71,7 +71,9 @@ def algorithmic_bytes(w, ks, lens=None, rows=1):
     visual tokens. q, outputs, scores and indices are < 1% and not counted.
     lens: per-step sequence lengths of a decode loop (same for every sequence);
     the figures are then averages over its steps. rows: selection rows per
-    sequence (Hkv with per-KV-group budgets: KV head g reads its own k_g rows)."""
+    sequence (T queries x (1, or Hkv with per-KV-group budgets)); kv_per_row:
+    the KV heads whose kept rows a selection row's list names (Hkv, or 1)."""
+    kv_per_row = w.Hkv if kv_per_row is None else kv_per_row
     esz = 2 if w.dtype == "bf16" else 4
     row = w.Hkv * w.d * esz
     vis = text = kept = 0
@@ -80,7 +82,7 @@ def algorithmic_bytes(w, ks, lens=None, rows=1):
         nv = sum(n for _, n in w.segments[b])
         vis += nv * row
         text += sum(2 * (L - nv) * row for L in Ls) / len(Ls)
-        kept += 2 * int(sum(ks[b * rows:(b + 1) * rows])) * row // rows  # a row covers Hkv/rows KV heads
+        kept += 2 * int(sum(ks[b * rows:(b + 1) * rows])) * w.d * esz * kv_per_row
     return {"visual": vis, "text": text, "kept": kept}
 
 
@@ -120,8 +122,11 @@ def cpu_baseline(w, budget_s: float, kv_groups: bool = False):
     n = 0
     while True:
         b = n % w.B
-        run = O.decode_step_sequence_kv_groups if kv_groups else O.decode_step_sequence
-        run(w.q[b], w.K[b], w.V[b], int(w.seq_len[b]), w.segments[b], p)
+        if w.q.ndim == 4:  # several queries per sequence
+            O.decode_step_queries(w.q[b], w.K[b], w.V[b], int(w.seq_len[b]), w.segments[b], p, kv_groups=kv_groups)
+        else:
+            run = O.decode_step_sequence_kv_groups if kv_groups else O.decode_step_sequence
+            run(w.q[b], w.K[b], w.V[b], int(w.seq_len[b]), w.segments[b], p)
         n += 1
         el = time.perf_counter() - t0
         if el >= budget_s and n >= 1:
@@ -185,7 +190,8 @@ def bench_layers(args, w, ds, bufs, loop, steps, warmup, sp, hip):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     ks = ds.k.cpu().numpy()
-    nb = algorithmic_bytes(w, ks, None if loop is None else loop[3], rows=ds.rows)
+    nb = algorithmic_bytes(w, ks, None if loop is None else loop[3], rows=ds.T * ds.rows,
+                           kv_per_row=w.Hkv // ds.rows)
     esz = 2 if w.dtype == "bf16" else 4
     row = w.Hkv * w.d * esz
     if args.dense:
@@ -225,6 +231,9 @@ def main():
     ap.add_argument("--paged", type=int, default=0, metavar="P",
                     help="paged KV caches: blocks of P rows (a power of two) dealt to physical blocks in a "
                          "seeded random order, addressed through a block table")
+    ap.add_argument("--queries", type=int, default=1, metavar="T",
+                    help="T queries per sequence in one step (speculative / multi-token decoding; configs 1-4): "
+                         "the last T positions are the queries, each a step of its own over its prefix")
     ap.add_argument("--kv-groups", action="store_true",
                     help="one budget and kept set per KV group (VP_SCOPE_KV_GROUP) instead of per sequence")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -256,6 +265,10 @@ def main():
         return
 
     cfg = args.config
+    if args.queries > 1 and cfg == 5:
+        print("bench.py --queries: configs 1-4 (the decode loop of config 5 runs one query per step)",
+              file=sys.stderr)
+        sys.exit(2)
     steps, warmup = DEFAULT_STEPS[cfg]
     steps = args.steps if args.steps is not None else steps
     warmup = args.warmup if args.warmup is not None else warmup
@@ -285,6 +298,8 @@ def main():
         loop = (stream5.steps, q_all, layouts, [stream5.base_len + t + 1 for t in range(stream5.steps)])
     else:
         w = W.generate(cfg)
+        if args.queries > 1:
+            w = W.with_queries(w, args.queries)
         ds = S.DeviceStep(w, block_size=args.paged, kv_groups=args.kv_groups)
     kv_bytes = ds.K.numel() * ds.K.element_size() * 2
     R = args.rotate or max(1, math.ceil(MALL_DEFEAT_BYTES / kv_bytes))
@@ -366,7 +381,8 @@ def main():
     if loop is None:
         assert np.array_equal(ds.k.cpu().numpy(), ks), "budget changed between warm-up and timed steps"
 
-    nb = algorithmic_bytes(w, ks, None if loop is None else loop[3], rows=ds.rows)
+    nb = algorithmic_bytes(w, ks, None if loop is None else loop[3], rows=ds.T * ds.rows,
+                           kv_per_row=w.Hkv // ds.rows)
     step_bytes = nb["visual"] + nb["text"] + nb["kept"]
     ms_per_step = wall * 1e3 / steps
     plan = vp.vp_step_plan(ds.shape, ds.params)
@@ -395,7 +411,8 @@ def main():
                    "tau_mass": w.tau_mass, "retention_clamp_bp": [w.r_lo_bp, w.r_hi_bp],
                    "kept_k": [int(x) for x in ks[:8]], "kv_rotation": R, "parallelism": "single GPU",
                    "kv_block_size": args.paged or None,
-                   "budget_scope": "per KV group" if args.kv_groups else "per sequence"},
+                   "budget_scope": "per KV group" if args.kv_groups else "per sequence",
+                   "queries_per_sequence": ds.T},
         "step_algorithmic_bytes": step_bytes,
         "step_achieved_GBps": step_gbs,
         "step_frac_of_peak": step_gbs / PEAK_HBM_GBS,
@@ -416,6 +433,7 @@ def main():
         "entry_point": "four calls" if args.calls else "vp_decode_step",
         "plan": {"one_context_launch": one_launch, "select_in_one_group": bool(plan & vp.VP_PLAN_FUSED_TAIL)},
     }
+    res["query_tokens_per_s"] = res["value"] * w.B * ds.T
     if not args.no_cpu_baseline:
         print("[bench] timing the fp64 reference on the host", file=sys.stderr, flush=True)
         res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, args.kv_groups)
