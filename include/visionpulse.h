@@ -22,8 +22,9 @@
  *           vp_workspace_size().
  * Streams.  `stream` is a hipStream_t (NULL = the legacy default stream). Every
  *           call only enqueues kernels on that stream and returns; none
- *           synchronises. k and the kept indices stay on the device, so a step
- *           never waits for the host.
+ *           synchronises (vp_validate_layout, a debug helper, excepted). k and
+ *           the kept indices stay on the device, so a step never waits for the
+ *           host.
  * Shapes.   q and out are [B, T, Hq, d] contiguous (T = 1 by default). K and V caches are addressed as
  *           base + b*kv_stride_b + h*kv_stride_h + s*kv_stride_s (elements) with
  *           the d elements of a row contiguous. Query head h reads KV head
@@ -297,6 +298,19 @@ vp_status vp_decode_step(const vp_shape* shape, const vp_layout* layout, const v
 #define VP_PLAN_ONE_CONTEXT_LAUNCH 1
 #define VP_PLAN_FUSED_TAIL 2
 vp_status vp_step_plan(const vp_shape* shape, const vp_params* params, int32_t* flags);
+
+/*
+ * vp_validate_layout -- debug and test helper: synchronises `stream`, copies the
+ * device-resident layout to the host and checks what the kernels otherwise
+ * trust (they only clip): 0 <= seq_len[b] <= max_seq_len; vis_seg_off
+ * non-decreasing from >= 0; at most max_segs segments per sequence, each of
+ * length >= 1, ascending, disjoint and inside [0, seq_len[b]); N_v <= max_vis;
+ * with paged caches, block ids >= 0 for every block a sequence uses (that an id
+ * addresses a block of the caller's caches is not checkable here). Returns
+ * VP_ERR_SHAPE naming the first violation (vp_last_error), VP_ERR_HIP if a copy
+ * fails. The only call that synchronises; not for the decode loop.
+ */
+vp_status vp_validate_layout(const vp_shape* shape, const vp_layout* layout, void* stream);
 
 /* Host mirror of vp_budget's rule for one sequence (pure; for callers that keep
  * the mass on the host). Returns -1 for invalid parameters. */

@@ -6,6 +6,7 @@
 #include <cstdio>
 #include <cstring>
 #include <string>
+#include <vector>
 
 #include "vp_internal.h"
 
@@ -447,6 +448,69 @@ vp_status vp_select_topk(const vp_shape* shape, const vp_layout* layout, const f
   if (!scores || !k || !vis_idx) return fail(VP_ERR_NULL, "scores, k, vis_idx required");
   if (hipError_t e = launch_topk(topk_args(shape, layout, scores, k, vis_idx), static_cast<hipStream_t>(stream)))
     return hip_fail(e, "top-k launch");
+  return VP_OK;
+}
+
+vp_status vp_validate_layout(const vp_shape* shape, const vp_layout* layout, void* stream) {
+  g_last_error.clear();
+  if (vp_status e = check_shape(shape)) return e;
+  if (vp_status e = check_layout(shape, layout)) return e;
+  const int B = shape->batch;
+  // the layout may have been written by work queued on the stream
+  if (hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream))) return hip_fail(e, "stream sync");
+  std::vector<int32_t> len(B), off(B + 1);
+  if (hipError_t e = hipMemcpy(len.data(), layout->seq_len, B * sizeof(int32_t), hipMemcpyDeviceToHost))
+    return hip_fail(e, "seq_len copy");
+  if (hipError_t e = hipMemcpy(off.data(), layout->vis_seg_off, (B + 1) * sizeof(int32_t), hipMemcpyDeviceToHost))
+    return hip_fail(e, "vis_seg_off copy");
+  if (off[0] < 0) return fail(VP_ERR_SHAPE, "vis_seg_off[0] = %d < 0", off[0]);
+  for (int b = 0; b < B; ++b)
+    if (off[b + 1] < off[b]) return fail(VP_ERR_SHAPE, "vis_seg_off decreases at sequence %d", b);
+  std::vector<int32_t> seg(2 * static_cast<size_t>(off[B]) + 2);
+  if (off[B] > 0) {
+    if (hipError_t e = hipMemcpy(seg.data(), layout->vis_seg, 2 * static_cast<size_t>(off[B]) * sizeof(int32_t),
+                                 hipMemcpyDeviceToHost))
+      return hip_fail(e, "vis_seg copy");
+  }
+  std::vector<int32_t> table;
+  int64_t nblk = 0;
+  if (shape->block_size > 0) {
+    nblk = (shape->max_seq_len + shape->block_size - 1) / shape->block_size;
+    table.resize(static_cast<size_t>(B) * nblk);
+    if (hipError_t e = hipMemcpy(table.data(), layout->block_table, table.size() * sizeof(int32_t),
+                                 hipMemcpyDeviceToHost))
+      return hip_fail(e, "block_table copy");
+  }
+  for (int b = 0; b < B; ++b) {
+    const int L = len[b];
+    if (L < 0 || L > shape->max_seq_len)
+      return fail(VP_ERR_SHAPE, "sequence %d: seq_len %d outside [0, max_seq_len %d]", b, L, shape->max_seq_len);
+    const int n = off[b + 1] - off[b];
+    if (n > shape->max_segs) return fail(VP_ERR_SHAPE, "sequence %d: %d segments > max_segs %d", b, n, shape->max_segs);
+    int64_t end = 0, nv = 0;
+    for (int i = off[b]; i < off[b + 1]; ++i) {
+      const int st = seg[2 * static_cast<size_t>(i)], ln = seg[2 * static_cast<size_t>(i) + 1];
+      if (ln < 1) return fail(VP_ERR_SHAPE, "sequence %d: segment %d has length %d < 1", b, i - off[b], ln);
+      if (st < end)
+        return fail(VP_ERR_SHAPE, "sequence %d: segment %d starts at %d, before the previous end %lld", b,
+                    i - off[b], st, static_cast<long long>(end));
+      if (static_cast<int64_t>(st) + ln > L)
+        return fail(VP_ERR_SHAPE, "sequence %d: segment %d [%d, %lld) ends past seq_len %d", b, i - off[b], st,
+                    static_cast<long long>(st) + ln, L);
+      end = static_cast<int64_t>(st) + ln;
+      nv += ln;
+    }
+    if (nv > shape->max_vis)
+      return fail(VP_ERR_SHAPE, "sequence %d: %lld visual tokens > max_vis %d", b, static_cast<long long>(nv),
+                  shape->max_vis);
+    if (shape->block_size > 0) {
+      const int64_t used = (L + shape->block_size - 1) / shape->block_size;
+      for (int64_t j = 0; j < used; ++j)
+        if (table[b * nblk + j] < 0)
+          return fail(VP_ERR_SHAPE, "sequence %d: block_table entry %lld is %d < 0", b, static_cast<long long>(j),
+                      table[b * nblk + j]);
+    }
+  }
   return VP_OK;
 }
 

@@ -72,6 +72,7 @@ def lib() -> ctypes.CDLL:
             "vp_sparse_decode_attn": ([P(vp_shape), P(vp_layout), P(vp_params), V, V, V, V, V, V,
                                        ctypes.c_int32, V, S, V], ctypes.c_int),
             "vp_budget_host": ([ctypes.c_double, ctypes.c_int32, P(vp_params)], ctypes.c_int32),
+            "vp_validate_layout": ([P(vp_shape), P(vp_layout), V], ctypes.c_int),
             "vp_decode_step": ([P(vp_shape), P(vp_layout), P(vp_params), V, V, V, V, V, V, V, V, V, V, S, V,
                                 ctypes.POINTER(V), ctypes.c_int32], ctypes.c_int),
         }
@@ -194,6 +195,12 @@ def vp_sparse_decode_attn(shape, layout, params, q, K, V, vis_idx, k, out, flags
     _check("vp_sparse_decode_attn", lib().vp_sparse_decode_attn(
         ctypes.byref(shape), ctypes.byref(layout), ctypes.byref(params), _p(q), _p(K), _p(V),
         _p(vis_idx), _p(k), _p(out), int(flags), _p(workspace), nbytes, _stream(stream)))
+
+
+def vp_validate_layout(shape, layout, stream=None):
+    """Debug helper: raises VPError naming the first problem of the device layout."""
+    _check("vp_validate_layout", lib().vp_validate_layout(ctypes.byref(shape), ctypes.byref(layout),
+                                                          _stream(stream)))
 
 
 def vp_budget_host(m_max: float, n_vis: int, params: vp_params) -> int:

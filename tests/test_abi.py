@@ -131,6 +131,8 @@ def test_calls_reject_nulls_and_bad_params_before_launch(L):
         vp.vp_select_topk(s, lay, fake, None, fake, 0)
     with pytest.raises(vp.VPError, match="VP_ERR_NULL"):
         vp.vp_select_topk(s, vp.vp_layout(seq_len=0x1000, vis_seg_off=None, vis_seg=0x3000), fake, fake, fake, 0)
+    with pytest.raises(vp.VPError, match="VP_ERR_NULL"):
+        vp.vp_validate_layout(s, vp.vp_layout(seq_len=None, vis_seg_off=0x2000, vis_seg=0x3000), 0)
     # paged caches need a block table
     with pytest.raises(vp.VPError, match="VP_ERR_NULL"):
         vp.vp_visual_mass(_shape(block_size=32), lay, p, fake, fake, None, fake, fake, fake, fake,
