@@ -179,6 +179,9 @@ AttendArgs attend_args(const vp_shape* s, const vp_layout* l, const vp_params* p
 #ifndef VP_TARGET_PARTS
 #define VP_TARGET_PARTS 2048
 #endif
+#ifndef VP_MIN_TILES
+#define VP_MIN_TILES 2  // 32-row tiles per context-pass part, at least
+#endif
 
 MassArgs mass_args(const vp_shape* s, const vp_layout* l, const Plan& plan, const AttendArgs& a, char* ws,
                    float* mass_head, float* mass_seq, float* scores) {
@@ -297,7 +300,7 @@ Plan make_plan(const vp_shape& s) {
   const int64_t pairs = static_cast<int64_t>(s.batch) * s.n_kv_heads;
   const int64_t tiles = (s.max_seq_len + 31) / 32;
   int64_t parts = (VP_TARGET_PARTS + pairs - 1) / pairs;
-  if (parts > (tiles + 1) / 2) parts = (tiles + 1) / 2;
+  if (parts > (tiles + VP_MIN_TILES - 1) / VP_MIN_TILES) parts = (tiles + VP_MIN_TILES - 1) / VP_MIN_TILES;
   if (parts < 1) parts = 1;
   p.nparts = static_cast<int>(parts);
   // Kept pass: 64 rows (two tiles) per work-group, or 32 when that leaves

@@ -13,6 +13,19 @@ namespace vp {
 namespace {
 
 constexpr int kMergeThreads = 256;
+constexpr int kHeld = 8;  // partials a lane group holds in registers (np <= kHeld * R)
+
+// maximum over the block (every thread gets it)
+__device__ __forceinline__ float block_max(float m, float* s_red, int lane, int wid) {
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) m = fmaxf(m, __shfl_xor(m, off));
+  if (lane == 0) s_red[wid] = m;
+  __syncthreads();
+  m = s_red[0];
+#pragma unroll
+  for (int v = 1; v < kMergeThreads / 64; ++v) m = fmaxf(m, s_red[v]);
+  return m;
+}
 
 template <int D>
 __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a) {
@@ -48,31 +61,56 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a)
                   : *reinterpret_cast<const float2*>(ks + (i - nc) * 2);
   };
 
-  float M = kNegInf;
-  for (int i = tid; i < np; i += kMergeThreads) {
-    const float2 v = ml(i);
-    if (v.y > 0.f) M = fmaxf(M, v.x);
-  }
-#pragma unroll
-  for (int off = 32; off > 0; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
-  if (lane == 0) s_red[wid] = M;
-  __syncthreads();
-  M = s_red[0];
-#pragma unroll
-  for (int v = 1; v < kMergeThreads / 64; ++v) M = fmaxf(M, s_red[v]);
-
   float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
   float den = 0.f;
+  if (np <= kHeld * R) {
+    // every partial of this lane group requested at once, value rows included;
+    // the maximum is then reduced and the registers rescaled (one round trip)
+    float2 v[kHeld];
+    float4 xv[kHeld];
+#pragma unroll
+    for (int j = 0; j < kHeld; ++j) {
+      const int i = r + j * R;
+      const bool ok = i < np;
+      const int ii = ok ? i : 0;  // an in-bounds slot; its values are not used
+      v[j] = ml(ii);
+      xv[j] = ii < nc ? ac[static_cast<size_t>(ii) * COLS] : ka[static_cast<size_t>(ii - nc) * COLS];
+      if (!ok) v[j] = make_float2(kNegInf, 0.f);
+    }
+    float M = kNegInf;
+#pragma unroll
+    for (int j = 0; j < kHeld; ++j)
+      if (v[j].y > 0.f) M = fmaxf(M, v[j].x);
+    M = block_max(M, s_red, lane, wid);
+#pragma unroll
+    for (int j = 0; j < kHeld; ++j) {
+      if (v[j].y > 0.f) {  // empty partials (and the unused slots) contribute nothing
+        const float w = fast_exp2(v[j].x - M);
+        den += w * v[j].y;
+        num.x += w * xv[j].x;
+        num.y += w * xv[j].y;
+        num.z += w * xv[j].z;
+        num.w += w * xv[j].w;
+      }
+    }
+  } else {
+    float M = kNegInf;
+    for (int i = tid; i < np; i += kMergeThreads) {
+      const float2 v = ml(i);
+      if (v.y > 0.f) M = fmaxf(M, v.x);
+    }
+    M = block_max(M, s_red, lane, wid);
 #pragma unroll 4
-  for (int i = r; i < np; i += R) {
-    const float2 v = ml(i);
-    const float w = v.y > 0.f ? fast_exp2(v.x - M) : 0.f;
-    const float4 x = i < nc ? ac[static_cast<size_t>(i) * COLS] : ka[static_cast<size_t>(i - nc) * COLS];
-    den += w * v.y;
-    num.x += w * x.x;
-    num.y += w * x.y;
-    num.z += w * x.z;
-    num.w += w * x.w;
+    for (int i = r; i < np; i += R) {
+      const float2 v = ml(i);
+      const float w = v.y > 0.f ? fast_exp2(v.x - M) : 0.f;
+      const float4 x = i < nc ? ac[static_cast<size_t>(i) * COLS] : ka[static_cast<size_t>(i - nc) * COLS];
+      den += w * v.y;
+      num.x += w * x.x;
+      num.y += w * x.y;
+      num.z += w * x.z;
+      num.w += w * x.w;
+    }
   }
   s_num[r][col] = num;
   if (col == 0) s_den[r] = den;

@@ -49,20 +49,17 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
   const int L = clamp_len(a.seq_len[b], a.max_seq_len);
   for (int i = tid; i < kHistWords; i += kSelThreads) sh.hist[i] = 0;
 
-  // ---- per-head statistics; wave 0 builds the segment table while the
+  // ---- per-head statistics; the segment table is copied in while the
   // statistics are in flight (the reduction's barriers publish it) ----
   reduce_heads(a, b, qt, u, L, tid, hs, c == 0, [&] {
-    if (wid == 0) {
-      // the context pass left the clipped table in the workspace: one round of loads
+    // the context pass left the clipped table in the workspace: one 16-byte
+    // load for every fourth thread, spread over the waves so that no wave
+    // waits on more than its own statistics and one load
+    constexpr int kWords = static_cast<int>(sizeof(SegTable) / 16);
+    static_assert(4 * kWords <= kSelThreads, "segment table copy");
+    if ((tid & 3) == 0 && (tid >> 2) < kWords) {
       const uint4* src = reinterpret_cast<const uint4*>(static_cast<const SegTable*>(t.segtab) + b);
-      uint4* dst = reinterpret_cast<uint4*>(&tab);
-      constexpr int kWords = static_cast<int>(sizeof(SegTable) / 16);
-      uint4 w[(kWords + 63) / 64];
-#pragma unroll
-      for (int j = 0; j < (kWords + 63) / 64; ++j) w[j] = src[min(j * 64 + lane, kWords - 1)];
-#pragma unroll
-      for (int j = 0; j < (kWords + 63) / 64; ++j)
-        if (j * 64 + lane < kWords) dst[j * 64 + lane] = w[j];
+      reinterpret_cast<uint4*>(&tab)[tid >> 2] = src[tid >> 2];
     }
   });
   const int nvis = tab.rk[tab.n];
