@@ -272,8 +272,13 @@ MergeArgs merge_args(const vp_shape* s, const vp_layout* l, const Plan& plan, co
 // Both context passes in one launch: saves a launch and overlaps the two
 // passes' latency chains where the cache is small; kept apart otherwise, so
 // the visual pass's logit writes stay out of the text pass's read stream.
+// Measured: the 8 x 10.5k batch of the 72B shape (22k tiles) gains 6 us from the
+// one launch with half the parts; the 64 x 32k batch (262k tiles) loses 100 us.
 #ifndef VP_DUAL_MAX_TILES
-#define VP_DUAL_MAX_TILES 4096  // 32-row tiles over the batch and KV heads
+#define VP_DUAL_MAX_TILES 32768  // 32-row tiles over the batch and KV heads
+#endif
+#ifndef VP_DUAL_PART_DIV
+#define VP_DUAL_PART_DIV 2  // parts of the one-launch context pass: VP_TARGET_PARTS / this
 #endif
 bool use_dual(const vp_shape* s) {
   const int64_t tiles = static_cast<int64_t>(s->batch) * s->n_kv_heads * ((s->max_seq_len + 31) / 32);
@@ -299,7 +304,9 @@ Plan make_plan(const vp_shape& s) {
   // XCDs only visual (K) or only text (K + V) rows.
   const int64_t pairs = static_cast<int64_t>(s.batch) * s.n_kv_heads;
   const int64_t tiles = (s.max_seq_len + 31) / 32;
-  int64_t parts = (VP_TARGET_PARTS + pairs - 1) / pairs;
+  // the one-launch context pass runs a visual and a text work-group per part
+  const int64_t target = use_dual(&s) ? VP_TARGET_PARTS / VP_DUAL_PART_DIV : VP_TARGET_PARTS;
+  int64_t parts = (target + pairs - 1) / pairs;
   if (parts > (tiles + VP_MIN_TILES - 1) / VP_MIN_TILES) parts = (tiles + VP_MIN_TILES - 1) / VP_MIN_TILES;
   if (parts < 1) parts = 1;
   p.nparts = static_cast<int>(parts);
