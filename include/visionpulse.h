@@ -177,14 +177,15 @@ vp_status vp_visual_mass(const vp_shape* shape, const vp_layout* layout, const v
 
 /*
  * vp_visual_mass_timed -- vp_visual_mass that also records caller-created HIP
- * events (hipEvent_t) on `stream` between its kernel launches, so a profiler or
- * benchmark can time each kernel alone with hipEventElapsedTime. events[i],
+ * events (hipEvent_t) on `stream` around its kernel launches, so a profiler or
+ * benchmark can time the kernels with hipEventElapsedTime. events[i],
  * i < n_events (at most VP_MASS_EVENTS; NULL entries are skipped), is recorded
- *   [0] before the visual pass      [1] after it, before the text pass
- *   [2] after the text pass         [3] after the mass reduction
- *   [4] after the scores kernel.
- * (With VP_PLAN_ONE_CONTEXT_LAUNCH and V given, [0] and [1] both precede the
- * one launch of both passes; see vp_step_plan.)
+ *   [0] before the visual pass
+ *   [1] when the text pass starts executing, [2] when it ends (both attached
+ *       to that launch, hipExtLaunchKernel: [1]..[2] is its execution alone)
+ *   [3] after the mass reduction    [4] after the scores kernel.
+ * (With VP_PLAN_ONE_CONTEXT_LAUNCH and V given, [1]..[2] is the one launch of
+ * both passes; see vp_step_plan.)
  * events may be NULL when n_events is 0. Results are identical to
  * vp_visual_mass. VP_ERR_RANGE if n_events is outside [0, VP_MASS_EVENTS].
  */
@@ -268,10 +269,11 @@ vp_status vp_sparse_decode_attn(const vp_shape* shape, const vp_layout* layout, 
  *
  * events: optional caller-created hipEvent_t recorded on `stream`, i < n_events
  * (at most VP_STEP_EVENTS; NULL entries skipped):
- *   [0] before the visual pass   [1] before the text pass
- *   [2] after the text pass      [3] before the kept-row pass
- *   (with VP_PLAN_ONE_CONTEXT_LAUNCH, [0] and [1] both precede that launch)
- *   [4] before the merge         [5] after the merge.
+ *   [0] before the visual pass
+ *   [1] when the text pass starts executing, [2] when it ends (attached to
+ *       that launch: [1]..[2] is its execution alone, as a profiler sees it;
+ *       with VP_PLAN_ONE_CONTEXT_LAUNCH, the one launch of both passes)
+ *   [3] before the kept-row pass  [4] before the merge  [5] after the merge.
  * Errors as for the four calls; VP_ERR_RANGE if n_events is outside
  * [0, VP_STEP_EVENTS]. The workspace must not be shared by concurrent calls.
  */
@@ -287,9 +289,8 @@ vp_status vp_decode_step(const vp_shape* shape, const vp_layout* layout, const v
  * their kernels for this shape (pure host computation; for profiling and
  * benchmarks). flags is a bit set of
  *   VP_PLAN_ONE_CONTEXT_LAUNCH  the visual and text passes share one launch
- *                               (small caches); events [0] and [1] are then
- *                               recorded together before it, so [1]..[2]
- *                               times the whole context pass;
+ *                               (small and mid-size caches); events [1]..[2]
+ *                               then time that whole launch;
  *   VP_PLAN_FUSED_TAIL          vp_decode_step's select launch scores and
  *                               selects each sequence in a single work-group
  *                               (small visual sets; otherwise in chunks, the

@@ -409,19 +409,19 @@ vp_status vp_visual_mass_timed(const vp_shape* shape, const vp_layout* layout, c
   auto mark = [&](int i) -> hipError_t {
     return (i < n_events && events[i]) ? hipEventRecord(static_cast<hipEvent_t>(events[i]), st) : hipSuccess;
   };
+  // events [1] and [2] ride on the text (or one) context launch: its execution alone
+  auto ev = [&](int i) -> hipEvent_t { return i < n_events ? static_cast<hipEvent_t>(events[i]) : nullptr; };
   if (hipError_t e = mark(0)) return hip_fail(e, "event record");
   if (V && use_dual(shape)) {
-    if (hipError_t e = mark(1)) return hip_fail(e, "event record");
-    if (hipError_t e = launch_attend(a, MODE_DUAL, shape->dtype, shape->head_dim, st))
+    if (hipError_t e = launch_attend(a, MODE_DUAL, shape->dtype, shape->head_dim, st, ev(1), ev(2)))
       return hip_fail(e, "context pass launch");
   } else {
     if (hipError_t e = launch_attend(a, MODE_VIS, shape->dtype, shape->head_dim, st))
       return hip_fail(e, "visual pass launch");
-    if (hipError_t e = mark(1)) return hip_fail(e, "event record");
-    if (hipError_t e = launch_attend(a, V ? MODE_TEXT_BOTH : MODE_TEXT_STATS, shape->dtype, shape->head_dim, st))
+    if (hipError_t e = launch_attend(a, V ? MODE_TEXT_BOTH : MODE_TEXT_STATS, shape->dtype, shape->head_dim, st, ev(1),
+                                     ev(2)))
       return hip_fail(e, "text pass launch");
   }
-  if (hipError_t e = mark(2)) return hip_fail(e, "event record");
   const MassArgs m = mass_args(shape, layout, plan, a, ws, mass_head, mass_seq, scores);
   if (hipError_t e = launch_mass_finalize(m, st)) return hip_fail(e, "mass finalize launch");
   if (hipError_t e = mark(3)) return hip_fail(e, "event record");
@@ -611,16 +611,15 @@ vp_status vp_decode_step(const vp_shape* shape, const vp_layout* layout, const v
     return (i < n_events && events[i]) ? hipEventRecord(static_cast<hipEvent_t>(events[i]), st) : hipSuccess;
   };
   const int dt = shape->dtype, hd = shape->head_dim;
+  // events [1] and [2] ride on the text (or one) context launch: its execution alone
+  auto ev = [&](int i) -> hipEvent_t { return i < n_events ? static_cast<hipEvent_t>(events[i]) : nullptr; };
   if (hipError_t e = mark(0)) return hip_fail(e, "event record");
   if (use_dual(shape)) {
-    if (hipError_t e = mark(1)) return hip_fail(e, "event record");
-    if (hipError_t e = launch_attend(a, MODE_DUAL, dt, hd, st)) return hip_fail(e, "context pass launch");
+    if (hipError_t e = launch_attend(a, MODE_DUAL, dt, hd, st, ev(1), ev(2))) return hip_fail(e, "context pass launch");
   } else {
     if (hipError_t e = launch_attend(a, MODE_VIS, dt, hd, st)) return hip_fail(e, "visual pass launch");
-    if (hipError_t e = mark(1)) return hip_fail(e, "event record");
-    if (hipError_t e = launch_attend(a, MODE_TEXT_BOTH, dt, hd, st)) return hip_fail(e, "text pass launch");
+    if (hipError_t e = launch_attend(a, MODE_TEXT_BOTH, dt, hd, st, ev(1), ev(2))) return hip_fail(e, "text pass launch");
   }
-  if (hipError_t e = mark(2)) return hip_fail(e, "event record");
   SelectArgs t{};
   t.m = mass_args(shape, layout, plan, a, ws, mass_head, mass_seq, scores);
   t.r_lo_bp = params->r_lo_bp;

@@ -60,6 +60,8 @@
 #include "vp_common.h"
 #include "vp_internal.h"
 
+#include <hip/hip_ext.h>
+
 #ifndef VP_ATTEND_WAVES
 #define VP_ATTEND_WAVES 2  // bf16 passes that read V
 #endif
@@ -730,48 +732,50 @@ attend_dual_kernel(const AttendArgs a) {
     step_setup(a, blockIdx.y, blockIdx.z);
 }
 
+// Launches one pass. With events given, they are attached to the launch itself
+// (hipExtLaunchKernel): they time the kernel's execution alone, as a profiler does.
+template <typename K>
+hipError_t launch_one(K kernel, dim3 grid, const AttendArgs& a, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
+  if (ev0 || ev1) {
+    void* args[1] = {const_cast<AttendArgs*>(&a)};
+    return hipExtLaunchKernel(reinterpret_cast<const void*>(kernel), grid, dim3(64), args, 0, st, ev0, ev1, 0);
+  }
+  hipLaunchKernelGGL(kernel, grid, dim3(64), 0, st, a);
+  return hipGetLastError();
+}
+
 template <int DT, int D, int PG>
-hipError_t launch_dd(const AttendArgs& a, int mode, hipStream_t st) {
+hipError_t launch_dd(const AttendArgs& a, int mode, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
   // launches with the visual role carry one more work-group per sequence (step_setup)
   const int gx = mode == MODE_KEPT ? a.nsplit
                                    : (mode == MODE_DUAL ? 2 * a.nparts + 1 : (mode == MODE_VIS ? a.nparts + 1 : a.nparts));
   const dim3 grid(gx, mode == MODE_KEPT ? a.Hkv * a.T : a.Hkv, a.B);
-  const dim3 block(64);
   switch (mode) {
-    case MODE_DUAL:
-      hipLaunchKernelGGL((attend_dual_kernel<DT, D, PG>), grid, block, 0, st, a);
-      break;
-    case MODE_VIS:
-      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_VIS | PG>), grid, block, 0, st, a);
-      break;
-    case MODE_TEXT_STATS:
-      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_TEXT_STATS | PG>), grid, block, 0, st, a);
-      break;
-    case MODE_TEXT_ATTN:
-      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_TEXT_ATTN | PG>), grid, block, 0, st, a);
-      break;
-    case MODE_TEXT_BOTH:
-      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_TEXT_BOTH | PG>), grid, block, 0, st, a);
-      break;
-    case MODE_KEPT:
-      hipLaunchKernelGGL((attend_kernel<DT, D, MODE_KEPT | PG>), grid, block, 0, st, a);
-      break;
-    default:
-      return hipErrorInvalidValue;
+    case MODE_DUAL: return launch_one(attend_dual_kernel<DT, D, PG>, grid, a, st, ev0, ev1);
+    case MODE_VIS: return launch_one(attend_kernel<DT, D, MODE_VIS | PG>, grid, a, st, ev0, ev1);
+    case MODE_TEXT_STATS: return launch_one(attend_kernel<DT, D, MODE_TEXT_STATS | PG>, grid, a, st, ev0, ev1);
+    case MODE_TEXT_ATTN: return launch_one(attend_kernel<DT, D, MODE_TEXT_ATTN | PG>, grid, a, st, ev0, ev1);
+    case MODE_TEXT_BOTH: return launch_one(attend_kernel<DT, D, MODE_TEXT_BOTH | PG>, grid, a, st, ev0, ev1);
+    case MODE_KEPT: return launch_one(attend_kernel<DT, D, MODE_KEPT | PG>, grid, a, st, ev0, ev1);
+    default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
 }
 
 }  // namespace
 
-hipError_t launch_attend(const AttendArgs& a, int mode, int dtype, int head_dim, hipStream_t st) {
+hipError_t launch_attend(const AttendArgs& a, int mode, int dtype, int head_dim, hipStream_t st, hipEvent_t ev0,
+                         hipEvent_t ev1) {
   const bool paged = a.bs_log2 >= 0;
   if (dtype == VP_BF16) {
-    if (head_dim == 128) return paged ? launch_dd<VP_BF16, 128, MODE_PAGED>(a, mode, st) : launch_dd<VP_BF16, 128, 0>(a, mode, st);
-    if (head_dim == 64) return paged ? launch_dd<VP_BF16, 64, MODE_PAGED>(a, mode, st) : launch_dd<VP_BF16, 64, 0>(a, mode, st);
+    if (head_dim == 128)
+      return paged ? launch_dd<VP_BF16, 128, MODE_PAGED>(a, mode, st, ev0, ev1) : launch_dd<VP_BF16, 128, 0>(a, mode, st, ev0, ev1);
+    if (head_dim == 64)
+      return paged ? launch_dd<VP_BF16, 64, MODE_PAGED>(a, mode, st, ev0, ev1) : launch_dd<VP_BF16, 64, 0>(a, mode, st, ev0, ev1);
   } else if (dtype == VP_F32) {
-    if (head_dim == 128) return paged ? launch_dd<VP_F32, 128, MODE_PAGED>(a, mode, st) : launch_dd<VP_F32, 128, 0>(a, mode, st);
-    if (head_dim == 64) return paged ? launch_dd<VP_F32, 64, MODE_PAGED>(a, mode, st) : launch_dd<VP_F32, 64, 0>(a, mode, st);
+    if (head_dim == 128)
+      return paged ? launch_dd<VP_F32, 128, MODE_PAGED>(a, mode, st, ev0, ev1) : launch_dd<VP_F32, 128, 0>(a, mode, st, ev0, ev1);
+    if (head_dim == 64)
+      return paged ? launch_dd<VP_F32, 64, MODE_PAGED>(a, mode, st, ev0, ev1) : launch_dd<VP_F32, 64, 0>(a, mode, st, ev0, ev1);
   }
   return hipErrorInvalidValue;
 }

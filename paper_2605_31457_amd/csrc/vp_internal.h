@@ -100,7 +100,9 @@ __host__ __device__ inline int parts_used(int L, int nparts) {
   return tiles < nparts ? tiles : nparts;
 }
 
-hipError_t launch_attend(const AttendArgs& a, int mode, int dtype, int head_dim, hipStream_t st);
+// ev0 / ev1 (optional): events attached to the launch, timing the kernel alone
+hipError_t launch_attend(const AttendArgs& a, int mode, int dtype, int head_dim, hipStream_t st,
+                         hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr);
 
 struct MassArgs {
   const int32_t* seq_len;
