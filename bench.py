@@ -86,27 +86,37 @@ def algorithmic_bytes(w, ks, lens=None, rows=1, kv_per_row=None):
     return {"visual": vis, "text": text, "kept": kept}
 
 
+def kernel_source_hash(root: str) -> str:
+    """sha256 over the HIP sources with comments and blank space removed, so that
+    a comment edit does not mark the stored counter figures stale."""
+    import glob
+    import hashlib
+    import re
+    h = hashlib.sha256()
+    for f in sorted(glob.glob(os.path.join(root, "paper_2605_31457_amd", "csrc", "*"))):
+        with open(f) as src:
+            text = src.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(os.path.basename(f).encode())
+        h.update(" ".join(text.split()).encode())
+    return h.hexdigest()
+
+
 def counter_traffic(cfg: int, kernel: str):
     """HBM bytes per launch of the roofline kernel ("text": the text pass;
     "one_launch": both context passes in one launch) from the FETCH_SIZE /
     WRITE_SIZE counter runs summarised in profiles/ (FETCH_SIZE scaled by a
     plain copy's reading), or None when they were taken on other kernel
     sources, another configuration or another kernel."""
-    import glob
-    import hashlib
     root = os.path.dirname(os.path.abspath(__file__))
     path = os.path.join(root, "profiles", "text_pass_traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as fh:
         rec = json.load(fh)
-    h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(root, "paper_2605_31457_amd", "csrc", "*"))):
-        h.update(os.path.basename(f).encode())
-        with open(f, "rb") as src:
-            h.update(src.read())
     entry = rec.get("configs", {}).get(str(cfg))
-    if h.hexdigest() != rec.get("source_sha256") or entry is None or entry.get("kernel") != kernel:
+    if kernel_source_hash(root) != rec.get("source_sha256") or entry is None or entry.get("kernel") != kernel:
         return None
     return entry["traffic_bytes"]
 

@@ -2,7 +2,8 @@
 // behind vp_visual_mass (Eq. (2), (5), (6)) and the attention partials of
 // vp_sparse_decode_attn (Sec. 4.1/4.2).
 //
-// Work decomposition: one 64-lane wave per work-group; grid = (parts, Hkv, B).
+// Work decomposition: one 64-lane wave per work-group; grid = (parts, Hkv, B)
+// (kept pass: (splits, Hkv * T, B), one row of work-groups per query).
 // In the context pass part p of `nparts` takes the 32-row tiles p, p + nparts,
 // p + 2 nparts, ... of the cache (a cyclic deal: every part, and so every XCD,
 // sees the sequence's own mix of visual and text rows); in the kept pass a part

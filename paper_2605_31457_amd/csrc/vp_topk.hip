@@ -1,6 +1,7 @@
 // Eq. (3): Top-K_t selection of visual tokens by score (Sec. 4.2).
 //
-// One 1024-thread work-group (16 waves) per sequence:
+// One 1024-thread work-group (16 waves) per selection row (a sequence, or one
+// query or KV group of it; the row's sequence gives the visual tokens):
 //  1. wave 0 loads the sequence's segment table into LDS while the block maps
 //     the scores to order-preserving 32-bit keys, stages them in LDS (when
 //     they fit) and finds their min and max;
