@@ -62,6 +62,7 @@ class DeviceStep:
                  kv=None, block_size: int = 0, block_seed: int = 0, kv_groups: bool = False):
         self.w = w
         self.T = w.q.shape[1] if w.q.ndim == 4 else 1
+        self.kv_groups = kv_groups
         self.rows = w.Hkv if kv_groups else 1  # selection rows per query
         self.device = torch.device(device)
         self.q = _dev(w.q, self.device)
@@ -143,7 +144,7 @@ class DeviceStep:
         torch.cuda.synchronize(self.device)
         B, T = self.w.B, self.T
         qlead = (B, T) if T > 1 else (B,)
-        lead = qlead + ((self.rows,) if self.rows > 1 else ())
+        lead = qlead + ((self.rows,) if self.kv_groups else ())
         rows = lambda t: t.cpu().numpy().reshape(lead + tuple(t.shape[1:]))
         per_query = lambda t: t.cpu().numpy().reshape(qlead + tuple(t.shape[1:]))
         return dict(mass_head=per_query(self.mass_head), mass_seq=rows(self.mass_seq),
