@@ -474,12 +474,17 @@ vp_status vp_validate_layout(const vp_shape* shape, const vp_layout* layout, voi
   if (hipError_t e = hipMemcpy(off.data(), layout->vis_seg_off, (B + 1) * sizeof(int32_t), hipMemcpyDeviceToHost))
     return hip_fail(e, "vis_seg_off copy");
   if (off[0] < 0) return fail(VP_ERR_SHAPE, "vis_seg_off[0] = %d < 0", off[0]);
-  for (int b = 0; b < B; ++b)
+  for (int b = 0; b < B; ++b) {
     if (off[b + 1] < off[b]) return fail(VP_ERR_SHAPE, "vis_seg_off decreases at sequence %d", b);
-  std::vector<int32_t> seg(2 * static_cast<size_t>(off[B]) + 2);
-  if (off[B] > 0) {
-    if (hipError_t e = hipMemcpy(seg.data(), layout->vis_seg, 2 * static_cast<size_t>(off[B]) * sizeof(int32_t),
-                                 hipMemcpyDeviceToHost))
+    if (off[b + 1] - off[b] > shape->max_segs)
+      return fail(VP_ERR_SHAPE, "sequence %d: %d segments > max_segs %d", b, off[b + 1] - off[b], shape->max_segs);
+  }
+  // segments off[0] .. off[B]: at most B * max_segs (<= 16.8M), a bounded host copy
+  const size_t nseg = static_cast<size_t>(off[B] - off[0]);
+  std::vector<int32_t> seg(2 * nseg + 2);
+  if (nseg > 0) {
+    if (hipError_t e = hipMemcpy(seg.data(), layout->vis_seg + 2 * static_cast<size_t>(off[0]),
+                                 2 * nseg * sizeof(int32_t), hipMemcpyDeviceToHost))
       return hip_fail(e, "vis_seg copy");
   }
   std::vector<int32_t> table;
@@ -495,11 +500,10 @@ vp_status vp_validate_layout(const vp_shape* shape, const vp_layout* layout, voi
     const int L = len[b];
     if (L < 0 || L > shape->max_seq_len)
       return fail(VP_ERR_SHAPE, "sequence %d: seq_len %d outside [0, max_seq_len %d]", b, L, shape->max_seq_len);
-    const int n = off[b + 1] - off[b];
-    if (n > shape->max_segs) return fail(VP_ERR_SHAPE, "sequence %d: %d segments > max_segs %d", b, n, shape->max_segs);
     int64_t end = 0, nv = 0;
     for (int i = off[b]; i < off[b + 1]; ++i) {
-      const int st = seg[2 * static_cast<size_t>(i)], ln = seg[2 * static_cast<size_t>(i) + 1];
+      const size_t j = static_cast<size_t>(i - off[0]);
+      const int st = seg[2 * j], ln = seg[2 * j + 1];
       if (ln < 1) return fail(VP_ERR_SHAPE, "sequence %d: segment %d has length %d < 1", b, i - off[b], ln);
       if (st < end)
         return fail(VP_ERR_SHAPE, "sequence %d: segment %d starts at %d, before the previous end %lld", b,

@@ -57,3 +57,15 @@ def test_negative_block_id_is_named():
     ds = _ds(block_size=32, block_seed=3)
     ds.block_table[2, 1] = -5
     _bad(ds, "block_table")
+
+
+def test_offsets_may_start_inside_a_larger_segment_array():
+    """vis_seg_off[0] > 0: the sequences' segments sit after unrelated entries."""
+    ds = _ds()
+    pad = torch.tensor([999999, -5], dtype=torch.int32, device=ds.device)  # never read
+    seg = torch.cat([pad, ds.seg])
+    off = ds.seg_off + 1
+    lay = vp.vp_layout(seq_len=ds.seq_len.data_ptr(), vis_seg_off=off.data_ptr(), vis_seg=seg.data_ptr())
+    vp.vp_validate_layout(ds.shape, lay)
+    seg[2 + 2] = 90  # the second segment of sequence 0 now overlaps the first
+    _bad(ds, "before the previous end", layout=lay)
