@@ -244,6 +244,8 @@ def main():
     ap.add_argument("--queries", type=int, default=1, metavar="T",
                     help="T queries per sequence in one step (speculative / multi-token decoding; configs 1-4): "
                          "the last T positions are the queries, each a step of its own over its prefix")
+    ap.add_argument("--graph", action="store_true",
+                    help="time replays of a HIP graph holding one step per rotated cache copy")
     ap.add_argument("--kv-groups", action="store_true",
                     help="one budget and kept set per KV group (VP_SCOPE_KV_GROUP) instead of per sequence")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
@@ -275,6 +277,9 @@ def main():
         return
 
     cfg = args.config
+    if args.graph and (cfg == 5 or args.calls or args.layers > 1 or args.dense):
+        print("bench.py --graph: configs 1-4, one-call steps, one layer", file=sys.stderr)
+        sys.exit(2)
     if args.queries > 1 and cfg == 5:
         print("bench.py --queries: configs 1-4 (the decode loop of config 5 runs one query per step)",
               file=sys.stderr)
@@ -367,20 +372,41 @@ def main():
         if evs and evs[5]:
             hip.h.hipEventRecord(evs[5], sp)
 
+    gs = None
+    if args.graph:
+        # capture needs a stream of its own; every step of the run goes there
+        gs = torch.cuda.Stream()
+        sp = gs.cuda_stream
+        torch.cuda.set_stream(gs)
     for i in range(warmup):
         one_step(i)
     torch.cuda.synchronize()
     ks = ds.k.cpu().numpy().copy()
 
+    graph = None
+    if args.graph:
+        # one step per rotated cache copy in one graph; the timed region replays it
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph, stream=gs):
+            for i in range(R):
+                one_step(warmup + i)
+        torch.cuda.synchronize()
+        reps = max(1, round(steps / R))
+        steps = reps * R
     hip.h.hipEventRecord(ev_t0, sp)
     t0 = time.perf_counter()
-    for i in range(steps):
-        one_step(warmup + i, evs_all[i], arr_all[i], arr_all3[i])
+    if graph is not None:
+        for _ in range(reps):
+            graph.replay()
+    else:
+        for i in range(steps):
+            one_step(warmup + i, evs_all[i], arr_all[i], arr_all3[i])
     hip.h.hipEventRecord(ev_t1, sp)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     gpu_ms = hip.elapsed_ms(ev_t0, ev_t1)
-    text_ms = float(np.mean([hip.elapsed_ms(e[1], e[2]) for e in evs_all if e[1] is not None]))
+    if graph is None:
+        text_ms = float(np.mean([hip.elapsed_ms(e[1], e[2]) for e in evs_all if e[1] is not None]))
     for i in range(n_phase):
         one_step(warmup + steps + i, evs_phase[i], arr_phase[i], arr_phase3[i])
     torch.cuda.synchronize()
@@ -388,6 +414,8 @@ def main():
     def phase(i, j):
         return float(np.mean([hip.elapsed_ms(e[i], e[j]) for e in evs_phase]))
     vis_ms, tail_ms, attn_ms = phase(0, 1), phase(2, 3), phase(3, 5)
+    if graph is not None:
+        text_ms = phase(1, 2)  # the roofline launch, from the eager steps after the replays
     if loop is None:
         assert np.array_equal(ds.k.cpu().numpy(), ks), "budget changed between warm-up and timed steps"
 
@@ -442,7 +470,7 @@ def main():
                                                 "avg_phase_ms": vis_ms},
         "phases_ms": {"visual_pass": vis_ms, "text_pass": text_ms,
                       "mass_budget_scores_topk": tail_ms, "kept_pass_and_merge": attn_ms},
-        "entry_point": "four calls" if args.calls else "vp_decode_step",
+        "entry_point": ("four calls" if args.calls else "vp_decode_step") + (" (HIP graph replays)" if args.graph else ""),
         "plan": {"one_context_launch": one_launch, "select_in_one_group": bool(plan & vp.VP_PLAN_FUSED_TAIL)},
     }
     res["query_tokens_per_s"] = res["value"] * w.B * ds.T
