@@ -107,10 +107,10 @@ typedef struct vp_shape {
   int32_t n_kv_heads;   /* Hkv >= 1, Hq % Hkv == 0, Hq / Hkv <= 16 */
   int32_t head_dim;     /* d: 64 or 128 */
   int32_t dtype;        /* vp_dtype of q, K, V and out */
-  int32_t max_seq_len;  /* cache capacity; every seq_len[b] <= max_seq_len */
-  int32_t max_vis;      /* >= N_v of every sequence; row stride of scores */
+  int32_t max_seq_len;  /* cache capacity (rows); every seq_len[b] <= max_seq_len <= 2^28 */
+  int32_t max_vis;      /* >= N_v of every sequence; row stride of scores; <= 2^28 */
   int32_t max_segs;     /* >= visual segments of any sequence; <= 256 */
-  int32_t k_cap;        /* row stride of vis_idx; >= every budget vp_budget can return */
+  int32_t k_cap;        /* row stride of vis_idx; >= every budget vp_budget can return; <= 2^28 */
   int32_t block_size;   /* 0: contiguous caches; P > 0 (a power of two <= 65536): paged caches of P rows per block */
   int32_t scope;        /* vp_scope: selection rows per sequence R = 1 (VP_SCOPE_SEQUENCE) or Hkv (VP_SCOPE_KV_GROUP) */
   int32_t n_queries;    /* T: queries per sequence (0 is read as 1); T * Hq / Hkv <= 16 */

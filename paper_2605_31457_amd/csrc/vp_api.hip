@@ -33,6 +33,7 @@ vp_status hip_fail(hipError_t e, const char* what) {
 constexpr int kMaxGroup = 16;
 constexpr int kMaxHq = kMaxHq_;
 constexpr int kMaxBatch = 65535;
+constexpr int kMaxTokens = 1 << 28;  // bound on max_seq_len, max_vis and k_cap (32-bit index arithmetic)
 
 size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
 
@@ -54,6 +55,8 @@ vp_status check_shape(const vp_shape* s) {
   if (s->head_dim != 64 && s->head_dim != 128) return fail(VP_ERR_UNSUPPORTED, "head_dim %d (64 or 128)", s->head_dim);
   if (s->max_seq_len < 1) return fail(VP_ERR_SHAPE, "max_seq_len %d < 1", s->max_seq_len);
   if (s->max_vis < 1) return fail(VP_ERR_SHAPE, "max_vis %d < 1", s->max_vis);
+  if (s->max_seq_len > kMaxTokens || s->max_vis > kMaxTokens || s->k_cap > kMaxTokens)
+    return fail(VP_ERR_UNSUPPORTED, "max_seq_len, max_vis and k_cap must not exceed %d", kMaxTokens);
   if (s->max_segs < 0 || s->max_segs > 256) return fail(VP_ERR_UNSUPPORTED, "max_segs %d outside [0, 256]", s->max_segs);
   if (s->k_cap < 1) return fail(VP_ERR_SHAPE, "k_cap %d < 1", s->k_cap);
   if (s->block_size < 0 || s->block_size > 65536 || (s->block_size & (s->block_size - 1)) != 0)
@@ -61,7 +64,7 @@ vp_status check_shape(const vp_shape* s) {
   if (s->scope != VP_SCOPE_SEQUENCE && s->scope != VP_SCOPE_KV_GROUP)
     return fail(VP_ERR_RANGE, "scope %d: VP_SCOPE_SEQUENCE or VP_SCOPE_KV_GROUP", s->scope);
   if (s->n_queries < 0) return fail(VP_ERR_RANGE, "n_queries %d < 0", s->n_queries);
-  if (queries(*s) * (s->n_q_heads / s->n_kv_heads) > kMaxGroup)
+  if (static_cast<int64_t>(queries(*s)) * (s->n_q_heads / s->n_kv_heads) > kMaxGroup)
     return fail(VP_ERR_UNSUPPORTED, "n_queries %d x query group %d > %d rows per KV head", queries(*s),
                 s->n_q_heads / s->n_kv_heads, kMaxGroup);
   if (static_cast<int64_t>(s->batch) * rows_per_seq(*s) > kMaxBatch)

@@ -81,6 +81,9 @@ def test_workspace_size_is_pure_and_scales(L):
     (dict(scope=2), "VP_ERR_RANGE"),
     (dict(scope=-1), "VP_ERR_RANGE"),
     (dict(n_queries=-1), "VP_ERR_RANGE"),
+    (dict(n_queries=1 << 30), "VP_ERR_UNSUPPORTED"),
+    (dict(max_seq_len=(1 << 28) + 1), "VP_ERR_UNSUPPORTED"),
+    (dict(max_vis=(1 << 28) + 1), "VP_ERR_UNSUPPORTED"),
     (dict(n_queries=3), "VP_ERR_UNSUPPORTED"),  # 3 queries x 7 heads > 16 rows per KV head
     (dict(n_queries=17, n_q_heads=4, n_kv_heads=4), "VP_ERR_UNSUPPORTED"),
     (dict(scope=1, batch=20000), "VP_ERR_UNSUPPORTED"),  # 80000 selection rows
