@@ -86,14 +86,19 @@ def algorithmic_bytes(w, ks, lens=None, rows=1, kv_per_row=None):
     return {"visual": vis, "text": text, "kept": kept}
 
 
+# the sources that set what the context passes (the roofline kernels) read and
+# write: their kernels, their launch plan and their arguments
+ROOFLINE_SOURCES = ("vp_attend.hip", "vp_common.h", "vp_internal.h", "vp_plan.hip")
+
+
 def kernel_source_hash(root: str) -> str:
-    """sha256 over the HIP sources with comments and blank space removed, so that
-    a comment edit does not mark the stored counter figures stale."""
-    import glob
+    """sha256 over the roofline kernels' sources with comments and blank space
+    removed, so that a comment edit does not mark the stored counter figures stale."""
     import hashlib
     import re
     h = hashlib.sha256()
-    for f in sorted(glob.glob(os.path.join(root, "paper_2605_31457_amd", "csrc", "*"))):
+    for name in sorted(ROOFLINE_SOURCES):
+        f = os.path.join(root, "paper_2605_31457_amd", "csrc", name)
         with open(f) as src:
             text = src.read()
         text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)

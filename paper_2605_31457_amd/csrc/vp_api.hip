@@ -35,12 +35,6 @@ constexpr int kMaxHq = kMaxHq_;
 constexpr int kMaxBatch = 65535;
 constexpr int kMaxTokens = 1 << 28;  // bound on max_seq_len, max_vis and k_cap (32-bit index arithmetic)
 
-size_t align256(size_t x) { return (x + 255) & ~static_cast<size_t>(255); }
-
-// queries per sequence, and selection rows per query: one, or one per KV group
-int queries(const vp_shape& s) { return s.n_queries > 1 ? s.n_queries : 1; }
-int rows_per_query(const vp_shape& s) { return s.scope == VP_SCOPE_KV_GROUP ? s.n_kv_heads : 1; }
-int rows_per_seq(const vp_shape& s) { return queries(s) * rows_per_query(s); }
 
 vp_status check_shape(const vp_shape* s) {
   if (!s) return fail(VP_ERR_NULL, "shape is NULL");
@@ -175,17 +169,6 @@ AttendArgs attend_args(const vp_shape* s, const vp_layout* l, const vp_params* p
 
 }  // namespace
 
-// Context-pass work-groups per launch: 2048 is one resident round of the text
-// pass (8 work-groups per CU x 256 CUs), so no work-group waits for a second
-// round; measured best against 1024, 4096 and 8192 on every configuration
-// (the 64 x 32k batch: 689 -> 665 us per step).
-#ifndef VP_TARGET_PARTS
-#define VP_TARGET_PARTS 2048
-#endif
-#ifndef VP_MIN_TILES
-#define VP_MIN_TILES 2  // 32-row tiles per context-pass part, at least
-#endif
-
 MassArgs mass_args(const vp_shape* s, const vp_layout* l, const Plan& plan, const AttendArgs& a, char* ws,
                    float* mass_head, float* mass_seq, float* scores) {
   MassArgs m{};
@@ -272,89 +255,10 @@ MergeArgs merge_args(const vp_shape* s, const vp_layout* l, const Plan& plan, co
   return m;
 }
 
-// Both context passes in one launch: saves a launch and overlaps the two
-// passes' latency chains where the cache is small; kept apart otherwise, so
-// the visual pass's logit writes stay out of the text pass's read stream.
-// Measured: the 8 x 10.5k batch of the 72B shape (22k tiles) gains 6 us from the
-// one launch with half the parts; the 64 x 32k batch (262k tiles) loses 100 us.
-#ifndef VP_DUAL_MAX_TILES
-#define VP_DUAL_MAX_TILES 32768  // 32-row tiles over the batch and KV heads
-#endif
-#ifndef VP_DUAL_PART_DIV
-#define VP_DUAL_PART_DIV 2  // parts of the one-launch context pass: VP_TARGET_PARTS / this
-#endif
-bool use_dual(const vp_shape* s) {
-  const int64_t tiles = static_cast<int64_t>(s->batch) * s->n_kv_heads * ((s->max_seq_len + 31) / 32);
-  return tiles <= static_cast<int64_t>(VP_DUAL_MAX_TILES);
-}
-
 vp_status check_budget_cap(const vp_shape* s, const vp_params* p) {
   if (s->k_cap < max_budget(s, p))
     return fail(VP_ERR_SHAPE, "k_cap %d < largest budget %d for max_vis %d", s->k_cap, max_budget(s, p), s->max_vis);
   return VP_OK;
-}
-
-#ifndef VP_SELECT_WGS
-#define VP_SELECT_WGS 256  // target work-groups of the select launch: one per CU
-#endif
-
-Plan make_plan(const vp_shape& s) {
-  Plan p{};
-  // Context pass: about VP_TARGET_PARTS one-wave work-groups in all, each
-  // with at least two 32-row tiles. Tiles are dealt out cyclically, so every
-  // part sees the sequence's own mix of visual and text rows: consecutive
-  // work-groups land on different XCDs, and contiguous chunks would hand whole
-  // XCDs only visual (K) or only text (K + V) rows.
-  const int64_t pairs = static_cast<int64_t>(s.batch) * s.n_kv_heads;
-  const int64_t tiles = (s.max_seq_len + 31) / 32;
-  // the one-launch context pass runs a visual and a text work-group per part
-  const int64_t target = use_dual(&s) ? VP_TARGET_PARTS / VP_DUAL_PART_DIV : VP_TARGET_PARTS;
-  int64_t parts = (target + pairs - 1) / pairs;
-  if (parts > (tiles + VP_MIN_TILES - 1) / VP_MIN_TILES) parts = (tiles + VP_MIN_TILES - 1) / VP_MIN_TILES;
-  if (parts < 1) parts = 1;
-  p.nparts = static_cast<int>(parts);
-  // Kept pass: 64 rows (two tiles) per work-group, or 32 when that leaves
-  // fewer than 1024 work-groups.
-#ifdef VP_KEPT_SPLIT
-  p.split = VP_KEPT_SPLIT;
-#else
-  p.split = static_cast<int64_t>(s.batch) * s.n_kv_heads * queries(s) * ((s.k_cap + 63) / 64) >= 1024 ? 64 : 32;
-#endif
-  p.nsplit = (s.k_cap + p.split - 1) / p.split;
-  // per-head arrays hold one entry per query row (virtual head): T*Hq per sequence
-  const size_t B = s.batch, Hq = static_cast<size_t>(s.n_q_heads) * queries(s), d = s.head_dim;
-  p.zs_rows = ((s.max_seq_len + 31) / 32) * 32;
-  p.zs_gp = queries(s) * (s.n_q_heads / s.n_kv_heads) <= 8 ? 8 : 16;
-  size_t off = 0;
-  p.zs = off;
-  off = align256(off + B * static_cast<size_t>(s.n_kv_heads) * p.zs_rows * static_cast<size_t>(p.zs_gp) * 4);
-  p.stats = off;
-  off = align256(off + B * Hq * p.nparts * 8 * 4);
-  p.acc = off;
-  off = align256(off + B * Hq * p.nparts * d * 4);
-  p.head = off;
-  off = align256(off + B * Hq * 2 * 4);
-  p.kstats = off;
-  off = align256(off + B * Hq * p.nsplit * 2 * 4);
-  p.kacc = off;
-  off = align256(off + B * Hq * p.nsplit * d * 4);
-  const size_t rows = B * static_cast<size_t>(rows_per_seq(s));
-  p.sync = off;
-  off = align256(off + rows * 4);
-  p.segtab = off;
-  off = align256(off + B * kSegTableBytes);
-  p.total = off;
-  // Select kernel: chunks of whole rounds (a round scores 1024 / lanes-per-token
-  // visual ranks), enough rounds per chunk that the launch has about
-  // VP_SELECT_WGS work-groups, so the spilled logits stream through many CUs.
-  const int64_t tpr = select_tokens_per_round(s.n_kv_heads, rows_per_query(s));
-  const int64_t want = static_cast<int64_t>(rows) * s.max_vis;
-  int64_t rounds = (want + tpr * VP_SELECT_WGS - 1) / (tpr * VP_SELECT_WGS);
-  if (rounds < 1) rounds = 1;
-  const int64_t chunk = tpr * rounds;
-  p.sel_chunks = static_cast<int>((s.max_vis + chunk - 1) / chunk);
-  p.sel_chunk = p.sel_chunks == 1 ? s.max_vis : static_cast<int>(chunk);
-  return p;
 }
 
 }  // namespace vp

@@ -46,6 +46,12 @@ struct Plan {
 };
 
 Plan make_plan(const vp_shape& s);
+// both context passes in one launch (VP_PLAN_ONE_CONTEXT_LAUNCH)
+bool use_dual(const vp_shape* s);
+// queries per sequence, and selection rows per query: one, or one per KV group
+int queries(const vp_shape& s);
+int rows_per_query(const vp_shape& s);
+int rows_per_seq(const vp_shape& s);
 
 // Passes over the cache. The visual pass is the only one that writes a large
 // output (the logit spill); keeping it apart from the text pass keeps writes out
