@@ -126,22 +126,28 @@ def counter_traffic(cfg: int, kernel: str):
     return entry["traffic_bytes"]
 
 
-def cpu_baseline(w, budget_s: float, kv_groups: bool = False):
-    """fp64 reference on this host: whole sequences until about budget_s seconds."""
-    import numpy as np
+def cpu_baseline(w, budget_s: float, kv_groups: bool = False, gpu=None):
+    """fp64 reference on this host: whole sequences until about budget_s seconds.
+
+    With ``gpu`` (the GPU step's results on the same inputs, one query per
+    sequence, budgets per sequence), every sequence the reference finished is
+    also compared with them: parity of the measured run's outputs."""
     from oracle import vp_oracle as O
     from oracle.plant import params_of
     p = params_of(w)
     t0 = time.perf_counter()
     c0 = time.process_time()
     n = 0
+    done = {}
     while True:
         b = n % w.B
         if w.q.ndim == 4:  # several queries per sequence
             O.decode_step_queries(w.q[b], w.K[b], w.V[b], int(w.seq_len[b]), w.segments[b], p, kv_groups=kv_groups)
         else:
             run = O.decode_step_sequence_kv_groups if kv_groups else O.decode_step_sequence
-            run(w.q[b], w.K[b], w.V[b], int(w.seq_len[b]), w.segments[b], p)
+            r = run(w.q[b], w.K[b], w.V[b], int(w.seq_len[b]), w.segments[b], p)
+            if b not in done:
+                done[b] = r
         n += 1
         el = time.perf_counter() - t0
         if el >= budget_s and n >= 1:
@@ -149,10 +155,73 @@ def cpu_baseline(w, budget_s: float, kv_groups: bool = False):
     cpu = time.process_time() - c0
     per_seq = el / n
     steps_per_s = 1.0 / (per_seq * w.B)
-    del np
-    return {"value": steps_per_s, "unit": "steps/s", "cores": max(1, round(cpu / el)), "kind": "oracle",
-            "sample": f"{n} sequence-steps of this workload's batch (sequences 0..{min(n, w.B) - 1}), "
-                      f"{el:.1f} s wall; steps/s = 1 / (mean time per sequence x B={w.B})"}
+    out = {"value": steps_per_s, "unit": "steps/s", "cores": max(1, round(cpu / el)), "kind": "oracle",
+           "sample": f"{n} sequence-steps of this workload's batch (sequences 0..{min(n, w.B) - 1}), "
+                     f"{el:.1f} s wall; steps/s = 1 / (mean time per sequence x B={w.B})"}
+    if gpu is not None and w.q.ndim == 3 and not kv_groups:
+        out["parity_of_measured_run"] = measured_parity(w, gpu, done, p, O)
+    return out
+
+
+def loop_parity(w, gpu, q_t, L_t, seqs=(0, 1)):
+    """The decode loop's last timed step (query q_t, length L_t) against the
+    reference, on a few of its sequences (the cpu_baseline leg's oracle use)."""
+    import dataclasses
+    import numpy as np
+    from oracle import vp_oracle as O
+    from oracle.plant import params_of
+    wl = dataclasses.replace(w, q=np.ascontiguousarray(q_t), seq_len=np.full(w.B, L_t, np.int32))
+    p = params_of(wl)
+    ref = {b: O.decode_step_sequence(wl.q[b], wl.K[b], wl.V[b], L_t, wl.segments[b], p) for b in seqs}
+    rep = measured_parity(wl, gpu, ref, p, O)
+    rep["step"] = f"loop step with length {L_t}"
+    return rep
+
+
+def measured_parity(w, gpu, ref, p, O):
+    """The timed run's outputs against the reference on the same (unplanted)
+    inputs: masses and scores to 1e-5 relative; the budget exact unless
+    M_vis,max * N_v lies within 2e-5 of a rounding boundary; the kept set exact,
+    or differing only in tokens within 2e-5 relative of the cut score; outputs to
+    the dtype's tolerance wherever the sets agree."""
+    import numpy as np
+    band = 2e-5
+    atol, rtol = (2e-2, 1e-2) if w.dtype == "bf16" else (1e-5, 1e-5)
+    rep = {"sequences": len(ref), "masses_and_scores": True, "budgets_exact": 0, "budgets_in_band": 0,
+           "sets_exact": 0, "sets_in_band": 0, "outputs_checked": 0, "outputs_ok": True, "ok": True}
+    for b, r in ref.items():
+        vis = O.visual_positions(int(w.seq_len[b]), w.segments[b])
+        nv = len(vis)
+        close = lambda x, y: np.allclose(x, y, rtol=1e-5, atol=1e-30)
+        if not (close(gpu["mass_head"][b], r.mass_head) and close(gpu["mass_seq"][b], [r.M_vis, r.M_vis_max])
+                and close(gpu["scores"][b, :nv], r.scores)):
+            rep["masses_and_scores"] = False
+        k = int(gpu["k"][b])
+        ks = {O.budget(r.M_vis_max * (1 + s * band), nv, p.r_lo_bp, p.r_hi_bp, p.clamp) for s in (-1, 0, 1)}
+        if k == r.k:
+            rep["budgets_exact"] += 1
+        elif k in ks:
+            rep["budgets_in_band"] += 1
+        else:
+            rep["ok"] = False
+        sel = gpu["vis_idx"][b, :k]
+        want = O.select_top_k(r.scores, vis, k)
+        if np.array_equal(sel, want):
+            rep["sets_exact"] += 1
+            if k == r.k:
+                rep["outputs_checked"] += 1
+                if not np.allclose(gpu["out"][b], r.out, atol=atol, rtol=rtol):
+                    rep["outputs_ok"] = False
+        else:
+            order = np.lexsort((vis, -r.scores))
+            cut = r.scores[order[k - 1]] if k > 0 else 0.0
+            diff = np.searchsorted(vis, np.setxor1d(sel, want))
+            if np.all(np.abs(r.scores[diff] - cut) <= band * cut):
+                rep["sets_in_band"] += 1
+            else:
+                rep["ok"] = False
+    rep["ok"] = rep["ok"] and rep["masses_and_scores"] and rep["outputs_ok"]
+    return rep
 
 
 def bench_layers(args, w, ds, bufs, loop, steps, warmup, sp, hip):
@@ -481,7 +550,13 @@ def main():
     res["query_tokens_per_s"] = res["value"] * w.B * ds.T
     if not args.no_cpu_baseline:
         print("[bench] timing the fp64 reference on the host", file=sys.stderr, flush=True)
-        res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, args.kv_groups)
+        # the reference on the timed run's inputs; for a single-step workload its
+        # sequences are also compared with the run's own outputs
+        gpu = ds.results() if loop is None and ds.T == 1 else None
+        res["cpu_baseline"] = cpu_baseline(w, args.cpu_seconds, args.kv_groups, gpu)
+        if loop is not None and not args.kv_groups:
+            t_last = (warmup + steps + n_phase - 1) % loop[0]
+            res["cpu_baseline"]["parity_of_measured_run"] = loop_parity(w, ds.results(), qs[t_last], loop[3][t_last])
     print(json.dumps(res), flush=True)
 
 
