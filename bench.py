@@ -155,7 +155,14 @@ def cpu_baseline(w, budget_s: float, kv_groups: bool = False, gpu=None):
     cpu = time.process_time() - c0
     per_seq = el / n
     steps_per_s = 1.0 / (per_seq * w.B)
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), "")
+    except OSError:
+        pass
     out = {"value": steps_per_s, "unit": "steps/s", "cores": max(1, round(cpu / el)), "kind": "oracle",
+           "host_cpu": model,
            "sample": f"{n} sequence-steps of this workload's batch (sequences 0..{min(n, w.B) - 1}), "
                      f"{el:.1f} s wall; steps/s = 1 / (mean time per sequence x B={w.B})"}
     if gpu is not None and w.q.ndim == 3 and not kv_groups:

@@ -92,6 +92,35 @@ int main(void) {
   p.tau_mass = 0.0f;
   CHECK(vp_budget_host(0.5, 100, &p) == -1);     /* invalid parameters */
 
+  /* every call rejects bad arguments before touching the device */
+  p.clamp = 1;
+  p.tau_mass = 0.1f;
+  vp_layout lay;
+  memset(&lay, 0, sizeof(lay));
+  int32_t dummy[4] = {0, 0, 0, 0};
+  lay.seq_len = dummy;
+  lay.vis_seg_off = dummy;
+  lay.vis_seg = dummy;
+  s = shape_7b();
+  CHECK(vp_workspace_size(&s, &bytes) == VP_OK);
+  CHECK(vp_decode_step(&s, &lay, &p, NULL, dummy, dummy, NULL, NULL, NULL, NULL, NULL, NULL, NULL, bytes, NULL,
+                       NULL, 0) == VP_ERR_NULL);
+  CHECK(vp_visual_mass(&s, NULL, &p, dummy, dummy, NULL, NULL, NULL, NULL, NULL, bytes, NULL) == VP_ERR_NULL);
+  CHECK(vp_budget(&s, &lay, &p, NULL, NULL, NULL) == VP_ERR_NULL);
+  CHECK(vp_select_topk(&s, &lay, NULL, NULL, NULL, NULL) == VP_ERR_NULL);
+  CHECK(vp_budget_top_p(&s, &lay, (const float*)dummy, 2.0f, dummy, NULL) == VP_ERR_RANGE);
+  CHECK(vp_validate_layout(&s, NULL, NULL) == VP_ERR_NULL);
+  s.block_size = 32; /* paged caches need a block table */
+  CHECK(vp_validate_layout(&s, &lay, NULL) == VP_ERR_NULL);
+  s = shape_7b();
+  p.tau_mass = -1.0f;
+  CHECK(vp_sparse_decode_attn(&s, &lay, &p, dummy, dummy, dummy, dummy, dummy, dummy, 0, dummy, bytes, NULL) ==
+        VP_ERR_RANGE);
+  p.tau_mass = 0.1f;
+  CHECK(vp_sparse_decode_attn(&s, &lay, &p, dummy, dummy, dummy, dummy, dummy, dummy, 0, dummy, 16, NULL) ==
+        VP_ERR_WORKSPACE);
+  CHECK(strlen(vp_last_error()) > 0);
+
   if (failures) {
     fprintf(stderr, "%d check(s) failed\n", failures);
     return 1;
