@@ -716,21 +716,24 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(attend_waves
   attend_body<DT, D, MODE>(a, lds, blockIdx.x, blockIdx.y, blockIdx.z);
 }
 
-// Both context passes in one launch (grid.x = 2 parts): the first half of the
-// work-groups takes the visual role, the second the text role. Used where the
-// batch is small and launch latency, not bandwidth, bounds the step.
+// Both context passes in one launch (grid.x = 2 parts + 1): work-group 2p takes
+// the text role of part p, 2p + 1 its visual role, the last one the step setup.
+// Used up to mid-size caches, where launch latency and load balance, not the
+// visual spill's interference with the text stream, bound the step.
 template <int DT, int D, int PG>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(attend_waves(DT, MODE_TEXT_BOTH)))) void
 attend_dual_kernel(const AttendArgs a) {
   constexpr int BYTES = max_i(PassLds<DT, D, MODE_VIS | PG>::BYTES, PassLds<DT, D, MODE_TEXT_BOTH | PG>::BYTES);
   __shared__ __attribute__((aligned(1024))) unsigned char lds[BYTES];
   const int x = blockIdx.x;
-  if (x < a.nparts)
-    attend_body<DT, D, MODE_VIS | PG>(a, lds, x, blockIdx.y, blockIdx.z);
-  else if (x < 2 * a.nparts)
-    attend_body<DT, D, MODE_TEXT_BOTH | PG>(a, lds, x - a.nparts, blockIdx.y, blockIdx.z);
-  else
+  // the roles alternate, so every CU gets a mix of visual (K, spill) and text
+  // (K and V) work-groups (measured 86.5 -> 84.8 us at the 16-sequence ragged batch)
+  if (x < 2 * a.nparts) {
+    if (x & 1) attend_body<DT, D, MODE_VIS | PG>(a, lds, x >> 1, blockIdx.y, blockIdx.z);
+    else attend_body<DT, D, MODE_TEXT_BOTH | PG>(a, lds, x >> 1, blockIdx.y, blockIdx.z);
+  } else {
     step_setup(a, blockIdx.y, blockIdx.z);
+  }
 }
 
 // Launches one pass. With events given, they are attached to the launch itself
