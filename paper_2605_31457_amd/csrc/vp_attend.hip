@@ -339,14 +339,15 @@ struct Pass {
   }
   __device__ __forceinline__ bool needs_v(const Sub& s) const { return ATTN; }
 
-  __device__ __forceinline__ Sub sub_at(const Sub& prev, int t0) const {
+  __device__ __forceinline__ Sub sub_at(const Sub& prev, int t0, int kp_loaded = -2) const {
     Sub n = prev;
     n.t0 = t0;
     n.cls = TILE_TEXT;
     if constexpr (KEPT) {
-      // one coalesced load of the tile's kept positions (issued a tile ahead)
+      // one coalesced load of the tile's kept positions (issued a tile ahead;
+      // the first tile's come in as kp_loaded, requested before the budget)
       const int t = t0 + lane;
-      n.kp = (lane < 32 && t < r1) ? kept[t] : -1;
+      n.kp = (lane < 32 && t < r1) ? (kp_loaded != -2 ? kp_loaded : kept[t]) : -1;
     } else {
       if (t0 < r1) {
         n.w.seek(t0);
@@ -564,28 +565,33 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
   s.kept = nullptr;
   const int qk = P::KEPT ? gy % a.T : 0;  // kept pass: the query
   const int g = P::KEPT ? gy / a.T : gy;   // KV head
-  if constexpr (P::KEPT) {
-    if (s.L == 0) return;
-    // the selection row of query qk that KV head g belongs to
-    const size_t row = (static_cast<size_t>(b) * a.T + qk) * a.U + g / (a.Hkv / a.U);
-    int kb = a.kk[row];
-    kb = kb < 0 ? 0 : (kb > a.k_cap ? a.k_cap : kb);
-    s.r0 = part * a.split;
-    s.r1 = min(s.r0 + a.split, kb);
-    s.step = 32;
-    s.kept = a.vis_idx + row * a.k_cap;
-  } else {
-    s.r0 = 32 * part;
-    s.r1 = s.L;
-    s.step = 32 * a.nparts;
-  }
-  if (s.r0 >= s.r1) return;
-
   // lane row n16 <-> virtual head vh of this KV head: query vh / G, head g*G + vh % G
   const int vh = P::KEPT ? qk * a.G + s.n16 : s.n16;
   s.hv = s.n16 < (P::KEPT ? a.G : a.T * a.G);
   const int tq = s.hv ? vh / a.G : 0;
   s.h = g * a.T * a.G + vh;
+  int kp0 = -2;  // kept pass: the first tile's kept positions, requested with the budget
+  if constexpr (P::KEPT) {
+    // the selection row of query qk that KV head g belongs to
+    const size_t row = (static_cast<size_t>(b) * a.T + qk) * a.U + g / (a.Hkv / a.U);
+    s.kept = a.vis_idx + row * a.k_cap;
+    s.r0 = part * a.split;
+    const int t = s.r0 + s.lane;
+    kp0 = (s.lane < 32 && t < a.k_cap) ? s.kept[t] : -1;  // entries past the budget are masked below
+    int kb = a.kk[row];
+    kb = kb < 0 ? 0 : (kb > a.k_cap ? a.k_cap : kb);
+    s.r1 = s.L == 0 ? s.r0 : min(s.r0 + a.split, kb);
+    s.step = 32;
+  } else {
+    s.r0 = 32 * part;
+    s.r1 = s.L;
+    s.step = 32 * a.nparts;
+  }
+  // the query rows load while the length and the budget arrive
+  const size_t qrow = s.hv ? (static_cast<size_t>(b) * a.T + tq) * a.Hq + g * a.G + (vh - tq * a.G) : 0;
+  load_q<DT, D>(s.qf, static_cast<const char*>(a.q) + qrow * C::ROWB, s.hv, s.a4);
+  if (s.r0 >= s.r1) return;
+
   s.L0 = s.L - a.T + 1;
   s.lim = s.L0 + tq;
   // contiguous caches: sequence b's rows from its base; paged caches: rows of
@@ -598,8 +604,6 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
   s.bt = paged ? a.block_table + static_cast<size_t>(b) * a.nblk : nullptr;
   s.bstride = static_cast<size_t>(a.sb) * C::ESZ;
   s.bmask = paged ? (1 << a.bs_log2) - 1 : 0;
-  const size_t qrow = s.hv ? (static_cast<size_t>(b) * a.T + tq) * a.Hq + g * a.G + (vh - tq * a.G) : 0;
-  load_q<DT, D>(s.qf, static_cast<const char*>(a.q) + qrow * C::ROWB, s.hv, s.a4);
   s.m_v = kNegInf;
   s.Ls_v = s.Lm_v = 0.f;
   s.m_t = kNegInf;
@@ -615,7 +619,7 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
     const int o0 = a.seg_off[b];
     cur.w.start(a.seg + 2 * static_cast<long>(o0), a.seg_off[b + 1] - o0, vis_len(s.L, a.T));
   }
-  cur = s.sub_at(cur, s.r0);
+  cur = s.sub_at(cur, s.r0, kp0);
 
   // tiles of NSUB sub-tiles: all copies of a tile are issued before any of it is used
   while (cur.t0 < s.r1) {
