@@ -361,6 +361,13 @@ def main():
     if args.graph and (cfg == 5 or args.calls or args.layers > 1 or args.dense):
         print("bench.py --graph: configs 1-4, one-call steps, one layer", file=sys.stderr)
         sys.exit(2)
+    if args.paged and cfg == 4:
+        # one run of this case ended in a host-side segmentation fault before
+        # its first kernel launch (while the 2.2 GB paged caches were built and
+        # uploaded), with no cause found in this code: held back until there is one
+        print("bench.py --paged: configs 1-3 and 5 (the paged 64 x 32k batch is held back after an "
+              "unexplained host-side crash during its set-up)", file=sys.stderr)
+        sys.exit(2)
     if args.queries > 1 and cfg == 5:
         print("bench.py --queries: configs 1-4 (the decode loop of config 5 runs one query per step)",
               file=sys.stderr)
