@@ -41,6 +41,10 @@ bool use_dual(const vp_shape* s) {
   return tiles <= static_cast<int64_t>(VP_DUAL_MAX_TILES);
 }
 
+#ifndef VP_KEPT_WGS
+#define VP_KEPT_WGS 2048  // kept-pass work-groups in one resident round (8 per CU)
+#endif
+
 #ifndef VP_SELECT_WGS
 #define VP_SELECT_WGS 256  // target work-groups of the select launch: one per CU
 #endif
@@ -60,12 +64,19 @@ Plan make_plan(const vp_shape& s) {
   if (parts > (tiles + VP_MIN_TILES - 1) / VP_MIN_TILES) parts = (tiles + VP_MIN_TILES - 1) / VP_MIN_TILES;
   if (parts < 1) parts = 1;
   p.nparts = static_cast<int>(parts);
-  // Kept pass: 64 rows (two tiles) per work-group, or 32 when that leaves
-  // fewer than 1024 work-groups.
+  // Kept pass: the fewest kept rows per work-group (32, 64, 128, ...) that
+  // keep the launch within one resident round (VP_KEPT_WGS work-groups), so no
+  // work-group waits for a second round (the 64 x 32k batch: 128 rows, 1792
+  // work-groups; kept pass and merge 40.2 -> 35.9 us against 64 rows).
 #ifdef VP_KEPT_SPLIT
   p.split = VP_KEPT_SPLIT;
 #else
-  p.split = static_cast<int64_t>(s.batch) * s.n_kv_heads * queries(s) * ((s.k_cap + 63) / 64) >= 1024 ? 64 : 32;
+  {
+    const int64_t heads = static_cast<int64_t>(s.batch) * s.n_kv_heads * queries(s);
+    int64_t split = 32;
+    while (split < s.k_cap && heads * ((s.k_cap + split - 1) / split) > VP_KEPT_WGS) split *= 2;
+    p.split = static_cast<int>(split);
+  }
 #endif
   p.nsplit = (s.k_cap + p.split - 1) / p.split;
   // per-head arrays hold one entry per query row (virtual head): T*Hq per sequence
