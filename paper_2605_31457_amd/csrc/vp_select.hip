@@ -11,9 +11,10 @@
 // visual ranks [c * chunk, (c + 1) * chunk) from the spilled logits and writes
 // them. With one chunk per row the keys stay in LDS and the same work-group
 // selects; with several, each work-group publishes its scores (device-scope
-// release) and counts itself in on the row's arrival counter (zeroed by the
-// context pass of the same step); the last to arrive reads every score of the
-// row back and selects. No work-group ever waits for another.
+// atomic stores, coherent across the XCDs) and, once they have completed,
+// counts itself in on the row's arrival counter (zeroed by the context pass of
+// the same step); the last to arrive reads every score of the row back with
+// device-scope loads and selects. No work-group ever waits for another.
 //
 // Latency: the statistics and the segment table (built by the context pass)
 // are requested at once at entry; the spilled logits of a thread's tokens (all heads) are one
@@ -25,6 +26,19 @@
 
 namespace vp {
 namespace {
+
+// The scores are the only data that crosses work-groups: they are stored and
+// re-read as device-scope atomics, which are coherent across the XCDs' L2
+// caches, so a work-group counts in once its own stores have completed, with no
+// L2 write-back (a release per work-group serialised at ~0.15 us per
+// work-group on each XCD: 4.9 us of arrival at the 16-sequence batch), and the
+// last one reads them back with no L2 invalidation.
+__device__ __forceinline__ void store_score(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_score(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
 // GP: floats per spill row (the query group padded to 8 or 16)
 template <int GP>
@@ -92,7 +106,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
     for (int j = 1; j < ng; ++j) total = total + __shfl(p, (lane & ~(ng - 1)) + j);
     if (ok && l == 0) {
       const float S = total / static_cast<float>(a.Hq / a.U);
-      sc[i] = S;
+      store_score(sc + i, S);
       const uint32_t u = order_key(S);
       if (single && in_lds) s_keys[i] = u;
       kmin = min(kmin, u);
@@ -102,14 +116,15 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
 
   if (!single) {
     // publish this chunk's scores and count in; the last work-group of the
-    // row selects. The barrier orders the block's stores before thread 0's
-    // device-scope release; the last arrival alone takes the acquire, which makes
-    // the other work-groups' scores visible to the block after the second barrier.
+    // row selects. Every wave waits for its own score stores to complete
+    // (device-coherent once acknowledged), the barrier then puts all of them
+    // before thread 0's count-in; the last arrival reads the scores with
+    // device-scope loads after the second barrier.
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
     __syncthreads();
     if (tid == 0) {
-      const bool last = __hip_atomic_fetch_add(t.sync + row, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT) ==
+      const bool last = __hip_atomic_fetch_add(t.sync + row, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) ==
                         static_cast<unsigned>(t.nchunks - 1);
-      if (last) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
       s_last = last;
     }
     __syncthreads();
@@ -120,7 +135,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
     for (int base = 0; base < n; base += kBatch * kSelThreads) {
       float v[kBatch];
 #pragma unroll
-      for (int j = 0; j < kBatch; ++j) v[j] = sc[min(base + j * kSelThreads + tid, n - 1)];
+      for (int j = 0; j < kBatch; ++j) v[j] = load_score(sc + min(base + j * kSelThreads + tid, n - 1));
 #pragma unroll
       for (int j = 0; j < kBatch; ++j) {
         const int i = base + j * kSelThreads + tid;
@@ -142,7 +157,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
   int32_t* out = t.vis_idx + static_cast<size_t>(row) * t.k_cap;
   for (int i = k + tid; i < t.k_cap; i += kSelThreads) out[i] = -1;
   if (k == 0) return;
-  auto key_at = [&](int i) -> uint32_t { return in_lds ? s_keys[i] : order_key(sc[i]); };
+  auto key_at = [&](int i) -> uint32_t { return in_lds ? s_keys[i] : order_key(load_score(sc + i)); };
   const bool take_all = k >= n;
   uint32_t T = 0u;
   int need = k;
