@@ -117,48 +117,61 @@ __device__ __forceinline__ void reduce_heads(const MassArgs& a, int b, int qt, i
   const int Hu = a.Hq / a.U;  // heads of the row
   const int h0 = u * Hu;
   const int lph = lanes_per_head(Hu, a.nparts);
-  const int sub = tid % lph;
-  const bool on = tid / lph < Hu;
-  const int h = h0 + (on ? tid / lph : 0);
-  // the head's statistics and merged results sit at its virtual head for query qt
-  const size_t vh = static_cast<size_t>(b) * a.T * a.Hq + vhead(h, qt, a.G, a.T);
+  // Only the waves that hold a head's lanes reduce; the others go straight to
+  // the barrier. Every wave of a 1024-thread block shares its SIMD with three
+  // others, so idle waves issuing the same instructions would slow the
+  // working ones down (the address arithmetic and the double sums).
+  const bool busy = (tid >> 6) < (Hu * lph + 63) / 64;  // uniform over the wave
   constexpr int U = kPartsPerLane;
-  // per part: [0] visual {m, Ls, Lm, -}, [1] text {m, l, Lm, Ls}
-  const float4* st = reinterpret_cast<const float4*>(a.stats + vh * a.nparts * 8);
   const bool one_round = a.nparts <= U * lph;
+  int sub = 0, h = h0;
+  bool on = false;
+  size_t vh = 0;
+  const float4* st = nullptr;
   float4 v[U], t[U];
-  if (one_round) load_parts(v, t, st, on, sub, lph, a.nparts);
-  between();
-  const int nv = parts_used(L, a.nparts);
-  float m = kNegInf;
-  double Ls = 0.0, Lm = 0.0, Vm = 0.0;
-  if (one_round) {
-    m = max_parts(m, v, t, on, sub, lph, nv);
-    m = group_max_f32(m, lph);
-    sum_parts(Ls, Lm, Vm, v, t, on, sub, lph, nv, m, a.inv_tau_m, a.inv_tau_s);
-  } else {
-    for (int c0 = sub; c0 < nv; c0 += U * lph) {
-      load_parts(v, t, st, on, c0, lph, nv);
-      m = max_parts(m, v, t, on, c0, lph, nv);
-    }
-    m = group_max_f32(m, lph);
-    for (int c0 = sub; c0 < nv; c0 += U * lph) {
-      load_parts(v, t, st, on, c0, lph, nv);
-      sum_parts(Ls, Lm, Vm, v, t, on, c0, lph, nv, m, a.inv_tau_m, a.inv_tau_s);
-    }
+  if (busy) {
+    sub = tid % lph;
+    on = tid / lph < Hu;
+    h = h0 + (on ? tid / lph : 0);
+    // the head's statistics and merged results sit at its virtual head for query qt
+    vh = static_cast<size_t>(b) * a.T * a.Hq + vhead(h, qt, a.G, a.T);
+    // per part: [0] visual {m, Ls, Lm, -}, [1] text {m, l, Lm, Ls}
+    st = reinterpret_cast<const float4*>(a.stats + vh * a.nparts * 8);
+    if (one_round) load_parts(v, t, st, on, sub, lph, a.nparts);
   }
-  Ls = group_sum_f64(Ls, lph);
-  Lm = group_sum_f64(Lm, lph);
-  Vm = group_sum_f64(Vm, lph);
-  if (on && sub == 0) {
-    const double mass = Lm > 0.0 ? Vm / Lm : 0.0;
-    const float ls = static_cast<float>(Ls);
-    hs.hm[h] = m;
-    hs.hinv[h] = ls > 0.f ? 1.0f / ls : 0.f;
-    hs.mass[h] = mass;
-    if (write_out) {
-      a.mass_head[(static_cast<size_t>(b) * a.T + qt) * a.Hq + h] = static_cast<float>(mass);
-      *reinterpret_cast<float2*>(a.head + vh * 2) = make_float2(m, ls);
+  between();
+  if (busy) {
+    const int nv = parts_used(L, a.nparts);
+    float m = kNegInf;
+    double Ls = 0.0, Lm = 0.0, Vm = 0.0;
+    if (one_round) {
+      m = max_parts(m, v, t, on, sub, lph, nv);
+      m = group_max_f32(m, lph);
+      sum_parts(Ls, Lm, Vm, v, t, on, sub, lph, nv, m, a.inv_tau_m, a.inv_tau_s);
+    } else {
+      for (int c0 = sub; c0 < nv; c0 += U * lph) {
+        load_parts(v, t, st, on, c0, lph, nv);
+        m = max_parts(m, v, t, on, c0, lph, nv);
+      }
+      m = group_max_f32(m, lph);
+      for (int c0 = sub; c0 < nv; c0 += U * lph) {
+        load_parts(v, t, st, on, c0, lph, nv);
+        sum_parts(Ls, Lm, Vm, v, t, on, c0, lph, nv, m, a.inv_tau_m, a.inv_tau_s);
+      }
+    }
+    Ls = group_sum_f64(Ls, lph);
+    Lm = group_sum_f64(Lm, lph);
+    Vm = group_sum_f64(Vm, lph);
+    if (on && sub == 0) {
+      const double mass = Lm > 0.0 ? Vm / Lm : 0.0;
+      const float ls = static_cast<float>(Ls);
+      hs.hm[h] = m;
+      hs.hinv[h] = ls > 0.f ? 1.0f / ls : 0.f;
+      hs.mass[h] = mass;
+      if (write_out) {
+        a.mass_head[(static_cast<size_t>(b) * a.T + qt) * a.Hq + h] = static_cast<float>(mass);
+        *reinterpret_cast<float2*>(a.head + vh * 2) = make_float2(m, ls);
+      }
     }
   }
   __syncthreads();

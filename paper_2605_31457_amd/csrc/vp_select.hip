@@ -61,7 +61,6 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
   uint32_t* s_keys = reinterpret_cast<uint32_t*>(dyn + head_lds_bytes(a.Hq));
 
   const int L = clamp_len(a.seq_len[b], a.max_seq_len);
-  for (int i = tid; i < kHistWords; i += kSelThreads) sh.hist[i] = 0;
 
   // ---- per-head statistics; the segment table is copied in while the
   // statistics are in flight (the reduction's barriers publish it) ----
@@ -76,6 +75,9 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
       reinterpret_cast<uint4*>(&tab)[tid >> 2] = src[tid >> 2];
     }
   });
+  // the radix counters are first used after the key-range barrier: cleared
+  // here, while the spilled logits below are in flight
+  for (int i = tid; i < kHistWords; i += kSelThreads) sh.hist[i] = 0;
   const int nvis = tab.rk[tab.n];
   const int n = min(nvis, a.max_vis);
   const bool single = t.nchunks == 1;
