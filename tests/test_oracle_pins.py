@@ -52,6 +52,37 @@ def test_worked_example_gqa2():
     np.testing.assert_allclose(r.out, want, rtol=1e-13)
 
 
+def test_worked_example_tempered_scores():
+    """Eq. (2) at a score temperature of its own (tau_score = 0.5, tau_mass = 0.25):
+    hand-derived exact rationals. The fixture is chosen so that scores taken at
+    tau_score = 1 or at tau_mass keep a different set, so an oracle that ignores
+    or swaps tau_score fails here."""
+    ex = json.load(open(os.path.join(GOLDEN, "worked_example_tau_score.json")))
+    inp, e = ex["inputs"], ex["expected"]
+    a, b, L = inp["a"], inp["b"], inp["seq_len"]
+    q = np.array([[1.0, 0.0], [0.0, 1.0]])
+    K = np.array([[[math.log(x), math.log(y)] for x, y in zip(a, b)]])
+    V = np.array([[[float(j), 1.0] for j in range(L)]])
+    p = O.OracleParams(tau_mass=inp["tau_mass"], tau_score=inp["tau_score"], sm_scale=inp["sm_scale"],
+                       r_lo_bp=inp["r_lo_bp"], r_hi_bp=inp["r_hi_bp"], clamp=inp["clamp"])
+    segs = [tuple(s) for s in inp["segments"]]
+    r = O.decode_step_sequence(q, K, V, L, segs, p)
+    frac = lambda f: f[0] / f[1]
+    np.testing.assert_allclose(r.mass_head, [frac(x) for x in e["mass_head"]], rtol=1e-13)
+    assert r.M_vis == pytest.approx(frac(e["M_vis"]), rel=1e-13)
+    assert r.M_vis_max == pytest.approx(frac(e["M_vis_max"]), rel=1e-13)
+    assert r.k == e["k"]
+    np.testing.assert_allclose(r.scores, [frac(x) for x in e["scores"]], rtol=1e-13)
+    assert list(r.vis_idx) == e["vis_idx"]
+    want = np.array([[frac(c) for c in row] for row in e["out"]])
+    np.testing.assert_allclose(r.out, want, rtol=1e-13)
+    # the same inputs with the scores at temperature 1 or at tau_mass keep {1, 3}
+    for ts in (1.0, inp["tau_mass"]):
+        p2 = O.OracleParams(tau_mass=inp["tau_mass"], tau_score=ts, sm_scale=1.0, r_lo_bp=inp["r_lo_bp"],
+                            r_hi_bp=inp["r_hi_bp"], clamp=True)
+        assert list(O.decode_step_sequence(q, K, V, L, segs, p2).vis_idx) == [1, 3]
+
+
 # ---------------------------------------------------------------------------
 # budget: closed-form table (Eq. (7) + Sec. 5.2 clamp)
 # ---------------------------------------------------------------------------
@@ -117,6 +148,27 @@ def test_scores_sum_to_mass_at_equal_temperature():
     p = O.OracleParams(tau_mass=1.0, tau_score=1.0, clamp=False)
     r = O.decode_step_sequence(q, K, V, L, segs, p)
     assert r.scores.sum() == pytest.approx(r.M_vis, rel=1e-13)
+
+
+@pytest.mark.parametrize("tau", [0.1, 0.4, 2.5])
+def test_scores_sum_to_mass_at_a_shared_temperature(tau):
+    """P2 at a temperature other than one: when Eq. (2) is taken over the
+    attention at the mass temperature (tau_score = tau_mass = tau), summing the
+    scores over visual tokens gives the mean over heads of the Eq. (5) masses;
+    and the visual and text scores of every head add to one, so a score
+    normaliser at the wrong temperature breaks the sum."""
+    rng = np.random.default_rng(20 + int(10 * tau))
+    q, K, V, L, segs = _rand_case(rng, Hq=6, Hkv=3)
+    p = O.OracleParams(tau_mass=tau, tau_score=tau, clamp=False)
+    r = O.decode_step_sequence(q, K, V, L, segs, p, keep_logits=True)
+    assert r.scores.sum() == pytest.approx(r.M_vis, rel=1e-12)
+    # the text tokens' scores at the same temperature carry the rest of the mass
+    txt = O.text_positions(L, segs)
+    assert r.scores.sum() + O.importance_scores(r.Z, txt, tau).sum() == pytest.approx(1.0, rel=1e-13)
+    # and at tau_score = 1 the identity fails for these inputs (the temperature matters)
+    p1 = O.OracleParams(tau_mass=tau, tau_score=1.0, clamp=False)
+    r1 = O.decode_step_sequence(q, K, V, L, segs, p1)
+    assert abs(r1.scores.sum() - r.M_vis) > 1e-6
 
 
 def test_zero_query_uniform_attention():
