@@ -9,8 +9,8 @@
 // Work-group c of row (b, u) reduces the per-part statistics of the row's heads
 // (every work-group of the row does, so none waits for another), scores the
 // visual ranks [c * chunk, (c + 1) * chunk) from the spilled logits and writes
-// them. With one chunk per row the keys stay in LDS and the same work-group
-// selects; with several, each work-group publishes its scores (device-scope
+// them. With one chunk per row the same work-group selects (its keys in LDS,
+// or, beyond the LDS room, re-read from its own score stores); with several, each work-group publishes its scores (device-scope
 // atomic stores, coherent across the XCDs) and, once they have completed,
 // counts itself in on the row's arrival counter (zeroed by the context pass of
 // the same step); the last to arrive reads every score of the row back with
@@ -116,6 +116,13 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
     }
   }
 
+  if (single && !in_lds) {
+    // one work-group, keys beyond its LDS room: the radix select reads the
+    // scores back from memory (device-scope loads, like the multi-chunk path).
+    // Every wave waits for its own score stores to complete; the barrier in
+    // block_key_range then puts them before any wave's reads.
+    __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0)
+  }
   if (!single) {
     // publish this chunk's scores and count in; the last work-group of the
     // row selects. Every wave waits for its own score stores to complete
@@ -191,9 +198,9 @@ int key_room(int Hq) {
 template <int GP>
 hipError_t launch_gp(const SelectArgs& t, hipStream_t st) {
   const int room = key_room<GP>(t.m.Hq);
+  // keys of up to `room` visual ranks stay in LDS; a row with more reads its
+  // scores back from memory during the selection
   const int keys = min(room, t.m.max_vis);
-  // one chunk keeps its keys in LDS: the launch plan guarantees they fit
-  if (t.nchunks == 1 && keys < t.m.max_vis) return hipErrorInvalidValue;
   const size_t dyn = static_cast<size_t>(head_lds_bytes(t.m.Hq)) + static_cast<size_t>(keys) * 4;
   hipLaunchKernelGGL((select_kernel<GP>), dim3(t.nchunks, t.m.B * t.m.T * t.m.U), dim3(kSelThreads), dyn, st, t,
                      keys);

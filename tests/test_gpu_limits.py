@@ -5,7 +5,7 @@ and the one-launch step against the four calls."""
 import numpy as np
 import pytest
 
-from _parity import check_sequence, small_workload
+from _parity import check_sequence, small_workload, tile_batch
 from oracle import plant as P
 from paper_2605_31457_amd import step as S
 
@@ -64,3 +64,23 @@ def test_131072_token_cache():
     w = small_workload(seed=65, B=1, Hq=4, Hkv=1, d=64, lens=[131072], segs=[[(1000, 60000), (70000, 20000)]])
     ref = _check("131072 tokens", w)
     _log(f"131072 tokens: k={ref[0].k}")
+
+
+def test_select_keys_beyond_lds_with_one_work_group_per_row():
+    """256 selection rows make the select launch score and select each row in a
+    single work-group; every other row here holds 40000 visual tokens, more keys
+    than that work-group's LDS holds, so its selection reads the scores back from
+    memory. Checked against the four calls and the reference."""
+    base = small_workload(seed=66, B=2, Hq=4, Hkv=1, d=64, lens=[40200, 300], segs=[[(100, 40000)], [(20, 200)]])
+    ref, _ = P.plant(base, P.params_of(base))
+    w = tile_batch(base, 256)
+    ds = S.DeviceStep(w, max_vis=40000)
+    ds.decode_step()
+    g = ds.results()
+    ds.run(fused=True)
+    c = ds.results()
+    for key in KEYS:
+        assert np.array_equal(g[key], c[key]), f"keys beyond LDS: {key} step != calls"
+    for b in range(w.B):
+        check_sequence("keys beyond LDS", w, g, b, ref[b % 2], b_src=b % 2)
+    _log(f"keys beyond LDS: k={[ref[b].k for b in range(2)]}")
