@@ -57,7 +57,7 @@ import numpy as np
 
 __all__ = [
     "as_f64", "logits", "tempered_attention", "visual_mass", "retention_bounds",
-    "budget", "budget_top_p", "importance_scores", "select_top_k", "pruned_attention",
+    "budget", "budget_top_p", "importance_scores", "select_top_k", "pruned_attention", "attention",
     "OracleParams", "SequenceResult", "decode_step_sequence", "decode_step",
     "visual_positions", "text_positions", "GroupedResult", "decode_step_sequence_kv_groups",
     "clip_segments", "decode_step_queries",
@@ -108,8 +108,12 @@ def text_positions(seq_len: int, segments) -> np.ndarray:
 # Eq. (6): logits and tempered attention
 # --------------------------------------------------------------------------
 def logits(q_h: np.ndarray, K_g: np.ndarray, sm_scale: float) -> np.ndarray:
-    """Z_{t,h}(q_t, j) for every row j of K_g: sm_scale * <q_h, k_j> (Eq. (6), reading A2)."""
-    return sm_scale * (as_f64(K_g) @ as_f64(q_h))
+    """Z_{t,h}(q_t, j) for every row j of K_g: sm_scale * <q_h, k_j> (Eq. (6), reading A2).
+
+    q_h is one head's query [d] (result [rows]) or the queries of several heads
+    that read the same KV head, [n, d] (result [n, rows], one row per head).
+    """
+    return sm_scale * (as_f64(q_h) @ as_f64(K_g).T)
 
 
 def tempered_attention(Z: np.ndarray, tau: float) -> np.ndarray:
@@ -216,9 +220,16 @@ def pruned_attention(q_h: np.ndarray, K_g: np.ndarray, V_g: np.ndarray,
     d = V_g.shape[-1]
     if len(J) == 0:
         return np.zeros(d, dtype=np.float64)
-    Z = logits(q_h, K_g[J], sm_scale)
-    p = np.exp(Z - Z.max())
-    return (p / p.sum()) @ as_f64(V_g[J])
+    return attention(q_h, K_g[J], V_g[J], sm_scale)
+
+
+def attention(q_h: np.ndarray, K_rows: np.ndarray, V_rows: np.ndarray, sm_scale: float) -> np.ndarray:
+    """softmax over the given rows of Z_{t,h}(q_t, j), applied to their V rows
+    (temperature 1; at least one row). q_h: [d], or [n, d] for n heads that read
+    the same rows (one softmax per head)."""
+    Z = logits(q_h, K_rows, sm_scale)
+    p = np.exp(Z - Z.max(axis=-1, keepdims=True))
+    return (p / p.sum(axis=-1, keepdims=True)) @ as_f64(V_rows)
 
 
 # --------------------------------------------------------------------------
@@ -274,9 +285,10 @@ def decode_step_sequence(q: np.ndarray, K: np.ndarray, V: np.ndarray,
     qf = as_f64(q)
 
     # Eq. (6) logits of every query head over every cached token (A1, A4)
+    # (the G query heads of KV head g in one product)
     Z = np.empty((Hq, seq_len), dtype=np.float64)
-    for h in range(Hq):
-        Z[h] = logits(qf[h], Kf[h // G], sm_scale)
+    for g in range(Hkv):
+        Z[g * G:(g + 1) * G] = logits(qf[g * G:(g + 1) * G], Kf[g], sm_scale)
 
     # Eq. (5)/(6) and the head-max; Eq. (7) with the clamp
     if seq_len > 0:
@@ -295,9 +307,12 @@ def decode_step_sequence(q: np.ndarray, K: np.ndarray, V: np.ndarray,
     out = None
     if with_output:
         J = np.sort(np.concatenate([sel, txt_pos]))
-        out = np.empty((Hq, d), dtype=np.float64)
-        for h in range(Hq):
-            out[h] = pruned_attention(qf[h], Kf[h // G], Vf[h // G], J, sm_scale)
+        out = np.zeros((Hq, d), dtype=np.float64)
+        if len(J):
+            for g in range(Hkv):
+                # the pruned context's rows of KV head g, gathered once for its G heads
+                KJ, VJ = Kf[g][J], Vf[g][J]
+                out[g * G:(g + 1) * G] = attention(qf[g * G:(g + 1) * G], KJ, VJ, sm_scale)
 
     return SequenceResult(m_head, M_vis, M_max, S, k, sel, out,
                           Z if keep_logits else None)
