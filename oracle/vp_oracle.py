@@ -119,12 +119,14 @@ def logits(q_h: np.ndarray, K_g: np.ndarray, sm_scale: float) -> np.ndarray:
 def tempered_attention(Z: np.ndarray, tau: float) -> np.ndarray:
     """A^{(tau)}(j) = exp(Z_j / tau) / sum_j' exp(Z_j' / tau)  (Eq. (6); A1: j over all tokens).
 
-    The common factor exp(-max Z / tau) is divided out of numerator and
-    denominator, which leaves the quotient unchanged and avoids overflow.
+    Z is one head's logits [n], or [H, n] for H heads (one softmax per head, over
+    the last axis). The common factor exp(-max Z / tau) is divided out of
+    numerator and denominator, which leaves the quotient unchanged and avoids
+    overflow.
     """
     x = np.asarray(Z, dtype=np.float64) / tau
-    e = np.exp(x - x.max())
-    return e / e.sum()
+    e = np.exp(x - x.max(axis=-1, keepdims=True))
+    return e / e.sum(axis=-1, keepdims=True)
 
 
 # --------------------------------------------------------------------------
@@ -136,11 +138,8 @@ def visual_mass(Z_heads: np.ndarray, vis_pos: np.ndarray, tau: float):
     Z_heads: [H, n] logits of every query head over every cached token.
     Returns (m_head [H], M_vis, M_vis_max).
     """
-    H = Z_heads.shape[0]
-    m_head = np.empty(H, dtype=np.float64)
-    for h in range(H):
-        A = tempered_attention(Z_heads[h], tau)
-        m_head[h] = A[vis_pos].sum()
+    A = tempered_attention(Z_heads, tau)          # [H, n], one softmax per head
+    m_head = A[:, vis_pos].sum(axis=1)
     return m_head, float(m_head.mean()), float(m_head.max())
 
 
@@ -176,10 +175,8 @@ def importance_scores(Z_heads: np.ndarray, vis_pos: np.ndarray,
                       tau_score: float = 1.0) -> np.ndarray:
     """S_i = (1/H) sum_h A_{t,h}(q_t, v_i), i over visual tokens in rank order (Eq. (2), A3, A4)."""
     H = Z_heads.shape[0]
-    S = np.zeros(len(vis_pos), dtype=np.float64)
-    for h in range(H):
-        S += tempered_attention(Z_heads[h], tau_score)[vis_pos]
-    return S / H
+    A = tempered_attention(Z_heads, tau_score)    # [H, n], one softmax per head
+    return A[:, vis_pos].sum(axis=0) / H
 
 
 def select_top_k(S: np.ndarray, vis_pos: np.ndarray, k: int) -> np.ndarray:
@@ -309,10 +306,15 @@ def decode_step_sequence(q: np.ndarray, K: np.ndarray, V: np.ndarray,
         J = np.sort(np.concatenate([sel, txt_pos]))
         out = np.zeros((Hq, d), dtype=np.float64)
         if len(J):
+            # softmax over J of the same logits Z (temperature 1): the dropped
+            # visual tokens are absent, i.e. carry weight exactly zero
+            inJ = np.zeros(seq_len, dtype=bool)
+            inJ[J] = True
+            ZJ = np.where(inJ, Z, -np.inf)
+            P = np.exp(ZJ - ZJ.max(axis=1, keepdims=True))
+            P /= P.sum(axis=1, keepdims=True)
             for g in range(Hkv):
-                # the pruned context's rows of KV head g, gathered once for its G heads
-                KJ, VJ = Kf[g][J], Vf[g][J]
-                out[g * G:(g + 1) * G] = attention(qf[g * G:(g + 1) * G], KJ, VJ, sm_scale)
+                out[g * G:(g + 1) * G] = P[g * G:(g + 1) * G] @ Vf[g]
 
     return SequenceResult(m_head, M_vis, M_max, S, k, sel, out,
                           Z if keep_logits else None)
