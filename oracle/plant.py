@@ -55,9 +55,12 @@ def _group_dirs(q_b, Hkv):
 
 def _push_rows(Kb, dirs, positions, signs, eps):
     """Kb[g, pos] += sign * eps * dirs[g] for every KV head g, re-rounded in place."""
-    for pos, sgn in zip(positions, signs):
-        row = _to_f32(Kb[:, pos, :]) + np.float32(sgn * eps) * dirs
-        Kb[:, pos, :] = _round_like(row, Kb.dtype)
+    pos = np.asarray(positions, dtype=np.int64)
+    if pos.size == 0:
+        return
+    step = (np.asarray(signs, dtype=np.float64) * eps).astype(np.float32)       # [n]
+    rows = _to_f32(Kb[:, pos, :]) + step[None, :, None] * dirs[:, None, :]       # [Hkv, n, d]
+    Kb[:, pos, :] = _round_like(rows, Kb.dtype)
 
 
 def margin_ok(M_max, n_vis, params: O.OracleParams, mu=MU) -> bool:
@@ -128,6 +131,67 @@ def plant_sequence(q_b, K_b, V_b, seq_len, segments, params: O.OracleParams,
         _push_rows(K_b, dirs, pos, sgn, PUSH)
         edits.extend(("gap", int(p)) for p in pos)
     raise RuntimeError("score gap could not be planted")
+
+
+def plant_loop_step(q_b, K_b, Kf_b, V_b, Vf_b, seq_len, segments, params: O.OracleParams,
+                    max_iter=12, with_output=True):
+    """Planting for one step of a decode loop whose cache carries over from step
+    to step (edits made at a step stay in the cache for the later steps).
+
+    K_b / V_b hold the stored rows [Hkv, S, d] (K_b edited in place, re-rounded to
+    the stored precision as in plant_sequence); Kf_b / Vf_b are their float64
+    copies, which the caller keeps equal to the stored values (this function
+    updates Kf_b for the rows it edits). Between edits the Eq. (6) logits are
+    updated for the edited rows only, and the masses, the budget and the Eq. (2)
+    scores are recomputed from them with the reference's own functions; the
+    result returned is a fresh reference evaluation of the planted step.
+    A budget margin that does not hold is planted by plant_sequence.
+
+    Returns (edited positions, SequenceResult of the planted step).
+    """
+    Hkv = K_b.shape[0]
+    Hq, d = q_b.shape
+    G = Hq // Hkv
+    sm = params.sm_scale if params.sm_scale is not None else 1.0 / math.sqrt(d)
+    vis_pos = O.visual_positions(seq_len, segments)
+    n_vis = len(vis_pos)
+    r = O.decode_step_sequence(q_b, Kf_b, Vf_b, seq_len, segments, params, keep_logits=True, with_output=False)
+    if not margin_ok(r.M_vis_max, n_vis, params):
+        _, edits = plant_sequence(q_b, K_b, V_b, seq_len, segments, params, max_iter=max_iter)
+        pos = sorted({p for _, p in edits})
+        if pos:
+            Kf_b[:, pos] = O.as_f64(K_b[:, pos])
+        return pos, O.decode_step_sequence(q_b, Kf_b, Vf_b, seq_len, segments, params, with_output=with_output)
+    if boundary_gap(r.scores, vis_pos, r.k) >= GAP:
+        if with_output:
+            r = O.decode_step_sequence(q_b, Kf_b, Vf_b, seq_len, segments, params)
+        return [], r
+    dirs = _group_dirs(q_b, Hkv)
+    qf = O.as_f64(q_b)
+    Z = r.Z
+    S, k = r.scores, r.k
+    edited = set()
+    for _ in range(max_iter):
+        order = np.lexsort((vis_pos, -S))
+        theta = math.sqrt(S[order[k - 1]] * S[order[k]])
+        lg = np.abs(np.log(np.maximum(S, 1e-300) / theta))
+        rank = np.empty(n_vis, dtype=np.int64)
+        rank[order] = np.arange(n_vis)
+        band = np.nonzero(lg < BAND)[0]
+        pos = vis_pos[band]
+        _push_rows(K_b, dirs, pos, np.where(rank[band] < k, 1.0, -1.0), PUSH)
+        Kf_b[:, pos] = O.as_f64(K_b[:, pos])
+        edited.update(int(p) for p in pos)
+        for g in range(Hkv):
+            Z[g * G:(g + 1) * G, pos] = O.logits(qf[g * G:(g + 1) * G], Kf_b[g, pos], sm)
+        _, _, M_max = O.visual_mass(Z, vis_pos, params.tau_mass)
+        k = O.budget(M_max, n_vis, params.r_lo_bp, params.r_hi_bp, params.clamp)
+        S = O.importance_scores(Z, vis_pos, params.tau_score)
+        if margin_ok(M_max, n_vis, params) and boundary_gap(S, vis_pos, k) >= GAP:
+            r = O.decode_step_sequence(q_b, Kf_b, Vf_b, seq_len, segments, params, with_output=with_output)
+            if margin_ok(r.M_vis_max, n_vis, params) and boundary_gap(r.scores, vis_pos, r.k) >= GAP:
+                return sorted(edited), r
+    raise RuntimeError("score gap could not be planted at this loop step")
 
 
 def plant(w, params: O.OracleParams, seqs=None):

@@ -71,3 +71,38 @@ def test_plant_queries_cfg2_two_queries():
         assert P.boundary_gap(r.scores, vis, r.k) >= P.GAP
         r2 = O.decode_step_sequence(w.q[0, t], w.K[0], w.V[0], L - 1 + t, segs, p, with_output=False)
         assert r2.k == r.k and list(r2.vis_idx) == list(r.vis_idx)
+
+
+def test_plant_loop_steps_of_the_72b_decode_loop():
+    """Per-step planting of the decode loop (a few steps past the point where the
+    drifting query has flattened the scores, so the cut needs planting): after
+    each step's planting the reference shows the gap and the margin, the float64
+    copy equals the stored rows, and the returned result is what a fresh
+    reference evaluation of the stored cache gives."""
+    s = W.Cfg5Stream(B=2, steps=48)
+    w = s.w
+    p = P.params_of(w)
+    Kf = [O.as_f64(w.K[b]) for b in range(w.B)]
+    Vf = [O.as_f64(w.V[b]) for b in range(w.B)]
+    edited = 0
+    for t in range(48):
+        q, kr, vr, pos = s.step_inputs(t)
+        w.K[:, :, pos] = kr
+        w.V[:, :, pos] = vr
+        for b in range(w.B):
+            Kf[b][:, pos] = O.as_f64(kr[b])
+            Vf[b][:, pos] = O.as_f64(vr[b])
+        if t < 40:
+            continue
+        for b in range(w.B):
+            edits, r = P.plant_loop_step(q[b], w.K[b], Kf[b], w.V[b], Vf[b], pos + 1, w.segments[b], p)
+            edited += len(edits)
+            vis = O.visual_positions(pos + 1, w.segments[b])
+            assert P.boundary_gap(r.scores, vis, r.k) >= P.GAP
+            assert P.margin_ok(r.M_vis_max, len(vis), p)
+            assert np.array_equal(Kf[b], O.as_f64(w.K[b]))
+            fresh = O.decode_step_sequence(q[b], w.K[b], w.V[b], pos + 1, w.segments[b], p)
+            assert fresh.k == r.k and np.array_equal(fresh.vis_idx, r.vis_idx)
+            np.testing.assert_allclose(fresh.scores, r.scores, rtol=1e-12)
+            np.testing.assert_allclose(fresh.out, r.out, rtol=1e-12, atol=1e-15)
+    assert edited > 0  # the loop needs planting by then
