@@ -11,12 +11,16 @@ reads, the step rotates over R distinct copies of the KV cache (R * KV bytes
 >= 1 GiB), as a real model's layers would.
 
 Prints one JSON line: steps/s, the roofline of the kernel that carries most of
-the step's bytes (the text pass: every text K and V row; HIP events that the
-step records between its launches, inside the timed steps, give its duration
-and those of the other phases) and the fp64 reference timed on this host's
-cores.
+the step's bytes (the text pass: every text K and V row; its duration comes from
+HIP events attached to that launch in steps run after the timed ones, so the
+timed steps record no events), the streaming-read ceiling measured on the same
+GPU, and the fp64 reference timed on this host's cores (one thread, and all the
+cores this process may use).
 
-Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+The default workload is config 4 (64 sequences of 32k tokens, 3.33 GB of
+algorithmic bytes per step), the largest that fits one GPU.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 4]
 """
 from __future__ import annotations
 
@@ -38,7 +42,7 @@ WORKLOAD_NAMES = {
     4: "7B-class multi-image 32k: B=64, 28/4 heads, d=128, 4 x 4096 visual + 16384 text",
     5: "72B-class decode loop: B=8, 64/8 heads, d=128, 6400 visual + 4097..4608 text over 512 steps",
 }
-DEFAULT_STEPS = {1: (200, 20), 2: (400, 40), 3: (100, 10), 4: (20, 3), 5: (512, 16)}
+DEFAULT_STEPS = {1: (200, 20), 2: (400, 40), 3: (200, 10), 4: (100, 5), 5: (512, 16)}
 
 
 class Hip:
@@ -126,45 +130,101 @@ def counter_traffic(cfg: int, kernel: str):
     return entry["traffic_bytes"]
 
 
+def stream_ceiling(hip, sp, nbytes=4 << 30, reps=5):
+    """Streaming-read ceiling of this GPU (informational): one read of a 4 GiB
+    buffer (16x the Infinity Cache) through vector loads and through the LDS
+    copies of the decode-step kernels (vp_stream_read), each timed with HIP
+    events around single launches; the best of `reps` per path."""
+    import numpy as np
+    import torch
+    from paper_2605_31457_amd import vp
+    buf = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    out = {"buffer_bytes": nbytes, "unit": "GB/s"}
+    e0, e1 = hip.event(), hip.event()
+    for mode, name in ((0, "vector_loads"), (1, "lds_copies")):
+        times = []
+        for r in range(reps + 1):
+            hip.h.hipEventRecord(e0, sp)
+            vp.vp_stream_read(buf, nbytes, mode, sink, sp)
+            hip.h.hipEventRecord(e1, sp)
+            hip.h.hipEventSynchronize(e1)
+            if r:
+                times.append(hip.elapsed_ms(e0, e1))
+        out[name] = nbytes / (min(times) * 1e-3) / 1e9
+        out[name + "_median"] = nbytes / (float(np.median(times)) * 1e-3) / 1e9
+    out["ceiling"] = max(out["vector_loads"], out["lds_copies"])
+    del buf
+    torch.cuda.empty_cache()
+    return out
+
+
+def _cores():
+    """Cores this process may use for the reference: its CPU affinity, capped by
+    OMP_NUM_THREADS when that is set (a GPU machine's share of a larger host)."""
+    n = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
+    env = os.environ.get("OMP_NUM_THREADS")
+    if env and env.isdigit() and int(env) > 0:
+        n = min(n, int(env))
+    return max(1, n)
+
+
 def cpu_baseline(w, budget_s: float, kv_groups: bool = False, gpu=None):
-    """fp64 reference on this host: whole sequences until about budget_s seconds.
+    """fp64 reference on this host, in two legs of about budget_s seconds each:
+    one thread (sequences one after another, single-threaded BLAS), then every
+    core this process may use (that many sequences at once, one thread each).
+    steps/s = sequence-steps done / wall time / B.
 
     With ``gpu`` (the GPU step's results on the same inputs, one query per
     sequence, budgets per sequence), every sequence the reference finished is
     also compared with them: parity of the measured run's outputs."""
+    from concurrent.futures import ThreadPoolExecutor
+
+    import threadpoolctl
+
     from oracle import vp_oracle as O
     from oracle.plant import params_of
     p = params_of(w)
-    t0 = time.perf_counter()
-    c0 = time.process_time()
-    n = 0
     done = {}
-    while True:
-        b = n % w.B
+
+    def one(b):
         if w.q.ndim == 4:  # several queries per sequence
-            O.decode_step_queries(w.q[b], w.K[b], w.V[b], int(w.seq_len[b]), w.segments[b], p, kv_groups=kv_groups)
-        else:
-            run = O.decode_step_sequence_kv_groups if kv_groups else O.decode_step_sequence
-            r = run(w.q[b], w.K[b], w.V[b], int(w.seq_len[b]), w.segments[b], p)
-            if b not in done:
-                done[b] = r
-        n += 1
-        el = time.perf_counter() - t0
-        if el >= budget_s and n >= 1:
-            break
-    cpu = time.process_time() - c0
-    per_seq = el / n
-    steps_per_s = 1.0 / (per_seq * w.B)
+            return O.decode_step_queries(w.q[b], w.K[b], w.V[b], int(w.seq_len[b]), w.segments[b], p,
+                                         kv_groups=kv_groups)
+        run = O.decode_step_sequence_kv_groups if kv_groups else O.decode_step_sequence
+        return run(w.q[b], w.K[b], w.V[b], int(w.seq_len[b]), w.segments[b], p)
+
+    def leg(workers):
+        n = 0
+        t0 = time.perf_counter()
+        with threadpoolctl.threadpool_limits(1), ThreadPoolExecutor(workers) as ex:
+            while True:
+                bs = [(n + i) % w.B for i in range(workers)]
+                for b, r in zip(bs, ex.map(one, bs)):
+                    if w.q.ndim == 3 and b not in done:
+                        done[b] = r
+                n += workers
+                el = time.perf_counter() - t0
+                if el >= budget_s:
+                    break
+        return {"value": n / el / w.B, "unit": "steps/s", "cores": workers, "sequence_steps": n,
+                "wall_s": round(el, 2)}
+
+    one_thread = leg(1)
+    cores = _cores()
+    all_cores = leg(cores) if cores > 1 else dict(one_thread)
     model = ""
     try:
         with open("/proc/cpuinfo") as fh:
             model = next((ln.split(":", 1)[1].strip() for ln in fh if ln.startswith("model name")), "")
     except OSError:
         pass
-    out = {"value": steps_per_s, "unit": "steps/s", "cores": max(1, round(cpu / el)), "kind": "oracle",
-           "host_cpu": model,
-           "sample": f"{n} sequence-steps of this workload's batch (sequences 0..{min(n, w.B) - 1}), "
-                     f"{el:.1f} s wall; steps/s = 1 / (mean time per sequence x B={w.B})"}
+    out = {"value": all_cores["value"], "unit": "steps/s", "cores": all_cores["cores"], "kind": "oracle",
+           "host_cpu": model, "one_thread": one_thread, "all_cores": all_cores,
+           "sample": f"whole sequence-steps of this workload's batch, sequences 0, 1, ... in turn: "
+                     f"{one_thread['sequence_steps']} on one thread in {one_thread['wall_s']} s, then "
+                     f"{all_cores['sequence_steps']} on {all_cores['cores']} threads (one sequence each, "
+                     f"single-threaded BLAS) in {all_cores['wall_s']} s; steps/s = sequence-steps / s / B={w.B}"}
     if gpu is not None and w.q.ndim == 3 and not kv_groups:
         out["parity_of_measured_run"] = measured_parity(w, gpu, done, p, O)
     return out
@@ -309,9 +369,10 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=None)
-    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--config", type=int, default=4, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--rotate", type=int, default=0, help="KV copies to rotate over (0: >= 1 GiB)")
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="seconds of reference work per leg (one thread, then all cores)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calls", action="store_true", help="time the four separate calls instead of vp_decode_step")
     ap.add_argument("--layers", type=int, default=1,
@@ -424,18 +485,12 @@ def main():
         return
     # step events: [0] visual pass [1] text pass [2] tail [3] kept pass [4] merge [5].
     # An event record costs microseconds of queue time, which shows on small
-    # steps, so the timed steps record only the two around the text pass (the
-    # roofline kernel), and only on every `stride`-th step (at most 50 samples);
-    # the per-phase split comes from separate steps after the timed ones.
+    # steps, so the timed steps record none; the roofline launch's duration and
+    # the per-phase split come from further steps run after the timed ones.
     NEV = vp.VP_STEP_EVENTS
-    stride = max(1, steps // 50)
-    evs_all = [[None, hip.event(), hip.event(), None, None, None] if i % stride == 0 else [None] * NEV
-               for i in range(steps)]
-    n_phase = min(steps, 50)
+    n_phase = 50
     evs_phase = [[hip.event() for _ in range(NEV)] for _ in range(n_phase)]
-    # argument arrays built ahead of the timed loop
-    arr_all = [vp.event_array(e) if e[1] is not None else () for e in evs_all]
-    arr_all3 = [vp.event_array(e[:3]) if e[1] is not None else () for e in evs_all]
+    # argument arrays built ahead of the runs
     arr_phase = [vp.event_array(e) for e in evs_phase]
     arr_phase3 = [vp.event_array(e[:3]) for e in evs_phase]
     ev_t0, ev_t1 = hip.event(), hip.event()
@@ -488,22 +543,20 @@ def main():
             graph.replay()
     else:
         for i in range(steps):
-            one_step(warmup + i, evs_all[i], arr_all[i], arr_all3[i])
+            one_step(warmup + i)
     hip.h.hipEventRecord(ev_t1, sp)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     gpu_ms = hip.elapsed_ms(ev_t0, ev_t1)
-    if graph is None:
-        text_ms = float(np.mean([hip.elapsed_ms(e[1], e[2]) for e in evs_all if e[1] is not None]))
     for i in range(n_phase):
         one_step(warmup + steps + i, evs_phase[i], arr_phase[i], arr_phase3[i])
     torch.cuda.synchronize()
 
     def phase(i, j):
         return float(np.mean([hip.elapsed_ms(e[i], e[j]) for e in evs_phase]))
-    vis_ms, tail_ms, attn_ms = phase(0, 1), phase(2, 3), phase(3, 5)
-    if graph is not None:
-        text_ms = phase(1, 2)  # the roofline launch, from the eager steps after the replays
+    # [1]..[2]: the roofline launch's execution alone (events attached to it)
+    vis_ms, text_ms, tail_ms, attn_ms = phase(0, 1), phase(1, 2), phase(2, 3), phase(3, 5)
+    ceiling = stream_ceiling(hip, sp)
     if loop is None:
         assert np.array_equal(ds.k.cpu().numpy(), ks), "budget changed between warm-up and timed steps"
 
@@ -551,7 +604,12 @@ def main():
                      "achieved": achieved, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": achieved / PEAK_HBM_GBS,
                      "traffic": counter_traffic(cfg, "one_launch" if one_launch else "text"),
                      "algorithmic_bytes_per_launch": roof_bytes,
-                     "avg_launch_ms": text_ms, "share_of_step": text_ms / ms_per_step},
+                     "avg_launch_ms": text_ms, "share_of_step": text_ms / ms_per_step,
+                     "launch_time_source": f"HIP events attached to the launch, mean of {n_phase} steps run "
+                                           "after the timed ones",
+                     "frac_of_measured_ceiling": achieved / ceiling["ceiling"]},
+        "stream_read_ceiling": ceiling,
+        "step_frac_of_measured_ceiling": step_gbs / ceiling["ceiling"],
         # separate visual launch: [0]..[1] runs from before it to the text pass's start
         "visual_pass": None if one_launch else {"achieved": nb["visual"] / (vis_ms * 1e-3) / 1e9, "unit": "GB/s",
                                                 "algorithmic_bytes_per_launch": nb["visual"],

@@ -17,9 +17,15 @@
  * Conventions shared by every call
  * --------------------------------
  * Memory.   All tensor arguments are DEVICE pointers owned by the caller; the
- *           library allocates nothing and keeps no state between calls, so it
- *           is reentrant. Scratch memory is the caller's workspace, sized by
- *           vp_workspace_size().
+ *           library allocates nothing. Scratch memory is the caller's
+ *           workspace, sized by vp_workspace_size().
+ * State.    No device state is carried from one call to the next: every call
+ *           leaves its results in the caller's buffers. The host side keeps
+ *           two things: the detail of the last error, per calling thread
+ *           (vp_last_error); per-kernel LDS figures read from the HIP runtime on
+ *           first use and cached for the process (one GPU model per process is
+ *           assumed). Calls from several threads are safe as long as they do
+ *           not share a workspace.
  * Streams.  `stream` is a hipStream_t (NULL = the legacy default stream). Every
  *           call only enqueues kernels on that stream and returns; none
  *           synchronises (vp_validate_layout, a debug helper, excepted). k and
@@ -312,6 +318,18 @@ vp_status vp_step_plan(const vp_shape* shape, const vp_params* params, int32_t* 
  * fails. The only call that synchronises; not for the decode loop.
  */
 vp_status vp_validate_layout(const vp_shape* shape, const vp_layout* layout, void* stream);
+
+/*
+ * vp_stream_read -- measurement helper, not part of the method: enqueues one
+ * read of `bytes` of device memory at `src` (16-byte aligned; bytes a positive
+ * multiple of 16 KiB), so that a benchmark can time the GPU's streaming-read
+ * ceiling next to the decode step. mode 0: 16-byte vector loads into
+ * registers; mode 1: the HBM -> LDS row copies the decode-step kernels use.
+ * Both are non-temporal. `sink` is a device uint32 the kernel may write (so
+ * the loads are kept); its value means nothing. VP_ERR_SHAPE / VP_ERR_RANGE /
+ * VP_ERR_NULL for bad arguments.
+ */
+vp_status vp_stream_read(const void* src, size_t bytes, int32_t mode, uint32_t* sink, void* stream);
 
 /* Host mirror of vp_budget's rule for one sequence (pure; for callers that keep
  * the mass on the host). Returns -1 for invalid parameters. */

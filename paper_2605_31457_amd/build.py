@@ -15,7 +15,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libvisionpulse.so")
 
-SOURCES = ["vp_api.hip", "vp_plan.hip", "vp_attend.hip", "vp_mass.hip", "vp_topk.hip", "vp_select.hip", "vp_merge.hip"]
+SOURCES = ["vp_api.hip", "vp_plan.hip", "vp_attend.hip", "vp_mass.hip", "vp_topk.hip", "vp_select.hip", "vp_merge.hip", "vp_stream.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

@@ -10,6 +10,7 @@
 
 #include "vp_internal.h"
 
+
 namespace vp {
 namespace {
 
@@ -29,6 +30,7 @@ vp_status fail(vp_status s, const char* fmt, ...) {
 vp_status hip_fail(hipError_t e, const char* what) {
   return fail(VP_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
+
 
 constexpr int kMaxGroup = 16;
 constexpr int kMaxHq = kMaxHq_;
@@ -261,6 +263,62 @@ vp_status check_budget_cap(const vp_shape* s, const vp_params* p) {
   return VP_OK;
 }
 
+// Host checks of a whole decode step's arguments (everything but the workspace).
+vp_status check_step_args(const vp_shape* shape, const vp_layout* layout, const vp_params* params, const void* q,
+                          const void* K, const void* V, const float* mass_head, const float* mass_seq,
+                          const float* scores, const int32_t* k, const int32_t* vis_idx, const void* out) {
+  if (vp_status e = check_shape(shape)) return e;
+  if (vp_status e = check_layout(shape, layout)) return e;
+  if (vp_status e = check_params(params)) return e;
+  if (!q || !K || !V || !mass_head || !mass_seq || !scores || !k || !vis_idx || !out)
+    return fail(VP_ERR_NULL, "q, K, V, mass_head, mass_seq, scores, k, vis_idx, out required");
+  if (!aligned16(q) || !aligned16(K) || !aligned16(V)) return fail(VP_ERR_SHAPE, "q, K, V must be 16-byte aligned");
+  return check_budget_cap(shape, params);
+}
+
+// The launches of one decode step (validated arguments; ws holds plan.total bytes):
+// the context pass, the select launch, the kept-row pass and the merge.
+vp_status launch_step(const vp_shape* shape, const vp_layout* layout, const vp_params* params, const Plan& plan,
+                      char* ws, const void* q, const void* K, const void* V, float* mass_head, float* mass_seq,
+                      float* scores, int32_t* k, int32_t* vis_idx, void* out, hipStream_t st, void* const* events,
+                      int32_t n_events) {
+  AttendArgs a = attend_args(shape, layout, params, plan, ws, q, K, V);
+  a.vis_idx = vis_idx;
+  a.kk = k;
+  auto mark = [&](int i) -> hipError_t {
+    return (i < n_events && events[i]) ? hipEventRecord(static_cast<hipEvent_t>(events[i]), st) : hipSuccess;
+  };
+  const int dt = shape->dtype, hd = shape->head_dim;
+  // events [1] and [2] ride on the text (or one) context launch: its execution alone
+  auto ev = [&](int i) -> hipEvent_t { return i < n_events ? static_cast<hipEvent_t>(events[i]) : nullptr; };
+  if (hipError_t e = mark(0)) return hip_fail(e, "event record");
+  if (use_dual(shape)) {
+    if (hipError_t e = launch_attend(a, MODE_DUAL, dt, hd, st, ev(1), ev(2))) return hip_fail(e, "context pass launch");
+  } else {
+    if (hipError_t e = launch_attend(a, MODE_VIS, dt, hd, st)) return hip_fail(e, "visual pass launch");
+    if (hipError_t e = launch_attend(a, MODE_TEXT_BOTH, dt, hd, st, ev(1), ev(2))) return hip_fail(e, "text pass launch");
+  }
+  SelectArgs t{};
+  t.m = mass_args(shape, layout, plan, a, ws, mass_head, mass_seq, scores);
+  t.r_lo_bp = params->r_lo_bp;
+  t.r_hi_bp = params->r_hi_bp;
+  t.clamp = params->clamp;
+  t.k_cap = shape->k_cap;
+  t.k = k;
+  t.vis_idx = vis_idx;
+  t.chunk = plan.sel_chunk;
+  t.nchunks = plan.sel_chunks;
+  t.sync = a.sync;
+  t.segtab = a.segtab;
+  if (hipError_t e = launch_select(t, st)) return hip_fail(e, "select launch");
+  if (hipError_t e = mark(3)) return hip_fail(e, "event record");
+  if (hipError_t e = launch_attend(a, MODE_KEPT, dt, hd, st)) return hip_fail(e, "kept pass launch");
+  if (hipError_t e = mark(4)) return hip_fail(e, "event record");
+  if (hipError_t e = launch_merge(merge_args(shape, layout, plan, a, k, out), hd, st)) return hip_fail(e, "merge launch");
+  if (hipError_t e = mark(5)) return hip_fail(e, "event record");
+  return VP_OK;
+}
+
 }  // namespace vp
 
 using namespace vp;
@@ -435,6 +493,17 @@ vp_status vp_validate_layout(const vp_shape* shape, const vp_layout* layout, voi
   return VP_OK;
 }
 
+vp_status vp_stream_read(const void* src, size_t bytes, int32_t mode, uint32_t* sink, void* stream) {
+  g_last_error.clear();
+  if (!src || !sink) return fail(VP_ERR_NULL, "src and sink required");
+  if (!aligned16(src)) return fail(VP_ERR_SHAPE, "src must be 16-byte aligned");
+  if (bytes == 0 || bytes % (16u << 10) != 0) return fail(VP_ERR_SHAPE, "bytes %zu: a positive multiple of 16 KiB", bytes);
+  if (mode != 0 && mode != 1) return fail(VP_ERR_RANGE, "mode %d: 0 (vector loads) or 1 (LDS copies)", mode);
+  if (hipError_t e = launch_stream_read(src, bytes, mode, sink, static_cast<hipStream_t>(stream)))
+    return hip_fail(e, "stream read launch");
+  return VP_OK;
+}
+
 vp_status vp_step_plan(const vp_shape* shape, const vp_params* params, int32_t* flags) {
   g_last_error.clear();
   if (vp_status e = check_shape(shape)) return e;
@@ -504,52 +573,12 @@ vp_status vp_decode_step(const vp_shape* shape, const vp_layout* layout, const v
   if (n_events < 0 || n_events > VP_STEP_EVENTS)
     return fail(VP_ERR_RANGE, "n_events %d outside [0, %d]", n_events, VP_STEP_EVENTS);
   if (n_events > 0 && !events) return fail(VP_ERR_NULL, "events is NULL with n_events %d", n_events);
-  if (vp_status e = check_shape(shape)) return e;
-  if (vp_status e = check_layout(shape, layout)) return e;
-  if (vp_status e = check_params(params)) return e;
-  if (!q || !K || !V || !mass_head || !mass_seq || !scores || !k || !vis_idx || !out)
-    return fail(VP_ERR_NULL, "q, K, V, mass_head, mass_seq, scores, k, vis_idx, out required");
-  if (!aligned16(q) || !aligned16(K) || !aligned16(V)) return fail(VP_ERR_SHAPE, "q, K, V must be 16-byte aligned");
-  if (vp_status e = check_budget_cap(shape, params)) return e;
+  if (vp_status e = check_step_args(shape, layout, params, q, K, V, mass_head, mass_seq, scores, k, vis_idx, out))
+    return e;
   Plan plan;
   if (vp_status e = check_ws(shape, workspace, workspace_bytes, plan)) return e;
-  hipStream_t st = static_cast<hipStream_t>(stream);
-  char* ws = static_cast<char*>(workspace);
-  AttendArgs a = attend_args(shape, layout, params, plan, ws, q, K, V);
-  a.vis_idx = vis_idx;
-  a.kk = k;
-  auto mark = [&](int i) -> hipError_t {
-    return (i < n_events && events[i]) ? hipEventRecord(static_cast<hipEvent_t>(events[i]), st) : hipSuccess;
-  };
-  const int dt = shape->dtype, hd = shape->head_dim;
-  // events [1] and [2] ride on the text (or one) context launch: its execution alone
-  auto ev = [&](int i) -> hipEvent_t { return i < n_events ? static_cast<hipEvent_t>(events[i]) : nullptr; };
-  if (hipError_t e = mark(0)) return hip_fail(e, "event record");
-  if (use_dual(shape)) {
-    if (hipError_t e = launch_attend(a, MODE_DUAL, dt, hd, st, ev(1), ev(2))) return hip_fail(e, "context pass launch");
-  } else {
-    if (hipError_t e = launch_attend(a, MODE_VIS, dt, hd, st)) return hip_fail(e, "visual pass launch");
-    if (hipError_t e = launch_attend(a, MODE_TEXT_BOTH, dt, hd, st, ev(1), ev(2))) return hip_fail(e, "text pass launch");
-  }
-  SelectArgs t{};
-  t.m = mass_args(shape, layout, plan, a, ws, mass_head, mass_seq, scores);
-  t.r_lo_bp = params->r_lo_bp;
-  t.r_hi_bp = params->r_hi_bp;
-  t.clamp = params->clamp;
-  t.k_cap = shape->k_cap;
-  t.k = k;
-  t.vis_idx = vis_idx;
-  t.chunk = plan.sel_chunk;
-  t.nchunks = plan.sel_chunks;
-  t.sync = a.sync;
-  t.segtab = a.segtab;
-  if (hipError_t e = launch_select(t, st)) return hip_fail(e, "select launch");
-  if (hipError_t e = mark(3)) return hip_fail(e, "event record");
-  if (hipError_t e = launch_attend(a, MODE_KEPT, dt, hd, st)) return hip_fail(e, "kept pass launch");
-  if (hipError_t e = mark(4)) return hip_fail(e, "event record");
-  if (hipError_t e = launch_merge(merge_args(shape, layout, plan, a, k, out), hd, st)) return hip_fail(e, "merge launch");
-  if (hipError_t e = mark(5)) return hip_fail(e, "event record");
-  return VP_OK;
+  return launch_step(shape, layout, params, plan, static_cast<char*>(workspace), q, K, V, mass_head, mass_seq, scores,
+                     k, vis_idx, out, static_cast<hipStream_t>(stream), events, n_events);
 }
 
 }  // extern "C"

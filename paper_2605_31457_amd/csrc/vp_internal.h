@@ -204,6 +204,9 @@ struct MergeArgs {
 
 hipError_t launch_merge(const MergeArgs& a, int head_dim, hipStream_t st);
 
+// one read of `bytes` (a multiple of 16 KiB) at src: mode 0 vector loads, 1 LDS copies
+hipError_t launch_stream_read(const void* src, size_t bytes, int mode, uint32_t* sink, hipStream_t st);
+
 // kept-row budget helpers shared by host validation and the budget kernel
 __host__ __device__ inline int ceil_bp(long n, int bp) { return static_cast<int>((static_cast<long>(bp) * n + 9999) / 10000); }
 __host__ __device__ inline int floor_bp(long n, int bp) { return static_cast<int>((static_cast<long>(bp) * n) / 10000); }

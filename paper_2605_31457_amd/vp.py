@@ -75,6 +75,7 @@ def lib() -> ctypes.CDLL:
             "vp_validate_layout": ([P(vp_shape), P(vp_layout), V], ctypes.c_int),
             "vp_decode_step": ([P(vp_shape), P(vp_layout), P(vp_params), V, V, V, V, V, V, V, V, V, V, S, V,
                                 ctypes.POINTER(V), ctypes.c_int32], ctypes.c_int),
+            "vp_stream_read": ([V, S, ctypes.c_int32, V, V], ctypes.c_int),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -205,3 +206,8 @@ def vp_validate_layout(shape, layout, stream=None):
 
 def vp_budget_host(m_max: float, n_vis: int, params: vp_params) -> int:
     return int(lib().vp_budget_host(float(m_max), int(n_vis), ctypes.byref(params)))
+
+
+def vp_stream_read(src, nbytes, mode, sink, stream=None):
+    """Measurement helper: one read of nbytes at src (mode 0 vector loads, 1 LDS copies)."""
+    _check("vp_stream_read", lib().vp_stream_read(_p(src), int(nbytes), int(mode), _p(sink), _stream(stream)))

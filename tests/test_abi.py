@@ -226,3 +226,15 @@ def test_budget_host_mirror_matches_table(L, m, n, lo, hi, c, k):
 
 def test_budget_host_rejects_bad_params(L):
     assert vp.vp_budget_host(0.5, 100, _params(tau_mass=-1.0)) == -1
+
+
+def test_stream_read_rejects_bad_arguments(L):
+    fake = 0x10000
+    with pytest.raises(vp.VPError, match="VP_ERR_NULL"):
+        vp.vp_stream_read(None, 1 << 20, 0, fake, 0)
+    with pytest.raises(vp.VPError, match="VP_ERR_SHAPE"):
+        vp.vp_stream_read(fake, (1 << 20) + 16, 0, fake, 0)   # not a multiple of 16 KiB
+    with pytest.raises(vp.VPError, match="VP_ERR_SHAPE"):
+        vp.vp_stream_read(fake + 8, 1 << 20, 1, fake, 0)       # misaligned
+    with pytest.raises(vp.VPError, match="VP_ERR_RANGE"):
+        vp.vp_stream_read(fake, 1 << 20, 2, fake, 0)
