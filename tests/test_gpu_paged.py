@@ -111,3 +111,31 @@ def test_paged_later_layer_dense_attention():
     sm = 1.0 / np.sqrt(wl.d)
     want = np.stack([O.pruned_attention(qf[h], wl.K[0, h // G], wl.V[0, h // G], J, sm) for h in range(wl.Hq)])
     np.testing.assert_allclose(got, want, atol=2e-2, rtol=1e-2)
+
+
+def test_paged_two_launch_plan():
+    """A batch past the one-launch limit of the context pass (16 sequences x 64
+    KV heads x 35 tiles > 32768 tiles), so the visual and text passes run as two
+    launches, both reading rows through the block table: bit-identical to the
+    contiguous caches and checked against the reference."""
+    rng = np.random.default_rng(71)
+    lens = [int(x) for x in rng.integers(1000, 1101, size=16)]
+    segs = [[(10, 300), (400, 250)] for _ in range(16)]
+    w = small_workload(seed=71, B=16, Hq=128, Hkv=64, d=64, lens=lens, segs=segs, S_cap=1100)
+    ref, _ = P.plant(w, P.params_of(w))
+    flat = S.DeviceStep(w)
+    from paper_2605_31457_amd import vp
+    assert not vp.vp_step_plan(flat.shape, flat.params) & vp.VP_PLAN_ONE_CONTEXT_LAUNCH
+    flat.decode_step()
+    a = flat.results()
+    paged = S.DeviceStep(w, block_size=32, block_seed=5)
+    paged.decode_step()
+    g = paged.results()
+    _same(a, g, "two-launch P=32")
+    for b in range(w.B):
+        check_sequence("paged two-launch", w, g, b, ref[b])
+    for fused in (True, False):
+        paged.run(fused=fused)
+        flat.run(fused=fused)
+        _same(flat.results(), paged.results(), f"two-launch P=32 calls fused={fused}")
+    _log(f"paged two-launch: k={[ref[b].k for b in range(4)]}...")
