@@ -18,14 +18,16 @@
  * --------------------------------
  * Memory.   All tensor arguments are DEVICE pointers owned by the caller; the
  *           library allocates nothing. Scratch memory is the caller's
- *           workspace, sized by vp_workspace_size().
+ *           workspace, sized by vp_workspace_size() (vp_decode_step_static
+ *           alone uses the library's own scratch instead, see there).
  * State.    No device state is carried from one call to the next: every call
  *           leaves its results in the caller's buffers. The host side keeps
- *           two things: the detail of the last error, per calling thread
+ *           three things: the detail of the last error, per calling thread
  *           (vp_last_error); per-kernel LDS figures read from the HIP runtime on
  *           first use and cached for the process (one GPU model per process is
- *           assumed). Calls from several threads are safe as long as they do
- *           not share a workspace.
+ *           assumed); and, per device, the address of vp_decode_step_static's
+ *           scratch array. Calls from several threads are safe as long as they
+ *           do not share a workspace (or, for vp_decode_step_static, a GPU).
  * Streams.  `stream` is a hipStream_t (NULL = the legacy default stream). Every
  *           call only enqueues kernels on that stream and returns; none
  *           synchronises (vp_validate_layout, a debug helper, excepted). k and
@@ -289,6 +291,33 @@ vp_status vp_decode_step(const vp_shape* shape, const vp_layout* layout, const v
                          float* mass_head, float* mass_seq, float* scores, int32_t* k, int32_t* vis_idx,
                          void* out, void* workspace, size_t workspace_bytes, void* stream,
                          void* const* events, int32_t n_events);
+
+/*
+ * vp_decode_step_static -- vp_decode_step for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops and harnesses that
+ * forbid hipMalloc): the same launches and results, bit for bit, with the
+ * library's own scratch in place of the caller's workspace. The scratch is a
+ * device array of VP_STATIC_SCRATCH_BYTES that every GPU the library runs on
+ * holds until the process ends; its address is looked up once per device, on
+ * the first call with that device current. This call allocates nothing and
+ * records no events. The stream must belong to the current device.
+ *
+ * The scratch keeps the last call's contents; nothing in it needs to start at
+ * zero (every step writes what it later reads). All calls on one GPU share it,
+ * so calls that may overlap on one GPU (several streams or threads) race and
+ * must be serialised by the caller.
+ *
+ * Errors: as vp_decode_step; VP_ERR_WORKSPACE, before anything is enqueued,
+ * when vp_workspace_size(shape) exceeds VP_STATIC_SCRATCH_BYTES (the 16-sequence
+ * 12k-token batch of the 7B shape needs about 29 MiB; 64 sequences of 32k
+ * tokens need 270 MiB and must use vp_decode_step); VP_ERR_HIP if the scratch
+ * address cannot be obtained.
+ */
+#define VP_STATIC_SCRATCH_BYTES (32u << 20)
+vp_status vp_decode_step_static(const vp_shape* shape, const vp_layout* layout, const vp_params* params,
+                                const void* q, const void* K, const void* V,
+                                float* mass_head, float* mass_seq, float* scores, int32_t* k, int32_t* vis_idx,
+                                void* out, void* stream);
 
 /*
  * vp_step_plan -- how vp_visual_mass (with V) and vp_decode_step will launch

@@ -1,15 +1,22 @@
 // C ABI of the VisionPulse decode-step path: argument validation, workspace
 // carving and kernel launches on the caller's stream (no allocation, no sync).
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
 #include "vp_internal.h"
 
+// Scratch memory of vp_decode_step_static: each GPU the library runs on holds
+// one copy of this array until the process ends. Host code never uses its name
+// as an address (on the host it is only a stand-in for the symbol): the device
+// address comes from hipGetSymbolAddress, once per device.
+static __device__ __align__(256) unsigned char scratch[VP_STATIC_SCRATCH_BYTES];
 
 namespace vp {
 namespace {
@@ -31,6 +38,29 @@ vp_status hip_fail(hipError_t e, const char* what) {
   return fail(VP_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
 }
 
+// Device address of `scratch` on the current device: looked up on the first
+// call for that device (with it current) and kept.
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+std::mutex g_scratch_mu;
+
+vp_status static_scratch(void** ptr) {
+  int dev = -1;
+  if (hipError_t e = hipGetDevice(&dev)) return hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(VP_ERR_UNSUPPORTED, "device %d >= %d", dev, kMaxDevices);
+  void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (!p) {
+      if (hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch))) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+      if (!p) return fail(VP_ERR_HIP, "hipGetSymbolAddress(scratch) returned NULL");
+      g_scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *ptr = p;
+  return VP_OK;
+}
 
 constexpr int kMaxGroup = 16;
 constexpr int kMaxHq = kMaxHq_;
@@ -579,6 +609,24 @@ vp_status vp_decode_step(const vp_shape* shape, const vp_layout* layout, const v
   if (vp_status e = check_ws(shape, workspace, workspace_bytes, plan)) return e;
   return launch_step(shape, layout, params, plan, static_cast<char*>(workspace), q, K, V, mass_head, mass_seq, scores,
                      k, vis_idx, out, static_cast<hipStream_t>(stream), events, n_events);
+}
+
+vp_status vp_decode_step_static(const vp_shape* shape, const vp_layout* layout, const vp_params* params, const void* q,
+                                const void* K, const void* V, float* mass_head, float* mass_seq, float* scores,
+                                int32_t* k, int32_t* vis_idx, void* out, void* stream) {
+  g_last_error.clear();
+  if (vp_status e = check_step_args(shape, layout, params, q, K, V, mass_head, mass_seq, scores, k, vis_idx, out))
+    return e;
+  const Plan plan = make_plan(*shape);
+  if (plan.total > static_cast<size_t>(VP_STATIC_SCRATCH_BYTES))
+    return fail(VP_ERR_WORKSPACE,
+                "this shape needs %zu bytes of scratch; the static scratch holds %zu (use vp_decode_step with a "
+                "workspace of vp_workspace_size bytes)",
+                plan.total, static_cast<size_t>(VP_STATIC_SCRATCH_BYTES));
+  void* ws = nullptr;
+  if (vp_status e = static_scratch(&ws)) return e;
+  return launch_step(shape, layout, params, plan, static_cast<char*>(ws), q, K, V, mass_head, mass_seq, scores, k,
+                     vis_idx, out, static_cast<hipStream_t>(stream), nullptr, 0);
 }
 
 }  // extern "C"

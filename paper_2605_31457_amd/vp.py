@@ -76,6 +76,8 @@ def lib() -> ctypes.CDLL:
             "vp_decode_step": ([P(vp_shape), P(vp_layout), P(vp_params), V, V, V, V, V, V, V, V, V, V, S, V,
                                 ctypes.POINTER(V), ctypes.c_int32], ctypes.c_int),
             "vp_stream_read": ([V, S, ctypes.c_int32, V, V], ctypes.c_int),
+            "vp_decode_step_static": ([P(vp_shape), P(vp_layout), P(vp_params), V, V, V, V, V, V, V, V, V, V],
+                                       ctypes.c_int),
         }
         for name, (args, res) in sig.items():
             f = getattr(L, name)
@@ -163,6 +165,17 @@ def vp_decode_step(shape, layout, params, q, K, V, mass_head, mass_seq, scores, 
         ctypes.byref(shape), ctypes.byref(layout), ctypes.byref(params), _p(q), _p(K), _p(V),
         _p(mass_head), _p(mass_seq), _p(scores), _p(k), _p(vis_idx), _p(out), _p(workspace), nbytes,
         _stream(stream), arr, n))
+
+
+VP_STATIC_SCRATCH_BYTES = 32 << 20
+
+
+def vp_decode_step_static(shape, layout, params, q, K, V, mass_head, mass_seq, scores, k, vis_idx, out,
+                          stream=None):
+    """vp_decode_step on the library's own per-device scratch (no workspace, no allocation)."""
+    _check("vp_decode_step_static", lib().vp_decode_step_static(
+        ctypes.byref(shape), ctypes.byref(layout), ctypes.byref(params), _p(q), _p(K), _p(V),
+        _p(mass_head), _p(mass_seq), _p(scores), _p(k), _p(vis_idx), _p(out), _stream(stream)))
 
 
 def vp_budget(shape, layout, params, mass_seq, k, stream=None):

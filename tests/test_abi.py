@@ -238,3 +238,22 @@ def test_stream_read_rejects_bad_arguments(L):
         vp.vp_stream_read(fake + 8, 1 << 20, 1, fake, 0)       # misaligned
     with pytest.raises(vp.VPError, match="VP_ERR_RANGE"):
         vp.vp_stream_read(fake, 1 << 20, 2, fake, 0)
+
+
+def test_static_scratch_step_refuses_before_launch(L):
+    """vp_decode_step_static checks its arguments, and that the shape's scratch
+    fits the library's static array, before touching the GPU."""
+    fake = 0x10000
+    lay, p = _layout(), _params()
+    big = _shape(batch=64, max_seq_len=32768, max_vis=16384, max_segs=4, k_cap=819,
+                 kv_stride_b=4 * 32768 * 128, kv_stride_h=32768 * 128)
+    assert vp.vp_workspace_size(big) > vp.VP_STATIC_SCRATCH_BYTES
+    args = [fake] * 9
+    with pytest.raises(vp.VPError, match="VP_ERR_WORKSPACE"):
+        vp.vp_decode_step_static(big, lay, p, *args, stream=0)
+    with pytest.raises(vp.VPError, match="VP_ERR_NULL"):
+        vp.vp_decode_step_static(_shape(), lay, p, fake, fake, None, *([fake] * 6), stream=0)
+    with pytest.raises(vp.VPError, match="VP_ERR_SHAPE"):
+        vp.vp_decode_step_static(_shape(k_cap=10), lay, p, *args, stream=0)
+    m = re.search(r"#define\s+VP_STATIC_SCRATCH_BYTES\s+\((\d+)u << (\d+)\)", open(HEADER).read())
+    assert m and vp.VP_STATIC_SCRATCH_BYTES == int(m.group(1)) << int(m.group(2))

@@ -1,0 +1,68 @@
+"""vp_decode_step_static, the decode step that allocates nothing (its scratch is
+a per-device array inside the library), against vp_decode_step with a caller
+workspace: every output identical, bit for bit, on two calls in a row, the
+second with a smaller input; and a shape beyond the static scratch refused
+before anything is enqueued."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2605_31457_amd import step as S
+from paper_2605_31457_amd import vp
+from paper_2605_31457_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+KEYS = ("mass_head", "mass_seq", "scores", "k", "vis_idx", "out")
+
+
+def _static_step(ds):
+    vp.vp_decode_step_static(ds.shape, ds.layout, ds.params, ds.q, ds.K, ds.V, ds.mass_head, ds.mass_seq, ds.scores,
+                             ds.k, ds.vis_idx, ds.out)
+
+
+def _clear(ds):
+    for t in (ds.mass_head, ds.mass_seq, ds.scores):
+        t.fill_(-3.0)
+    ds.k.fill_(-5)
+    ds.vis_idx.fill_(-7)
+    ds.out.fill_(-9.0)
+
+
+def test_static_scratch_matches_workspace_step():
+    cases = [("config 3, 16 ragged sequences", W.generate(3)), ("config 2", W.generate(2))]
+    sizes = []
+    for name, w in cases:
+        ds = S.DeviceStep(w)
+        sizes.append(ds.ws_bytes)
+        assert ds.ws_bytes <= vp.VP_STATIC_SCRATCH_BYTES, name
+        print(f"{name}: workspace {ds.ws_bytes} bytes", flush=True)
+        ds.decode_step()
+        ref = ds.results()
+        _clear(ds)
+        _static_step(ds)
+        got = ds.results()
+        for key in KEYS:
+            assert np.array_equal(got[key], ref[key]), f"{name}: {key}"
+        # and once more on the same inputs (the scratch keeps the last call's contents)
+        _clear(ds)
+        _static_step(ds)
+        again = ds.results()
+        for key in KEYS:
+            assert np.array_equal(again[key], ref[key]), f"{name} repeated: {key}"
+    assert sizes[1] < sizes[0]
+
+
+def test_static_scratch_refuses_a_larger_shape():
+    # the 64 x 32k batch needs ~270 MiB of scratch: refused before any launch
+    sh = vp.vp_shape(batch=64, n_q_heads=28, n_kv_heads=4, head_dim=128, dtype=vp.VP_BF16, max_seq_len=32768,
+                     max_vis=16384, max_segs=4, k_cap=819, block_size=0, scope=0, n_queries=1,
+                     kv_stride_b=4 * 32768 * 128, kv_stride_h=32768 * 128, kv_stride_s=128)
+    assert vp.vp_workspace_size(sh) > vp.VP_STATIC_SCRATCH_BYTES
+    dummy = torch.zeros(64, dtype=torch.int32, device="cuda")
+    lay = vp.vp_layout(seq_len=dummy.data_ptr(), vis_seg_off=dummy.data_ptr(), vis_seg=dummy.data_ptr(),
+                       block_table=None)
+    p = vp.vp_params(tau_mass=0.1, tau_score=1.0, sm_scale=0.0, r_lo_bp=100, r_hi_bp=500, clamp=1)
+    with pytest.raises(vp.VPError) as e:
+        vp.vp_decode_step_static(sh, lay, p, dummy, dummy, dummy, dummy, dummy, dummy, dummy, dummy, dummy)
+    assert e.value.status == 6 and "static scratch" in str(e.value)
