@@ -156,6 +156,37 @@ def test_repeat_runs_are_bitwise_identical():
             assert np.array_equal(first[key], again[key]), key
 
 
+def _repeat_case(name):
+    if name == "cfg4-chunked-select":
+        # 64 rows of 16384 visual ranks: the select launch scores each row in
+        # chunks on several work-groups and the last to arrive selects
+        return tile_batch(W.generate(4, seqs=[0, 1, 2, 3]), 64)
+    if name == "many-chunks-keys-in-memory":
+        # one row of 40000 visual ranks: many chunks, and the selecting
+        # work-group reads the keys back from memory (more than its LDS holds)
+        return small_workload(seed=16, B=1, Hq=4, Hkv=1, d=64, lens=[41000], segs=[[(500, 40000)]])
+    # 256 rows: one work-group per row, keys beyond its LDS read from memory
+    base = small_workload(seed=66, B=2, Hq=4, Hkv=1, d=64, lens=[40200, 300], segs=[[(100, 40000)], [(20, 200)]])
+    return tile_batch(base, 256)
+
+
+@pytest.mark.parametrize("name", ["cfg4-chunked-select", "many-chunks-keys-in-memory", "one-group-keys-in-memory"])
+def test_repeat_decode_steps_are_bitwise_identical(name):
+    """vp_decode_step's select launch hands scores between work-groups through
+    device-scope stores and an arrival counter; repeated steps on the same
+    inputs must give the same bits every time."""
+    w = _repeat_case(name)
+    ds = S.DeviceStep(w, max_vis=40000 if name == "one-group-keys-in-memory" else None)
+    ds.decode_step()
+    first = ds.results()
+    for rep in range(4):
+        ds.decode_step()
+        again = ds.results()
+        for key in first:
+            assert np.array_equal(first[key], again[key]), f"{name} repeat {rep}: {key}"
+    _log(f"repeat {name}: k={list(first['k'][:4])}")
+
+
 def test_budget_kernel_matches_rule_exactly():
     """vp_budget on given fp32 masses, including products that land exactly on
     an integer, against Eq. (7) + clamp on the same fp32 values widened."""
