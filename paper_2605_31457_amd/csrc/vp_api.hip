@@ -342,7 +342,9 @@ vp_status launch_step(const vp_shape* shape, const vp_layout* layout, const vp_p
   t.segtab = a.segtab;
   if (hipError_t e = launch_select(t, st)) return hip_fail(e, "select launch");
   if (hipError_t e = mark(3)) return hip_fail(e, "event record");
-  if (hipError_t e = launch_attend(a, MODE_KEPT, dt, hd, st)) return hip_fail(e, "kept pass launch");
+  // the kept rows are visual rows of this step's spill: their logits are read
+  // from it, so the kept pass reads V rows only
+  if (hipError_t e = launch_attend(a, MODE_KEPT | MODE_ZSPILL, dt, hd, st)) return hip_fail(e, "kept pass launch");
   if (hipError_t e = mark(4)) return hip_fail(e, "event record");
   if (hipError_t e = launch_merge(merge_args(shape, layout, plan, a, k, out), hd, st)) return hip_fail(e, "merge launch");
   if (hipError_t e = mark(5)) return hip_fail(e, "event record");

@@ -94,7 +94,7 @@ namespace {
 // waves per SIMD the register allocation is sized for (one wave per work-group)
 constexpr int attend_waves(int dt, int mode) {
   return dt != VP_BF16 ? 1
-                       : (((mode & ~MODE_PAGED) == MODE_VIS || (mode & ~MODE_PAGED) == MODE_TEXT_STATS)
+                       : ((base_mode(mode) == MODE_VIS || base_mode(mode) == MODE_TEXT_STATS)
                               ? VP_ATTEND_WAVES_LEAN
                               : VP_ATTEND_WAVES);
 }
@@ -111,7 +111,7 @@ constexpr int attend_waves(int dt, int mode) {
 constexpr int max_i(int x, int y) { return x > y ? x : y; }
 constexpr int lds_floor(int dt, int mode) {
   return dt != VP_BF16 ? 0
-                       : (((mode & ~MODE_PAGED) == MODE_VIS || (mode & ~MODE_PAGED) == MODE_TEXT_STATS)
+                       : ((base_mode(mode) == MODE_VIS || base_mode(mode) == MODE_TEXT_STATS)
                               ? VP_LDS_FLOOR_VIS
                               : VP_LDS_FLOOR_TEXT);
 }
@@ -290,9 +290,10 @@ struct Sub {
 template <int DT, int D, int MODE>
 struct Pass {
   using C = Cfg<DT, D>;
-  static constexpr int BASE = MODE & ~MODE_PAGED;
+  static constexpr int BASE = base_mode(MODE);
   static constexpr bool PAGED = (MODE & MODE_PAGED) != 0;        // rows through the block table
   static constexpr bool KEPT = BASE == MODE_KEPT;
+  static constexpr bool ZSPILL = KEPT && (MODE & MODE_ZSPILL) != 0;  // kept logits from the spill
   static constexpr bool VIS = BASE == MODE_VIS;                  // visual rows: statistics + spill
   static constexpr bool TSTATS = (BASE & MODE_TEXT_STATS) != 0;  // text rows: statistics
   static constexpr bool ATTN = KEPT || (BASE & MODE_TEXT_ATTN) != 0;
@@ -310,6 +311,7 @@ struct Pass {
   size_t bstride;     // paged caches: bytes per physical block
   int bmask;          // paged caches: rows per block - 1
   float* zbase;  // spill plane of this KV group: row p holds the logits of its heads at position p
+                 // (kept pass from the spill: offset to the query's first head)
   QFrag<DT, D> qf;
   // visual pass: lane-local reference and sums (merged over a head's 4 lanes at the end)
   float m_v, Ls_v, Lm_v;
@@ -367,6 +369,18 @@ struct Pass {
     return n;
   }
 
+  // kept pass from the spill: the logits of this lane's 8 rows (head n16 of
+  // the query), requested with the tile's V rows; rows past the list read
+  // position 0 and are masked like their V rows
+  __device__ __forceinline__ void load_spill(const Sub& s, float (&z)[8]) const {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int p = __shfl(s.kp, 16 * (i >> 2) + 4 * a4 + (i & 3));
+      const int pp = (p < 0 || p >= L) ? 0 : p;
+      z[i] = hv ? zbase[static_cast<size_t>(pp) * a.zs_gp + n16] : 0.f;
+    }
+  }
+
   // byte offsets (from the head's base) of what lane l copies in copy j: row
   // j*RPI + l/PIECES, 16-byte piece (l%PIECES) ^ (row & (PIECES-1)) (the swizzle)
   __device__ __forceinline__ void row_offsets(const Sub& s, size_t (&off)[C::COPIES]) const {
@@ -396,16 +410,23 @@ struct Pass {
   }
 
   __device__ __forceinline__ void process(const Sub& tile, const unsigned char* kblk, const unsigned char* vblk,
-                                         float* stage) {
+                                         float* stage, const float (&zk)[8]) {
     const int t0 = tile.t0;
     const int cls = tile.cls;
     const int t_end = min(t0 + 32, r1);
     // ---- scores of the 32 rows against the query group ----
-    const f32x4 c0 = score_half<DT, D>(kblk, 0, qf, a4, n16);
-    const f32x4 c1 = score_half<DT, D>(kblk, 1, qf, a4, n16);
     float z[8];
+    if constexpr (ZSPILL) {
+      // the visual pass computed these logits with the same products (the
+      // same operands and instructions give the same bits)
 #pragma unroll
-    for (int i = 0; i < 8; ++i) z[i] = (i < 4 ? c0[i & 3] : c1[i & 3]) * a.zscale;
+      for (int i = 0; i < 8; ++i) z[i] = zk[i];
+    } else {
+      const f32x4 c0 = score_half<DT, D>(kblk, 0, qf, a4, n16);
+      const f32x4 c1 = score_half<DT, D>(kblk, 1, qf, a4, n16);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) z[i] = (i < 4 ? c0[i & 3] : c1[i & 3]) * a.zscale;
+    }
 
     // value i of this lane is row t0 + 16*(i/4) + 4*a4 + i%4; bit i of the masks
     unsigned valid = 0xffu, vis = 0u;
@@ -610,7 +631,9 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
   s.l_t = s.Lm_t = s.Ls_t = 0.f;
 #pragma unroll
   for (int i = 0; i < C::ACC_N; ++i) s.acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  s.zbase = P::VIS ? a.zs + (static_cast<size_t>(b) * a.Hkv + g) * a.zs_rows * static_cast<size_t>(a.zs_gp) : nullptr;
+  s.zbase = (P::VIS || P::ZSPILL)
+                ? a.zs + (static_cast<size_t>(b) * a.Hkv + g) * a.zs_rows * static_cast<size_t>(a.zs_gp) + qk * a.G
+                : nullptr;
 
   Sub cur;
   cur.t0 = s.r0;
@@ -635,14 +658,16 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
     // previous tile). LDS reads of the previous tile must have returned before
     // the copies overwrite it:
     __builtin_amdgcn_s_waitcnt(kWaitLgkm0);
+    float zk[NSUB][8];
 #pragma unroll
     for (int i = 0; i < NSUB; ++i) {
       if (act[i]) {
         unsigned char* blk = lds + i * SUB;
         size_t off[C::COPIES];
         s.row_offsets(sub[i], off);
-        s.copy_rows(s.Kb, off, blk);
+        if constexpr (!P::ZSPILL) s.copy_rows(s.Kb, off, blk);
         if (s.needs_v(sub[i])) s.copy_rows(s.Vb, off, blk + C::SUB_ROWS_BYTES);
+        if constexpr (P::ZSPILL) s.load_spill(sub[i], zk[i]);
       }
     }
     // the next tile's kept positions / segment state load while these copies fly
@@ -653,7 +678,7 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
     for (int i = 0; i < NSUB; ++i)
       if (act[i])
         s.process(sub[i], lds + i * SUB, lds + i * SUB + C::SUB_ROWS_BYTES,
-                  reinterpret_cast<float*>(lds + i * SUB + C::SUB_ROWS_BYTES + VB));
+                  reinterpret_cast<float*>(lds + i * SUB + C::SUB_ROWS_BYTES + VB), zk[i]);
   }
 
   // ---- write this part's partials ----
@@ -713,7 +738,7 @@ template <int DT, int D, int MODE>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(attend_waves(DT, MODE)))) void attend_kernel(
     const AttendArgs a) {
   __shared__ __attribute__((aligned(1024))) unsigned char lds[PassLds<DT, D, MODE>::BYTES];
-  if ((MODE & ~MODE_PAGED) == MODE_VIS && static_cast<int>(blockIdx.x) == a.nparts) {
+  if (base_mode(MODE) == MODE_VIS && static_cast<int>(blockIdx.x) == a.nparts) {
     step_setup(a, blockIdx.y, blockIdx.z);
     return;
   }
@@ -755,9 +780,10 @@ hipError_t launch_one(K kernel, dim3 grid, const AttendArgs& a, hipStream_t st, 
 template <int DT, int D, int PG>
 hipError_t launch_dd(const AttendArgs& a, int mode, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
   // launches with the visual role carry one more work-group per sequence (step_setup)
-  const int gx = mode == MODE_KEPT ? a.nsplit
-                                   : (mode == MODE_DUAL ? 2 * a.nparts + 1 : (mode == MODE_VIS ? a.nparts + 1 : a.nparts));
-  const dim3 grid(gx, mode == MODE_KEPT ? a.Hkv * a.T : a.Hkv, a.B);
+  const bool kept = (mode & ~MODE_ZSPILL) == MODE_KEPT;
+  const int gx = kept ? a.nsplit
+                      : (mode == MODE_DUAL ? 2 * a.nparts + 1 : (mode == MODE_VIS ? a.nparts + 1 : a.nparts));
+  const dim3 grid(gx, kept ? a.Hkv * a.T : a.Hkv, a.B);
   switch (mode) {
     case MODE_DUAL: return launch_one(attend_dual_kernel<DT, D, PG>, grid, a, st, ev0, ev1);
     case MODE_VIS: return launch_one(attend_kernel<DT, D, MODE_VIS | PG>, grid, a, st, ev0, ev1);
@@ -765,6 +791,8 @@ hipError_t launch_dd(const AttendArgs& a, int mode, hipStream_t st, hipEvent_t e
     case MODE_TEXT_ATTN: return launch_one(attend_kernel<DT, D, MODE_TEXT_ATTN | PG>, grid, a, st, ev0, ev1);
     case MODE_TEXT_BOTH: return launch_one(attend_kernel<DT, D, MODE_TEXT_BOTH | PG>, grid, a, st, ev0, ev1);
     case MODE_KEPT: return launch_one(attend_kernel<DT, D, MODE_KEPT | PG>, grid, a, st, ev0, ev1);
+    case MODE_KEPT | MODE_ZSPILL:
+      return launch_one(attend_kernel<DT, D, MODE_KEPT | MODE_ZSPILL | PG>, grid, a, st, ev0, ev1);
     default: return hipErrorInvalidValue;
   }
 }
