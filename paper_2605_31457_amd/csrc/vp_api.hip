@@ -263,20 +263,13 @@ TopkArgs topk_args(const vp_shape* s, const vp_layout* l, const float* scores, c
   return t;
 }
 
-MergeArgs merge_args(const vp_shape* s, const vp_layout* l, const Plan& plan, const AttendArgs& a, const int32_t* k,
-                     void* out) {
+MergeArgs merge_args(const vp_shape* s, const Plan& plan, const AttendArgs& a, void* out) {
   MergeArgs m{};
-  m.seq_len = l->seq_len;
-  m.kk = k;
   m.B = s->batch;
   m.Hq = s->n_q_heads;
   m.G = s->n_q_heads / s->n_kv_heads;
   m.T = queries(*s);
-  m.U = rows_per_query(*s);
-  m.max_seq_len = s->max_seq_len;
-  m.k_cap = s->k_cap;
   m.nparts = plan.nparts;
-  m.split = plan.split;
   m.nsplit = plan.nsplit;
   m.dtype = s->dtype;
   m.stats = a.stats;
@@ -346,7 +339,7 @@ vp_status launch_step(const vp_shape* shape, const vp_layout* layout, const vp_p
   // from it, so the kept pass reads V rows only
   if (hipError_t e = launch_attend(a, MODE_KEPT | MODE_ZSPILL, dt, hd, st)) return hip_fail(e, "kept pass launch");
   if (hipError_t e = mark(4)) return hip_fail(e, "event record");
-  if (hipError_t e = launch_merge(merge_args(shape, layout, plan, a, k, out), hd, st)) return hip_fail(e, "merge launch");
+  if (hipError_t e = launch_merge(merge_args(shape, plan, a, out), hd, st)) return hip_fail(e, "merge launch");
   if (hipError_t e = mark(5)) return hip_fail(e, "event record");
   return VP_OK;
 }
@@ -592,7 +585,7 @@ vp_status vp_sparse_decode_attn(const vp_shape* shape, const vp_layout* layout, 
   }
   if (hipError_t e = launch_attend(a, MODE_KEPT, shape->dtype, shape->head_dim, st))
     return hip_fail(e, "kept pass launch");
-  if (hipError_t e = launch_merge(merge_args(shape, layout, plan, a, k, out), shape->head_dim, st))
+  if (hipError_t e = launch_merge(merge_args(shape, plan, a, out), shape->head_dim, st))
     return hip_fail(e, "merge launch");
   return VP_OK;
 }

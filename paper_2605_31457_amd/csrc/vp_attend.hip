@@ -611,7 +611,25 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
   // the query rows load while the length and the budget arrive
   const size_t qrow = s.hv ? (static_cast<size_t>(b) * a.T + tq) * a.Hq + g * a.G + (vh - tq * a.G) : 0;
   load_q<DT, D>(s.qf, static_cast<const char*>(a.q) + qrow * C::ROWB, s.hv, s.a4);
-  if (s.r0 >= s.r1) return;
+  if (s.r0 >= s.r1) {
+    // no rows: an empty partial (max -inf, sum 0), so that the merge can read
+    // every part's slot without first learning the length and the budget
+    if constexpr (P::ATTN) {
+      if (s.hv && s.a4 == 0) {
+        if constexpr (P::KEPT) {
+          const size_t row = (static_cast<size_t>(b) * a.T * a.Hq + s.h) * a.nsplit + part;
+          *reinterpret_cast<float2*>(a.kstats + row * 2) = make_float2(kNegInf, 0.f);
+        } else {
+          const size_t row = (static_cast<size_t>(b) * a.T * a.Hq + s.h) * a.nparts + part;
+          if constexpr (P::TSTATS)
+            *reinterpret_cast<float4*>(a.stats + row * 8 + 4) = make_float4(kNegInf, 0.f, 0.f, 0.f);
+          else
+            *reinterpret_cast<float2*>(a.stats + row * 8 + 4) = make_float2(kNegInf, 0.f);
+        }
+      }
+    }
+    return;
+  }
 
   s.L0 = s.L - a.T + 1;
   s.lim = s.L0 + tq;

@@ -195,9 +195,7 @@ struct TopPArgs {
 hipError_t launch_top_p(const TopPArgs& a, hipStream_t st);
 
 struct MergeArgs {
-  const int32_t* seq_len;
-  const int32_t* kk;
-  int B, Hq, G, T, U, max_seq_len, k_cap, nparts, split, nsplit, dtype;
+  int B, Hq, G, T, nparts, nsplit, dtype;
   const float* stats;
   const float* acc;
   const float* kstats;

@@ -2,7 +2,8 @@
 // partials of the context pass (one per context-pass part) and the kept-row partials
 // (one per split of the kept list) of every (sequence, query, query head):
 //   out = sum_i 2^(m_i - M) acc_i / sum_i 2^(m_i - M) l_i,  M = max_i m_i,
-// over the partials with l_i > 0; an empty context gives zeros.
+// over the partials with l_i > 0 (parts and splits with no rows write empty
+// ones); an empty context gives zeros.
 // grid = (T*Hq, B); 256 threads = (D/4 float4 columns) x R partial lanes, so the
 // partials are read in parallel (R at a time, each row as coalesced float4s)
 // rather than one after another.
@@ -43,12 +44,11 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a)
   const int wid = tid >> 6;
   const int col = tid % COLS;
   const int r = tid / COLS;
-  const int L = clamp_len(a.seq_len[b], a.max_seq_len);
-  const int nc = parts_used(L, a.nparts);
-  int kb = a.kk[(static_cast<size_t>(b) * a.T + qt) * a.U + h / (a.Hq / a.U)];  // the head's selection row
-  kb = kb < 0 ? 0 : (kb > a.k_cap ? a.k_cap : kb);
-  const int ns = L > 0 ? (kb + a.split - 1) / a.split : 0;
-  const int np = nc + ns;
+  // every slot holds a partial (parts past the sequence's tiles and splits
+  // past its budget hold empty ones), so none of them waits for the length or
+  // the budget to be read first
+  const int nc = a.nparts;
+  const int np = nc + a.nsplit;
   const size_t bh = static_cast<size_t>(b) * a.T * a.Hq + vhead(h, qt, a.G, a.T);  // partials: virtual head
   const size_t ob = static_cast<size_t>(b) * a.T * a.Hq + x;  // out [B][T][Hq][D]
   const float* st = a.stats + bh * a.nparts * 8;
