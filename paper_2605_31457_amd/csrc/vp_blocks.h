@@ -110,9 +110,13 @@ __device__ __forceinline__ void sum_parts(double& Ls, double& Lm, double& Vm, co
 }
 }  // namespace detail
 
-template <typename Between>
+// With `early_on` (uniform over the block), `early()` runs after `between()` and
+// a block barrier, before the reduction's arithmetic: loads it issues fly while
+// the statistics are reduced.
+template <typename Between, typename Early>
 __device__ __forceinline__ void reduce_heads(const MassArgs& a, int b, int qt, int u, int L, int tid,
-                                             const HeadLds& hs, bool write_out, Between between) {
+                                             const HeadLds& hs, bool write_out, Between between, bool early_on,
+                                             Early early) {
   using namespace detail;
   const int Hu = a.Hq / a.U;  // heads of the row
   const int h0 = u * Hu;
@@ -140,6 +144,10 @@ __device__ __forceinline__ void reduce_heads(const MassArgs& a, int b, int qt, i
     if (one_round) load_parts(v, t, st, on, sub, lph, a.nparts);
   }
   between();
+  if (early_on) {
+    __syncthreads();
+    early();
+  }
   if (busy) {
     const int nv = parts_used(L, a.nparts);
     float m = kNegInf;
@@ -219,13 +227,9 @@ __host__ __device__ inline int score_lanes(int Hkv) {
   return ng;
 }
 
-// p plus the score terms of one KV group's G heads of query t for one token,
-// from its spill row (GP floats, 16-byte aligned; the query's heads are
-// columns o .. o + G - 1, o = t*G); hm/hinv point at the group's first head
+// one KV group's spill row for one token (GP floats, 16-byte aligned)
 template <int GP>
-__device__ __forceinline__ float group_terms(float p, const float* row, int G, int o, const float* hm,
-                                             const float* hinv, float inv_tau) {
-  float z[GP];
+__device__ __forceinline__ void load_group_row(const float* row, float (&z)[GP]) {
 #pragma unroll
   for (int q = 0; q < GP / 4; ++q) {
     const float4 v = reinterpret_cast<const float4*>(row)[q];
@@ -234,10 +238,25 @@ __device__ __forceinline__ float group_terms(float p, const float* row, int G, i
     z[4 * q + 2] = v.z;
     z[4 * q + 3] = v.w;
   }
+}
+// p plus the score terms of the G heads of query t in a loaded spill row (the
+// query's heads are columns o .. o + G - 1, o = t*G); hm/hinv point at the
+// group's first head
+template <int GP>
+__device__ __forceinline__ float group_terms_of(float p, const float (&z)[GP], int G, int o, const float* hm,
+                                                const float* hinv, float inv_tau) {
 #pragma unroll
   for (int j = 0; j < GP; ++j)
     if (j >= o && j < o + G) p = score_term(p, z[j], hm[j - o], hinv[j - o], inv_tau);
   return p;
+}
+// the same, loading the row
+template <int GP>
+__device__ __forceinline__ float group_terms(float p, const float* row, int G, int o, const float* hm,
+                                             const float* hinv, float inv_tau) {
+  float z[GP];
+  load_group_row<GP>(row, z);
+  return group_terms_of<GP>(p, z, G, o, hm, hinv, inv_tau);
 }
 
 // ---------------------------------------------------------------------------

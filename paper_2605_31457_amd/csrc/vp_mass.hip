@@ -15,7 +15,7 @@ __global__ __launch_bounds__(kSelThreads) void mass_finalize_kernel(const MassAr
   const int b = row / (a.T * a.U);
   const int t = (row / a.U) % a.T;
   const int u = row % a.U;
-  reduce_heads(a, b, t, u, clamp_len(a.seq_len[b], a.max_seq_len), threadIdx.x, head_lds(dyn, a.Hq), true, [] {});
+  reduce_heads(a, b, t, u, clamp_len(a.seq_len[b], a.max_seq_len), threadIdx.x, head_lds(dyn, a.Hq), true, [] {}, false, [] {});
 }
 
 // S_i of Eq. (2) for every visual rank i of every selection row.

@@ -22,6 +22,8 @@
 // Results equal those of the separate kernels (mass_finalize_kernel,
 // scores_kernel, budget rule, topk_kernel): the same device functions in the
 // same order.
+#include <type_traits>
+
 #include "vp_blocks.h"
 
 namespace vp {
@@ -61,9 +63,25 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
   uint32_t* s_keys = reinterpret_cast<uint32_t*>(dyn + head_lds_bytes(a.Hq));
 
   const int L = clamp_len(a.seq_len[b], a.max_seq_len);
+  // the Eq. (2) scoring layout (below): ng lanes per token, lane l takes the
+  // row's KV groups g0 + l, g0 + l + ng, ...
+  const int Gu = a.Hkv / a.U;
+  const int g0 = u * Gu;
+  const int ng = score_lanes(Gu);
+  const int l = tid & (ng - 1);
+  const float* zb = a.zs + static_cast<size_t>(b) * a.Hkv * a.zs_rows * GP;
+  // the first scoring round's position and spill row of this lane's first
+  // KV group, requested as soon as the segment table is in LDS, when a chunk
+  // is a single round (latency-bound; with more rounds the extra barrier
+  // costs as much as the round it hides)
+  const bool early = t.chunk <= kSelThreads / ng;
+  int pos0 = 0;
+  bool pre = false;
+  float z0[GP];
 
   // ---- per-head statistics; the segment table is copied in while the
-  // statistics are in flight (the reduction's barriers publish it) ----
+  // statistics are in flight (a barrier publishes it, then the first round of
+  // spill rows is requested and flies while the statistics are reduced) ----
   reduce_heads(a, b, qt, u, L, tid, hs, c == 0, [&] {
     // the context pass left the clipped table in the workspace: one 16-byte
     // load for every fourth thread, spread over the waves so that no wave
@@ -73,6 +91,15 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
     if ((tid & 3) == 0 && (tid >> 2) < kWords) {
       const uint4* src = reinterpret_cast<const uint4*>(static_cast<const SegTable*>(t.segtab) + b);
       reinterpret_cast<uint4*>(&tab)[tid >> 2] = src[tid >> 2];
+    }
+  }, early, [&] {
+    const int nv = min(tab.rk[tab.n], a.max_vis);
+    const int q0 = min(nv, c * t.chunk);
+    const int i = q0 + tid / ng;
+    if (i < min(nv, q0 + t.chunk) && l < Gu) {
+      pos0 = rank_to_pos(tab, i);
+      load_group_row<GP>(zb + (static_cast<size_t>(g0 + l) * a.zs_rows + pos0) * GP, z0);
+      pre = true;
     }
   });
   // the radix counters are first used after the key-range barrier: cleared
@@ -87,23 +114,26 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
   // ---- Eq. (2) scores of this chunk's visual ranks: ng lanes per token, lane
   // l takes the row's KV groups g0 + l, g0 + l + ng, ... (a 16-byte-aligned
   // spill row each), the lane sums are added in lane order ----
-  const int Gu = a.Hkv / a.U;
-  const int g0 = u * Gu;
-  const int ng = score_lanes(Gu);
-  const int l = tid & (ng - 1);
   const int tpw = kSelThreads / ng;  // tokens per round
   const int r0 = min(n, c * t.chunk);
   const int r1 = min(n, r0 + t.chunk);
-  const float* zb = a.zs + static_cast<size_t>(b) * a.Hkv * a.zs_rows * GP;
   uint32_t kmin = 0xffffffffu, kmax = 0u;
-  for (int base = r0; base < r1; base += tpw) {
+  // one round of tokens; with kPre the lane's first KV group comes from the
+  // row requested during the head reduction
+  auto score_round = [&](int base, auto pre_tag) {
+    constexpr bool kPre = decltype(pre_tag)::value;
     const int i = base + tid / ng;
     const bool ok = i < r1;
-    const int pos = ok ? rank_to_pos(tab, i) : 0;
+    const bool use = kPre && pre;
+    const int pos = use ? pos0 : (ok ? rank_to_pos(tab, i) : 0);
     float p = 0.f;
-    for (int g = g0 + l; g < g0 + Gu; g += ng)
-      p = group_terms<GP>(p, zb + (static_cast<size_t>(g) * a.zs_rows + pos) * GP, a.G, qt * a.G, hs.hm + g * a.G,
-                          hs.hinv + g * a.G, a.inv_tau_s);
+    for (int g = g0 + l; g < g0 + Gu; g += ng) {
+      if (use && g == g0 + l)
+        p = group_terms_of<GP>(p, z0, a.G, qt * a.G, hs.hm + g * a.G, hs.hinv + g * a.G, a.inv_tau_s);
+      else
+        p = group_terms<GP>(p, zb + (static_cast<size_t>(g) * a.zs_rows + pos) * GP, a.G, qt * a.G,
+                            hs.hm + g * a.G, hs.hinv + g * a.G, a.inv_tau_s);
+    }
     float total = p;
     for (int j = 1; j < ng; ++j) total = total + __shfl(p, (lane & ~(ng - 1)) + j);
     if (ok && l == 0) {
@@ -114,7 +144,13 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(const SelectArgs t,
       kmin = min(kmin, u);
       kmax = max(kmax, u);
     }
+  };
+  int base = r0;
+  if (early && base < r1) {
+    score_round(base, std::true_type{});
+    base += tpw;
   }
+  for (; base < r1; base += tpw) score_round(base, std::false_type{});
 
   if (single && !in_lds) {
     // one work-group, keys beyond its LDS room: the radix select reads the
