@@ -307,6 +307,35 @@ def test_unclean_device_layout_is_clipped():
             check_sequence(f"clipped fused={fused}", w, g, b, ref[b])
 
 
+def test_zero_length_sequence_in_a_batch():
+    """A sequence of length 0 between two others gets the empty context's
+    results (masses 0, budget 0, no kept rows, output 0) from the four calls and
+    from the step alike; its neighbours still match the reference, and the step
+    equals the four calls bit for bit. Every context-pass part and kept split of
+    the empty sequence writes an empty partial, which the merge reads."""
+    w = small_workload(seed=21, B=3, Hq=8, Hkv=2, d=64, lens=[120, 40, 90], segs=[[(10, 60)], [(0, 20)], [(0, 40)]])
+    ref, _ = P.plant(w, P.params_of(w))
+    ds = S.DeviceStep(w)
+    ds.seq_len[1] = 0
+    got = {}
+    for fused in (True, False):
+        ds.scores.fill_(-1.0)
+        ds.out.fill_(7.0)
+        ds.run(fused=fused)
+        got[fused] = g = ds.results()
+        for b in (0, 2):
+            check_sequence(f"zero-length neighbour fused={fused}", w, g, b, ref[b])
+        assert np.all(g["mass_head"][1] == 0.0) and np.all(g["mass_seq"][1] == 0.0)
+        assert int(g["k"][1]) == 0 and np.all(g["vis_idx"][1] == -1)
+        assert np.all(g["scores"][1] == -1.0), "no visual rank: no score is written"
+        assert np.all(g["out"][1].astype(np.float32) == 0.0)
+    ds.out.fill_(7.0)
+    ds.decode_step()
+    g = ds.results()
+    for key in ("mass_head", "mass_seq", "scores", "k", "vis_idx", "out"):
+        assert np.array_equal(g[key], got[False][key]), key
+
+
 PRESETS = {
     # the 10% retention preset: tau = 0.4, clamp (0.05 N, 0.10 N)
     "retain10": dict(tau_mass=0.4, r_lo_bp=500, r_hi_bp=1000),
