@@ -87,6 +87,13 @@ constexpr int kCopyPolicy = 2;
 // s_waitcnt immediates (gfx9 encoding: vmcnt [3:0]+[15:14], expcnt [6:4], lgkmcnt [11:8])
 constexpr int kWaitLgkm0 = 0xC07F;  // lgkmcnt(0), others unconstrained
 constexpr int kWaitVm0 = 0x0F70;    // vmcnt(0), others unconstrained
+// buffer resource word 3 for raw (untyped) dword access: 32-bit data format
+constexpr int kRawBufferWord3 = 0x00020000;
+// cache policy of the full-tile spill stores: sc1 (device scope) in the visual
+// pass launched alone (64 x 32k batch: visual pass 230 -> 226 us; non-temporal
+// stores: 242), the default in the one-launch context pass (sc1 there: 72B-class
+// decode loop 84.0 -> 84.6 us per step)
+constexpr int spill_policy(int mode) { return (mode & vp::MODE_ONE_LAUNCH) ? 0 : 16; }
 
 namespace vp {
 namespace {
@@ -311,6 +318,7 @@ struct Pass {
   size_t bstride;     // paged caches: bytes per physical block
   int bmask;          // paged caches: rows per block - 1
   float* zbase;  // spill plane of this KV group: row p holds the logits of its heads at position p
+  __amdgpu_buffer_rsrc_t zrsrc;  // visual pass: the same plane as a buffer (its full-tile stores)
                  // (kept pass from the spill: offset to the query's first head)
   QFrag<DT, D> qf;
   // visual pass: lane-local reference and sums (merged over a head's 4 lanes at the end)
@@ -494,10 +502,12 @@ struct Pass {
 #pragma unroll
           for (int i = 0; i < 8; ++i) stage[(16 * (i >> 2) + 4 * a4 + (i & 3)) * gp + n16] = z[i];
         }
-        float4* dst = reinterpret_cast<float4*>(zbase + static_cast<size_t>(t0) * gp);
-        const float4* src = reinterpret_cast<const float4*>(stage);
-        dst[lane] = src[lane];
-        if (gp > 8) dst[64 + lane] = src[64 + lane];
+        typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+        const u32x4* src = reinterpret_cast<const u32x4*>(stage);
+        const int soff = t0 * gp * 4;
+        __builtin_amdgcn_raw_buffer_store_b128(src[lane], zrsrc, lane * 16, soff, spill_policy(MODE));
+        if (gp > 8)
+          __builtin_amdgcn_raw_buffer_store_b128(src[64 + lane], zrsrc, 1024 + lane * 16, soff, spill_policy(MODE));
       } else if (hv && vis) {
 #pragma unroll
         for (int i = 0; i < 8; ++i)
@@ -649,6 +659,13 @@ __device__ __forceinline__ void attend_body(const AttendArgs& a, unsigned char* 
   s.l_t = s.Lm_t = s.Ls_t = 0.f;
 #pragma unroll
   for (int i = 0; i < C::ACC_N; ++i) s.acc[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+  if constexpr (P::VIS) {
+    // the plane (zs_rows * zs_gp floats) as a raw buffer: offsets past it are dropped
+    const size_t plane = static_cast<size_t>(a.zs_rows) * a.zs_gp * 4;
+    s.zrsrc = __builtin_amdgcn_make_buffer_rsrc(
+        a.zs + (static_cast<size_t>(b) * a.Hkv + g) * a.zs_rows * static_cast<size_t>(a.zs_gp), 0,
+        static_cast<int>(plane < 0x7fffffffu ? plane : 0x7fffffffu), kRawBufferWord3);
+  }
   s.zbase = (P::VIS || P::ZSPILL)
                 ? a.zs + (static_cast<size_t>(b) * a.Hkv + g) * a.zs_rows * static_cast<size_t>(a.zs_gp) + qk * a.G
                 : nullptr;
@@ -770,14 +787,16 @@ __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(attend_waves
 template <int DT, int D, int PG>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(attend_waves(DT, MODE_TEXT_BOTH)))) void
 attend_dual_kernel(const AttendArgs a) {
-  constexpr int BYTES = max_i(PassLds<DT, D, MODE_VIS | PG>::BYTES, PassLds<DT, D, MODE_TEXT_BOTH | PG>::BYTES);
+  constexpr int VIS = MODE_VIS | MODE_ONE_LAUNCH | PG;
+  constexpr int TEXT = MODE_TEXT_BOTH | MODE_ONE_LAUNCH | PG;
+  constexpr int BYTES = max_i(PassLds<DT, D, VIS>::BYTES, PassLds<DT, D, TEXT>::BYTES);
   __shared__ __attribute__((aligned(1024))) unsigned char lds[BYTES];
   const int x = blockIdx.x;
   // the roles alternate, so every CU gets a mix of visual (K, spill) and text
   // (K and V) work-groups (measured 86.5 -> 84.8 us at the 16-sequence ragged batch)
   if (x < 2 * a.nparts) {
-    if (x & 1) attend_body<DT, D, MODE_VIS | PG>(a, lds, x >> 1, blockIdx.y, blockIdx.z);
-    else attend_body<DT, D, MODE_TEXT_BOTH | PG>(a, lds, x >> 1, blockIdx.y, blockIdx.z);
+    if (x & 1) attend_body<DT, D, VIS>(a, lds, x >> 1, blockIdx.y, blockIdx.z);
+    else attend_body<DT, D, TEXT>(a, lds, x >> 1, blockIdx.y, blockIdx.z);
   } else {
     step_setup(a, blockIdx.y, blockIdx.z);
   }

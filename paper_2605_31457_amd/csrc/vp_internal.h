@@ -64,10 +64,11 @@ enum Mode : int {
   MODE_KEPT = 8,        // kept visual rows: attention partial
   MODE_DUAL = 16,       // visual pass and text pass (statistics + attention) in one launch
   MODE_PAGED = 32,      // flag: K and V rows addressed through a block table (paged caches)
-  MODE_ZSPILL = 64      // flag (kept pass): the kept rows' logits come from the visual pass's
+  MODE_ZSPILL = 64,     // flag (kept pass): the kept rows' logits come from the visual pass's
                         // spill of the same step instead of their K rows (V rows only are read)
+  MODE_ONE_LAUNCH = 128 // flag: a role of the one-launch context pass (attend_dual_kernel)
 };
-constexpr int base_mode(int mode) { return mode & ~(MODE_PAGED | MODE_ZSPILL); }
+constexpr int base_mode(int mode) { return mode & ~(MODE_PAGED | MODE_ZSPILL | MODE_ONE_LAUNCH); }
 
 struct AttendArgs {
   const void* q;
