@@ -579,12 +579,18 @@ vp_status vp_sparse_decode_attn(const vp_shape* shape, const vp_layout* layout, 
   AttendArgs a = attend_args(shape, layout, params, plan, ws, q, K, V);
   a.vis_idx = vis_idx;
   a.kk = k;
-  if (!(flags & VP_ATTN_TEXT_FROM_WORKSPACE)) {
-    if (hipError_t e = launch_attend(a, MODE_TEXT_ATTN, shape->dtype, shape->head_dim, st))
-      return hip_fail(e, "text pass launch");
+  if (!(flags & VP_ATTN_TEXT_FROM_WORKSPACE) && plan.text_kept_one_launch) {
+    // a layer that reads its own text rows: the text and kept passes share one launch
+    if (hipError_t e = launch_attend(a, MODE_TEXT_KEPT, shape->dtype, shape->head_dim, st))
+      return hip_fail(e, "text and kept pass launch");
+  } else {
+    if (!(flags & VP_ATTN_TEXT_FROM_WORKSPACE)) {
+      if (hipError_t e = launch_attend(a, MODE_TEXT_ATTN, shape->dtype, shape->head_dim, st))
+        return hip_fail(e, "text pass launch");
+    }
+    if (hipError_t e = launch_attend(a, MODE_KEPT, shape->dtype, shape->head_dim, st))
+      return hip_fail(e, "kept pass launch");
   }
-  if (hipError_t e = launch_attend(a, MODE_KEPT, shape->dtype, shape->head_dim, st))
-    return hip_fail(e, "kept pass launch");
   if (hipError_t e = launch_merge(merge_args(shape, plan, a, out), shape->head_dim, st))
     return hip_fail(e, "merge launch");
   return VP_OK;

@@ -802,6 +802,28 @@ attend_dual_kernel(const AttendArgs a) {
   }
 }
 
+// A later layer's text attention pass and kept pass in one launch (their rows
+// are disjoint and the kept list is the anchor layer's, known before the
+// launch): grid.x = P text parts + T*splits kept work-groups per (KV head,
+// sequence); each work-group does what it does in its own launch, so the
+// partials are the same bits, and the kept work-groups fill the text pass's tail.
+template <int DT, int D, int PG>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(attend_waves(DT, MODE_TEXT_ATTN)))) void
+attend_text_kept_kernel(const AttendArgs a) {
+  constexpr int TEXT = MODE_TEXT_ATTN | PG;
+  constexpr int KEPT = MODE_KEPT | PG;
+  constexpr int BYTES = max_i(PassLds<DT, D, TEXT>::BYTES, PassLds<DT, D, KEPT>::BYTES);
+  __shared__ __attribute__((aligned(1024))) unsigned char lds[BYTES];
+  const int x = blockIdx.x;
+  if (x < a.nparts) {
+    attend_body<DT, D, TEXT>(a, lds, x, blockIdx.y, blockIdx.z);
+  } else {
+    const int j = x - a.nparts;
+    const int t = j / a.nsplit;
+    attend_body<DT, D, KEPT>(a, lds, j - t * a.nsplit, blockIdx.y * a.T + t, blockIdx.z);
+  }
+}
+
 // Launches one pass. With events given, they are attached to the launch itself
 // (hipExtLaunchKernel): they time the kernel's execution alone, as a profiler does.
 template <typename K>
@@ -819,9 +841,13 @@ hipError_t launch_dd(const AttendArgs& a, int mode, hipStream_t st, hipEvent_t e
   // launches with the visual role carry one more work-group per sequence (step_setup)
   const bool kept = (mode & ~MODE_ZSPILL) == MODE_KEPT;
   const int gx = kept ? a.nsplit
-                      : (mode == MODE_DUAL ? 2 * a.nparts + 1 : (mode == MODE_VIS ? a.nparts + 1 : a.nparts));
+                      : (mode == MODE_DUAL ? 2 * a.nparts + 1
+                                           : (mode == MODE_VIS ? a.nparts + 1
+                                                               : (mode == MODE_TEXT_KEPT ? a.nparts + a.T * a.nsplit
+                                                                                         : a.nparts)));
   const dim3 grid(gx, kept ? a.Hkv * a.T : a.Hkv, a.B);
   switch (mode) {
+    case MODE_TEXT_KEPT: return launch_one(attend_text_kept_kernel<DT, D, PG>, grid, a, st, ev0, ev1);
     case MODE_DUAL: return launch_one(attend_dual_kernel<DT, D, PG>, grid, a, st, ev0, ev1);
     case MODE_VIS: return launch_one(attend_kernel<DT, D, MODE_VIS | PG>, grid, a, st, ev0, ev1);
     case MODE_TEXT_STATS: return launch_one(attend_kernel<DT, D, MODE_TEXT_STATS | PG>, grid, a, st, ev0, ev1);

@@ -29,6 +29,7 @@ struct Plan {
                 // the 32-row tiles p, p + nparts, p + 2 nparts, ...
   int split;    // kept rows per kept-pass work-group (multiple of 32)
   int nsplit;   // ceil(k_cap / split)
+  bool text_kept_one_launch;  // a later layer's text and kept passes fit one resident round together
   int zs_rows;    // rows per spill plane: max_seq_len rounded up to 32
   int zs_gp;      // floats per spill row: the query group padded to 8 or 16
   size_t zs;      // float [B][Hkv][zs_rows][zs_gp]  visual logits (log2 domain) by cache position
@@ -66,7 +67,8 @@ enum Mode : int {
   MODE_PAGED = 32,      // flag: K and V rows addressed through a block table (paged caches)
   MODE_ZSPILL = 64,     // flag (kept pass): the kept rows' logits come from the visual pass's
                         // spill of the same step instead of their K rows (V rows only are read)
-  MODE_ONE_LAUNCH = 128 // flag: a role of the one-launch context pass (attend_dual_kernel)
+  MODE_ONE_LAUNCH = 128, // flag: a role of the one-launch context pass (attend_dual_kernel)
+  MODE_TEXT_KEPT = 256   // launch of a later layer: the text attention pass and the kept pass together
 };
 constexpr int base_mode(int mode) { return mode & ~(MODE_PAGED | MODE_ZSPILL | MODE_ONE_LAUNCH); }
 

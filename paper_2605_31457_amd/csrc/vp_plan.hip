@@ -79,6 +79,13 @@ Plan make_plan(const vp_shape& s) {
   }
 #endif
   p.nsplit = (s.k_cap + p.split - 1) / p.split;
+  // A later layer (its own text rows, the anchor's kept list) launches its text
+  // and kept passes together when both fit one resident round: the kept
+  // work-groups then fill the text pass's tail (8 layers: 131.8 -> 98.6 us at the
+  // 1-sequence batch, 381.9 -> 351.9 at the 72B-class loop); beyond one round
+  // the text pass is split over two (the 64 x 32k batch: 3081 -> 3663 us).
+  p.text_kept_one_launch = static_cast<int64_t>(p.nparts + queries(s) * p.nsplit) * s.n_kv_heads * s.batch <=
+                           static_cast<int64_t>(VP_KEPT_WGS);
   // per-head arrays hold one entry per query row (virtual head): T*Hq per sequence
   const size_t B = s.batch, Hq = static_cast<size_t>(s.n_q_heads) * queries(s), d = s.head_dim;
   p.zs_rows = ((s.max_seq_len + 31) / 32) * 32;
