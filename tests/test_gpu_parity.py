@@ -399,6 +399,37 @@ def test_later_layers_reuse_the_anchor_selection():
         np.testing.assert_allclose(got, want, atol=2e-2, rtol=1e-2, err_msg=f"dense layer seed {seed}")
 
 
+def test_later_layer_at_the_64x32k_batch():
+    """A later layer at the 64 x 32k batch, where the text and kept passes do not
+    fit one resident round together and run as two launches: its outputs against
+    the reference attention over the anchor's kept set and the layer's own text
+    rows, for the four source sequences and copies of them at the far end of the
+    batch."""
+    base = W.generate(4, seqs=[0, 1, 2, 3])
+    P.plant(base, P.params_of(base))
+    w = tile_batch(base, 64)
+    ds = S.DeviceStep(w)
+    ds.decode_step()
+    g = ds.results()
+    other = W.generate(4, seqs=[0, 1, 2, 3], seed=33)  # another layer: same layout, its own q, K, V
+    wl = tile_batch(other, 64)
+    dl = S.DeviceStep(wl)
+    dl.vis_idx.copy_(ds.vis_idx)
+    dl.k.copy_(ds.k)
+    dl.sparse_decode_attn(fused=False)
+    got = dl.results()["out"]
+    G = wl.Hq // wl.Hkv
+    sm = 1.0 / np.sqrt(wl.d)
+    for b in (0, 1, 2, 3, 61, 62, 63):
+        sel = g["vis_idx"][b, :int(g["k"][b])]
+        L = int(wl.seq_len[b])
+        J = np.sort(np.concatenate([sel, O.text_positions(L, wl.segments[b])]))
+        qf = O.as_f64(wl.q[b])
+        want = np.stack([O.pruned_attention(qf[h], wl.K[b, h // G], wl.V[b, h // G], J, sm) for h in range(wl.Hq)])
+        np.testing.assert_allclose(got[b], want, atol=2e-2, rtol=1e-2, err_msg=f"later layer, sequence {b}")
+    _log("later layer at 64 x 32k: 7 sequences match the reference")
+
+
 def _prefix_margin(S, vis, p):
     """Distance from p to the nearest prefix sum of S in the Eq. (3) order."""
     csum = np.cumsum(S[np.lexsort((vis, -S))])
