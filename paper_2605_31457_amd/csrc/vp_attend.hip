@@ -318,8 +318,8 @@ struct Pass {
   size_t bstride;     // paged caches: bytes per physical block
   int bmask;          // paged caches: rows per block - 1
   float* zbase;  // spill plane of this KV group: row p holds the logits of its heads at position p
-  __amdgpu_buffer_rsrc_t zrsrc;  // visual pass: the same plane as a buffer (its full-tile stores)
                  // (kept pass from the spill: offset to the query's first head)
+  __amdgpu_buffer_rsrc_t zrsrc;  // visual pass: the same plane as a buffer (its full-tile stores)
   QFrag<DT, D> qf;
   // visual pass: lane-local reference and sums (merged over a head's 4 lanes at the end)
   float m_v, Ls_v, Lm_v;
@@ -840,11 +840,11 @@ template <int DT, int D, int PG>
 hipError_t launch_dd(const AttendArgs& a, int mode, hipStream_t st, hipEvent_t ev0, hipEvent_t ev1) {
   // launches with the visual role carry one more work-group per sequence (step_setup)
   const bool kept = (mode & ~MODE_ZSPILL) == MODE_KEPT;
-  const int gx = kept ? a.nsplit
-                      : (mode == MODE_DUAL ? 2 * a.nparts + 1
-                                           : (mode == MODE_VIS ? a.nparts + 1
-                                                               : (mode == MODE_TEXT_KEPT ? a.nparts + a.T * a.nsplit
-                                                                                         : a.nparts)));
+  int gx = a.nparts;
+  if (kept) gx = a.nsplit;
+  else if (mode == MODE_DUAL) gx = 2 * a.nparts + 1;
+  else if (mode == MODE_VIS) gx = a.nparts + 1;
+  else if (mode == MODE_TEXT_KEPT) gx = a.nparts + a.T * a.nsplit;  // text parts, then kept splits
   const dim3 grid(gx, kept ? a.Hkv * a.T : a.Hkv, a.B);
   switch (mode) {
     case MODE_TEXT_KEPT: return launch_one(attend_text_kept_kernel<DT, D, PG>, grid, a, st, ev0, ev1);
