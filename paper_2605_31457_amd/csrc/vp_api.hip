@@ -271,6 +271,23 @@ MergeArgs merge_args(const vp_shape* s, const Plan& plan, const AttendArgs& a, v
   m.T = queries(*s);
   m.nparts = plan.nparts;
   m.nsplit = plan.nsplit;
+  m.seq_len = a.seq_len;
+  m.vis_idx = a.vis_idx;
+  m.kk = a.kk;
+  m.max_seq_len = s->max_seq_len;
+  m.Hkv = s->n_kv_heads;
+  m.U = rows_per_query(*s);
+  m.k_cap = s->k_cap;
+  m.q = a.q;
+  m.K = a.K;
+  m.V = a.V;
+  m.sb = a.sb;
+  m.sh = a.sh;
+  m.ss = a.ss;
+  m.block_table = a.bs_log2 >= 0 ? a.block_table : nullptr;
+  m.bs_log2 = a.bs_log2 >= 0 ? a.bs_log2 : 0;
+  m.nblk = a.nblk;
+  m.zscale = a.zscale;
   m.dtype = s->dtype;
   m.stats = a.stats;
   m.acc = a.acc;
@@ -335,11 +352,17 @@ vp_status launch_step(const vp_shape* shape, const vp_layout* layout, const vp_p
   t.segtab = a.segtab;
   if (hipError_t e = launch_select(t, st)) return hip_fail(e, "select launch");
   if (hipError_t e = mark(3)) return hip_fail(e, "event record");
-  // the kept rows are visual rows of this step's spill: their logits are read
-  // from it, so the kept pass reads V rows only
-  if (hipError_t e = launch_attend(a, MODE_KEPT | MODE_ZSPILL, dt, hd, st)) return hip_fail(e, "kept pass launch");
-  if (hipError_t e = mark(4)) return hip_fail(e, "event record");
-  if (hipError_t e = launch_merge(merge_args(shape, plan, a, out), hd, st)) return hip_fail(e, "merge launch");
+  if (plan.merge_kept) {
+    // a small step: the kept rows are merged directly (no kept pass)
+    if (hipError_t e = mark(4)) return hip_fail(e, "event record");
+    if (hipError_t e = launch_merge_kept(merge_args(shape, plan, a, out), hd, st)) return hip_fail(e, "merge launch");
+  } else {
+    // the kept rows are visual rows of this step's spill: their logits are read
+    // from it, so the kept pass reads V rows only
+    if (hipError_t e = launch_attend(a, MODE_KEPT | MODE_ZSPILL, dt, hd, st)) return hip_fail(e, "kept pass launch");
+    if (hipError_t e = mark(4)) return hip_fail(e, "event record");
+    if (hipError_t e = launch_merge(merge_args(shape, plan, a, out), hd, st)) return hip_fail(e, "merge launch");
+  }
   if (hipError_t e = mark(5)) return hip_fail(e, "event record");
   return VP_OK;
 }
@@ -579,6 +602,16 @@ vp_status vp_sparse_decode_attn(const vp_shape* shape, const vp_layout* layout, 
   AttendArgs a = attend_args(shape, layout, params, plan, ws, q, K, V);
   a.vis_idx = vis_idx;
   a.kk = k;
+  if (plan.merge_kept) {
+    // a small step: the kept rows are merged directly (no kept pass)
+    if (!(flags & VP_ATTN_TEXT_FROM_WORKSPACE)) {
+      if (hipError_t e = launch_attend(a, MODE_TEXT_ATTN, shape->dtype, shape->head_dim, st))
+        return hip_fail(e, "text pass launch");
+    }
+    if (hipError_t e = launch_merge_kept(merge_args(shape, plan, a, out), shape->head_dim, st))
+      return hip_fail(e, "merge launch");
+    return VP_OK;
+  }
   if (!(flags & VP_ATTN_TEXT_FROM_WORKSPACE) && plan.text_kept_one_launch) {
     // a layer that reads its own text rows: the text and kept passes share one launch
     if (hipError_t e = launch_attend(a, MODE_TEXT_KEPT, shape->dtype, shape->head_dim, st))

@@ -30,6 +30,7 @@ struct Plan {
   int split;    // kept rows per kept-pass work-group (multiple of 32)
   int nsplit;   // ceil(k_cap / split)
   bool text_kept_one_launch;  // a later layer's text and kept passes fit one resident round together
+  bool merge_kept;            // the step folds the kept rows into the merge (no kept pass)
   int zs_rows;    // rows per spill plane: max_seq_len rounded up to 32
   int zs_gp;      // floats per spill row: the query group padded to 8 or 16
   size_t zs;      // float [B][Hkv][zs_rows][zs_gp]  visual logits (log2 domain) by cache position
@@ -204,9 +205,28 @@ struct MergeArgs {
   const float* kstats;
   const float* kacc;
   void* out;
+  // merge of the kept rows themselves (launch_merge_kept): their positions,
+  // the query rows and the kept K and V rows
+  const int32_t* seq_len;
+  const int32_t* vis_idx;  // [B*T*U][k_cap]
+  const int32_t* kk;       // [B*T*U] budgets
+  int max_seq_len, Hkv, U, k_cap;
+  const void* q;
+  const void* K;
+  const void* V;
+  int64_t sb, sh, ss;  // K/V strides (elements); paged caches: sb is the block stride
+  const int32_t* block_table;  // paged caches: [B][nblk] physical blocks (else null)
+  int bs_log2, nblk;           // paged caches: log2 of the rows per block, table row stride
+  float zscale;        // sm_scale * log2(e)
 };
 
 hipError_t launch_merge(const MergeArgs& a, int head_dim, hipStream_t st);
+// The kept rows' attention folded into the merge, for small steps (plan.merge_kept):
+// bf16 caches.
+hipError_t launch_merge_kept(const MergeArgs& a, int head_dim, hipStream_t st);
+// capacities of launch_merge_kept's single batch: text parts and kept rows per head
+int merge_kept_max_parts(int head_dim);
+int merge_kept_max_rows(int head_dim);
 
 // one read of `bytes` (a multiple of 16 KiB) at src: mode 0 vector loads, 1 LDS copies
 hipError_t launch_stream_read(const void* src, size_t bytes, int mode, uint32_t* sink, hipStream_t st);

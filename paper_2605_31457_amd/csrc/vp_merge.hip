@@ -143,7 +143,170 @@ __global__ __launch_bounds__(kMergeThreads) void merge_kernel(const MergeArgs a)
   }
 }
 
+constexpr int kKeptHeld = 8;  // kept rows a lane group holds (k_cap <= kKeptHeld * R)
+
+// four bf16 values (two 32-bit words, low half first) as floats
+__device__ __forceinline__ float4 bf16x4_to_f32(uint2 u) {
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u), __uint_as_float(u.y << 16),
+                     __uint_as_float(u.y & 0xffff0000u));
+}
+
+// The kept rows' attention folded into the merge: each kept row of the head's
+// selection row is one more "partial" with maximum z (its logit, q.K scaled to
+// the log2 domain, summed over the lane group's columns in a fixed butterfly),
+// sum 1 and value row V (the weight is 2^(z - M) like a partial's). For small
+// steps (a handful of kept work-groups would leave the GPU idle): one launch
+// fewer. Every path that merges uses this kernel for such steps, so the step and
+// the four calls give the same bits.
+// Every kept slot up to k_cap is requested with the budget, the length and the
+// text partials; entries past the budget and positions outside [0, L) are skipped.
+template <int D>
+__global__ __launch_bounds__(kMergeThreads) void merge_kept_kernel(const MergeArgs a) {
+  constexpr int COLS = D / 4;
+  constexpr int R = kMergeThreads / COLS;
+  __shared__ float s_red[kMergeThreads / 64];
+  __shared__ float4 s_num[R][COLS];
+  __shared__ float s_den[R];
+  const int x = blockIdx.x;  // t*Hq + h
+  const int qt = x / a.Hq;
+  const int h = x - qt * a.Hq;
+  const int b = blockIdx.y;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wid = tid >> 6;
+  const int col = tid % COLS;
+  const int r = tid / COLS;
+  const int g = h / a.G;
+  const int nc = a.nparts;
+  const size_t bh = static_cast<size_t>(b) * a.T * a.Hq + vhead(h, qt, a.G, a.T);
+  const size_t ob = static_cast<size_t>(b) * a.T * a.Hq + x;
+  const float* st = a.stats + bh * a.nparts * 8;
+  const float4* ac = reinterpret_cast<const float4*>(a.acc + bh * a.nparts * D) + col;
+  const size_t srow = (static_cast<size_t>(b) * a.T + qt) * a.U + g / (a.Hkv / a.U);  // the head's selection row
+  const int32_t* kl = a.vis_idx + srow * a.k_cap;
+  // first round trip: the text partials, the kept positions, the budget, the
+  // length and this lane's four query columns
+  const int L = clamp_len(a.seq_len[b], a.max_seq_len);
+  const int kb = a.kk[srow];
+  const uint2 qu = reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(a.q) + ob * D)[col];
+  const float4 qv = bf16x4_to_f32(qu);
+  float2 v[kHeld];
+  float4 xv[kHeld];
+#pragma unroll
+  for (int j = 0; j < kHeld; ++j) {
+    const int i = r + j * R;
+    const int ii = i < nc ? i : 0;
+    v[j] = *reinterpret_cast<const float2*>(st + ii * 8 + 4);
+    xv[j] = ac[static_cast<size_t>(ii) * COLS];
+    if (i >= nc) v[j] = make_float2(kNegInf, 0.f);
+  }
+  int pos[kKeptHeld];
+#pragma unroll
+  for (int j = 0; j < kKeptHeld; ++j) {
+    const int i = r + j * R;
+    pos[j] = i < a.k_cap ? kl[i] : -1;
+  }
+  // each kept row's K and V columns (paged caches: after its block id)
+  bool okk[kKeptHeld];
+  size_t off[kKeptHeld];
+#pragma unroll
+  for (int j = 0; j < kKeptHeld; ++j) {
+    okk[j] = r + j * R < kb && pos[j] >= 0 && pos[j] < L;
+    const int p = okk[j] ? pos[j] : 0;
+    if (a.block_table) {
+      const int blk = a.block_table[static_cast<size_t>(b) * a.nblk + (p >> a.bs_log2)];
+      off[j] = static_cast<size_t>(blk) * a.sb + static_cast<size_t>(g) * a.sh +
+               static_cast<size_t>(p & ((1 << a.bs_log2) - 1)) * a.ss;
+    } else {
+      off[j] = static_cast<size_t>(b) * a.sb + static_cast<size_t>(g) * a.sh + static_cast<size_t>(p) * a.ss;
+    }
+  }
+  uint2 ku[kKeptHeld], vu[kKeptHeld];
+#pragma unroll
+  for (int j = 0; j < kKeptHeld; ++j) {
+    ku[j] = reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(a.K) + off[j])[col];
+    vu[j] = reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(a.V) + off[j])[col];
+  }
+  float zk[kKeptHeld];
+  float4 vk[kKeptHeld];
+#pragma unroll
+  for (int j = 0; j < kKeptHeld; ++j) {
+    const float4 kf = bf16x4_to_f32(ku[j]);
+    float z = ((qv.x * kf.x + qv.y * kf.y) + (qv.z * kf.z + qv.w * kf.w));
+#pragma unroll
+    for (int o = 1; o < COLS; o <<= 1) z += __shfl_xor(z, o);  // the row's COLS column lanes
+    zk[j] = okk[j] ? z * a.zscale : kNegInf;
+    vk[j] = bf16x4_to_f32(vu[j]);
+  }
+  float M = kNegInf;
+#pragma unroll
+  for (int j = 0; j < kHeld; ++j)
+    if (v[j].y > 0.f) M = fmaxf(M, v[j].x);
+#pragma unroll
+  for (int j = 0; j < kKeptHeld; ++j) M = fmaxf(M, zk[j]);
+  M = block_max(M, s_red, lane, wid);
+  float4 num = make_float4(0.f, 0.f, 0.f, 0.f);
+  float den = 0.f;
+#pragma unroll
+  for (int j = 0; j < kHeld; ++j) {
+    if (v[j].y > 0.f) {
+      const float w = fast_exp2(v[j].x - M);
+      den += w * v[j].y;
+      num.x += w * xv[j].x;
+      num.y += w * xv[j].y;
+      num.z += w * xv[j].z;
+      num.w += w * xv[j].w;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < kKeptHeld; ++j) {
+    if (zk[j] != kNegInf) {
+      const float w = fast_exp2(zk[j] - M);
+      den += w;
+      num.x += w * vk[j].x;
+      num.y += w * vk[j].y;
+      num.z += w * vk[j].z;
+      num.w += w * vk[j].w;
+    }
+  }
+  s_num[r][col] = num;
+  if (col == 0) s_den[r] = den;
+  __syncthreads();
+  if (r == 0) {
+    float dd = 0.f;
+    float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+    for (int j = 0; j < R; ++j) {
+      const float4 y = s_num[j][col];
+      o.x += y.x;
+      o.y += y.y;
+      o.z += y.z;
+      o.w += y.w;
+      dd += s_den[j];
+    }
+    const float inv = dd > 0.f ? 1.0f / dd : 0.f;
+    uint2 packed;
+    packed.x = f32_to_bf16_bits(o.x * inv) | (static_cast<uint32_t>(f32_to_bf16_bits(o.y * inv)) << 16);
+    packed.y = f32_to_bf16_bits(o.z * inv) | (static_cast<uint32_t>(f32_to_bf16_bits(o.w * inv)) << 16);
+    reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + ob * D)[col] = packed;
+  }
+}
+
 }  // namespace
+
+int merge_kept_max_parts(int head_dim) { return kHeld * (kMergeThreads / (head_dim / 4)); }
+int merge_kept_max_rows(int head_dim) { return kKeptHeld * (kMergeThreads / (head_dim / 4)); }
+
+hipError_t launch_merge_kept(const MergeArgs& a, int head_dim, hipStream_t st) {
+  const dim3 grid(a.T * a.Hq, a.B);
+  if (head_dim == 128)
+    hipLaunchKernelGGL(merge_kept_kernel<128>, grid, dim3(kMergeThreads), 0, st, a);
+  else if (head_dim == 64)
+    hipLaunchKernelGGL(merge_kept_kernel<64>, grid, dim3(kMergeThreads), 0, st, a);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
 
 hipError_t launch_merge(const MergeArgs& a, int head_dim, hipStream_t st) {
   const dim3 grid(a.T * a.Hq, a.B);

@@ -45,6 +45,10 @@ bool use_dual(const vp_shape* s) {
 #define VP_KEPT_WGS 2048  // kept-pass work-groups in one resident round (8 per CU)
 #endif
 
+#ifndef VP_MERGE_KEPT_WGS
+#define VP_MERGE_KEPT_WGS 64  // kept-pass work-groups at most for the kept rows to be merged directly
+#endif
+
 #ifndef VP_SELECT_WGS
 #define VP_SELECT_WGS 256  // target work-groups of the select launch: one per CU
 #endif
@@ -86,6 +90,12 @@ Plan make_plan(const vp_shape& s) {
   // the text pass is split over two (the 64 x 32k batch: 3081 -> 3663 us).
   p.text_kept_one_launch = static_cast<int64_t>(p.nparts + queries(s) * p.nsplit) * s.n_kv_heads * s.batch <=
                            static_cast<int64_t>(VP_KEPT_WGS);
+  // A step whose kept pass would be a handful of work-groups folds the kept
+  // rows into the merge (their K and V rows read there): bf16 caches, every
+  // text part and kept row in one batch per head.
+  p.merge_kept = s.dtype == VP_BF16 &&
+                 static_cast<int64_t>(p.nsplit) * queries(s) * s.n_kv_heads * s.batch <= VP_MERGE_KEPT_WGS &&
+                 p.nparts <= merge_kept_max_parts(s.head_dim) && s.k_cap <= merge_kept_max_rows(s.head_dim);
   // per-head arrays hold one entry per query row (virtual head): T*Hq per sequence
   const size_t B = s.batch, Hq = static_cast<size_t>(s.n_q_heads) * queries(s), d = s.head_dim;
   p.zs_rows = ((s.max_seq_len + 31) / 32) * 32;
