@@ -329,10 +329,17 @@ vp_status vp_decode_step_static(const vp_shape* shape, const vp_layout* layout, 
  *   VP_PLAN_FUSED_TAIL          vp_decode_step's select launch scores and
  *                               selects each sequence in a single work-group
  *                               (small visual sets; otherwise in chunks, the
- *                               last chunk selecting).
+ *                               last chunk selecting);
+ *   VP_PLAN_KEPT_IN_MERGE       small steps: vp_decode_step and
+ *                               vp_sparse_decode_attn(VP_ATTN_TEXT_FROM_WORKSPACE)
+ *                               read the kept rows in the merge launch (no kept
+ *                               pass); vp_sparse_decode_attn without that flag
+ *                               keeps its kept pass, so its output then agrees
+ *                               with theirs to rounding, not bit for bit.
  */
 #define VP_PLAN_ONE_CONTEXT_LAUNCH 1
 #define VP_PLAN_FUSED_TAIL 2
+#define VP_PLAN_KEPT_IN_MERGE 4
 vp_status vp_step_plan(const vp_shape* shape, const vp_params* params, int32_t* flags);
 
 /*

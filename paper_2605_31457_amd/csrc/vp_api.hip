@@ -557,7 +557,9 @@ vp_status vp_step_plan(const vp_shape* shape, const vp_params* params, int32_t* 
   if (vp_status e = check_shape(shape)) return e;
   if (vp_status e = check_params(params)) return e;
   if (!flags) return fail(VP_ERR_NULL, "flags is NULL");
-  *flags = (use_dual(shape) ? VP_PLAN_ONE_CONTEXT_LAUNCH : 0) | (make_plan(*shape).sel_chunks == 1 ? VP_PLAN_FUSED_TAIL : 0);
+  const Plan plan = make_plan(*shape);
+  *flags = (use_dual(shape) ? VP_PLAN_ONE_CONTEXT_LAUNCH : 0) | (plan.sel_chunks == 1 ? VP_PLAN_FUSED_TAIL : 0) |
+           (plan.merge_kept ? VP_PLAN_KEPT_IN_MERGE : 0);
   return VP_OK;
 }
 
@@ -602,12 +604,10 @@ vp_status vp_sparse_decode_attn(const vp_shape* shape, const vp_layout* layout, 
   AttendArgs a = attend_args(shape, layout, params, plan, ws, q, K, V);
   a.vis_idx = vis_idx;
   a.kk = k;
-  if (plan.merge_kept) {
-    // a small step: the kept rows are merged directly (no kept pass)
-    if (!(flags & VP_ATTN_TEXT_FROM_WORKSPACE)) {
-      if (hipError_t e = launch_attend(a, MODE_TEXT_ATTN, shape->dtype, shape->head_dim, st))
-        return hip_fail(e, "text pass launch");
-    }
+  if ((flags & VP_ATTN_TEXT_FROM_WORKSPACE) && plan.merge_kept) {
+    // a small step's attention: the kept rows are merged directly, as in
+    // vp_decode_step (a layer that reads its own text rows instead runs its
+    // kept pass in the text pass's launch, below: faster for later layers)
     if (hipError_t e = launch_merge_kept(merge_args(shape, plan, a, out), shape->head_dim, st))
       return hip_fail(e, "merge launch");
     return VP_OK;

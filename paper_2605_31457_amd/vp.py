@@ -185,6 +185,7 @@ def vp_budget(shape, layout, params, mass_seq, k, stream=None):
 
 VP_PLAN_ONE_CONTEXT_LAUNCH = 1
 VP_PLAN_FUSED_TAIL = 2
+VP_PLAN_KEPT_IN_MERGE = 4
 
 
 def vp_step_plan(shape, params) -> int:

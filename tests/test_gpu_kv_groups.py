@@ -11,7 +11,7 @@ the four calls give bit-identical results.
 import numpy as np
 import pytest
 
-from _parity import check_groups, small_workload
+from _parity import assert_step_equals_calls, check_groups, kept_in_merge, small_workload
 from oracle import plant as P
 from oracle import vp_oracle as O
 from paper_2605_31457_amd import step as S
@@ -31,11 +31,10 @@ def _step_and_calls(w, **kw):
     ds = S.DeviceStep(w, kv_groups=True, **kw)
     ds.decode_step()
     g = ds.results()
+    merged = kept_in_merge(ds)
     for fused in (True, False):
         ds.run(fused=fused)
-        c = ds.results()
-        for key in KEYS:
-            assert np.array_equal(g[key], c[key]), f"{key} differs between the step and the calls (fused={fused})"
+        assert_step_equals_calls(g, ds.results(), fused, merged)
     return ds, g
 
 

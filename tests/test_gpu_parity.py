@@ -9,7 +9,8 @@ import numpy as np
 import pytest
 import torch
 
-from _parity import check_sequence, small_workload, tile_batch
+from _parity import (ROUNDING_ATOL, ROUNDING_RTOL, assert_step_equals_calls, check_sequence, kept_in_merge,
+                     small_workload, tile_batch)
 from oracle import plant as P
 from oracle import vp_oracle as O
 from paper_2605_31457_amd import step as S
@@ -81,17 +82,17 @@ def test_small_shapes(name):
         _, g = _run(w, fused=fused)
         for b in range(w.B):
             check_sequence(f"{name} fused={fused}", w, g, b, ref[b])
-    _step_equals_calls(w, g)
+    _step_equals_calls(w, g, fused=False)
 
 
-def _step_equals_calls(w, calls, ds=None, **kw):
-    """vp_decode_step gives exactly what the four calls give (same arithmetic and
-    reduction order), and so passes the same reference checks."""
+def _step_equals_calls(w, calls, ds=None, fused=True, **kw):
+    """vp_decode_step gives what the four calls give (the same arithmetic and
+    reduction order: bit for bit when the calls took the text part from the
+    workspace), and so passes the same reference checks."""
     ds = ds or S.DeviceStep(w, **kw)
     ds.decode_step()
     g = ds.results()
-    for key in ("mass_head", "mass_seq", "scores", "k", "vis_idx", "out"):
-        assert np.array_equal(g[key], calls[key]), key
+    assert_step_equals_calls(g, calls, fused, kept_in_merge(ds))
     return g
 
 
@@ -133,15 +134,19 @@ def test_fused_and_unfused_text_paths_agree():
     """The text attention computed inside the mass pass (fused) and by the
     attention call itself (unfused) are separately compiled kernels: discrete
     results are identical, real ones agree to a few fp32 ulps (bf16 output to
-    one bf16 ulp)."""
+    one bf16 ulp). Where the fused path reads the kept rows in the merge, its
+    output differs from the kept pass's by that pass's bf16 probabilities."""
     w = W.generate(2)
-    _, a = _run(w, fused=True)
+    ds, a = _run(w, fused=True)
     _, b = _run(w, fused=False)
     for key in ("k", "vis_idx"):
         assert np.array_equal(a[key], b[key]), key
     for key in ("mass_head", "mass_seq", "scores"):
         np.testing.assert_allclose(a[key], b[key], rtol=4e-6, atol=1e-30, err_msg=key)
-    np.testing.assert_allclose(a["out"], b["out"], rtol=8e-3, atol=1e-6)
+    if kept_in_merge(ds):
+        np.testing.assert_allclose(a["out"], b["out"], rtol=ROUNDING_RTOL, atol=ROUNDING_ATOL)
+    else:
+        np.testing.assert_allclose(a["out"], b["out"], rtol=8e-3, atol=1e-6)
 
 
 def test_repeat_runs_are_bitwise_identical():
@@ -311,7 +316,8 @@ def test_zero_length_sequence_in_a_batch():
     """A sequence of length 0 between two others gets the empty context's
     results (masses 0, budget 0, no kept rows, output 0) from the four calls and
     from the step alike; its neighbours still match the reference, and the step
-    equals the four calls bit for bit. Every context-pass part and kept split of
+    equals the four calls (bit for bit but for the attention output of a step
+    that reads its kept rows in the merge). Every context-pass part and kept split of
     the empty sequence writes an empty partial, which the merge reads."""
     w = small_workload(seed=21, B=3, Hq=8, Hkv=2, d=64, lens=[120, 40, 90], segs=[[(10, 60)], [(0, 20)], [(0, 40)]])
     ref, _ = P.plant(w, P.params_of(w))
@@ -332,8 +338,8 @@ def test_zero_length_sequence_in_a_batch():
     ds.out.fill_(7.0)
     ds.decode_step()
     g = ds.results()
-    for key in ("mass_head", "mass_seq", "scores", "k", "vis_idx", "out"):
-        assert np.array_equal(g[key], got[False][key]), key
+    assert_step_equals_calls(g, got[False], False, kept_in_merge(ds), "zero-length batch")
+    assert np.all(g["out"][1].astype(np.float32) == 0.0)
 
 
 PRESETS = {

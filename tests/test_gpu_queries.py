@@ -12,7 +12,7 @@ and budget margin at once, outputs within bf16 atol 2e-2 / rtol 1e-2 (fp32
 import numpy as np
 import pytest
 
-from _parity import check_groups, check_sequence, small_workload
+from _parity import assert_step_equals_calls, check_groups, check_sequence, kept_in_merge, small_workload
 from oracle import plant as P
 from paper_2605_31457_amd import step as S
 from paper_2605_31457_amd import workloads as W
@@ -30,11 +30,10 @@ def _step_and_calls(w, **kw):
     ds = S.DeviceStep(w, **kw)
     ds.decode_step()
     g = ds.results()
+    merged = kept_in_merge(ds)
     for fused in (True, False):
         ds.run(fused=fused)
-        c = ds.results()
-        for key in KEYS:
-            assert np.array_equal(g[key], c[key]), f"{key} differs between the step and the calls (fused={fused})"
+        assert_step_equals_calls(g, ds.results(), fused, merged)
     return ds, g
 
 
