@@ -281,7 +281,9 @@ vp_status vp_sparse_decode_attn(const vp_shape* shape, const vp_layout* layout, 
  *   [1] when the text pass starts executing, [2] when it ends (attached to
  *       that launch: [1]..[2] is its execution alone, as a profiler sees it;
  *       with VP_PLAN_ONE_CONTEXT_LAUNCH, the one launch of both passes)
- *   [3] before the kept-row pass  [4] before the merge  [5] after the merge.
+ *   [3] before the kept-row pass  [4] before the merge  [5] after the merge
+ *   (with VP_PLAN_KEPT_IN_MERGE there is no kept-row pass: [3] and [4] both
+ *   mark the start of the merge).
  * Errors as for the four calls; VP_ERR_RANGE if n_events is outside
  * [0, VP_STEP_EVENTS]. The workspace must not be shared by concurrent calls.
  */
