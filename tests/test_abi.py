@@ -205,6 +205,38 @@ def test_header_constants_match_binding():
     assert int(consts["VP_ATTN_TEXT_FROM_WORKSPACE"]) == vp.VP_ATTN_TEXT_FROM_WORKSPACE
 
 
+def test_header_plan_flags_match_binding():
+    text = open(HEADER).read()
+    consts = dict(re.findall(r"#define\s+(VP_PLAN_[A-Z_]+)\s+(\d+)", text))
+    assert {k: int(v) for k, v in consts.items()} == {
+        "VP_PLAN_ONE_CONTEXT_LAUNCH": vp.VP_PLAN_ONE_CONTEXT_LAUNCH, "VP_PLAN_FUSED_TAIL": vp.VP_PLAN_FUSED_TAIL,
+        "VP_PLAN_KEPT_IN_MERGE": vp.VP_PLAN_KEPT_IN_MERGE}
+
+
+def _bench_shape(B, Hq, Hkv, S, n_vis, k_cap, **kw):
+    return _shape(batch=B, n_q_heads=Hq, n_kv_heads=Hkv, max_seq_len=S, max_vis=n_vis, max_segs=4, k_cap=k_cap,
+                  kv_stride_b=Hkv * S * 128, kv_stride_h=S * 128, **kw)
+
+
+@pytest.mark.parametrize("name, shape_kw, want", [
+    # 1 x 3358 tokens (1296 visual): one context launch, kept rows read in the merge
+    ("7b-b1", dict(B=1, Hq=28, Hkv=4, S=3358, n_vis=1296, k_cap=64), 1 | 4),
+    # 16 x up to 12288 tokens: one context launch, a kept pass of 448 work-groups
+    ("7b-b16", dict(B=16, Hq=28, Hkv=4, S=12288, n_vis=4096, k_cap=204), 1),
+    # 64 x 32768 tokens: visual and text passes in two launches, chunked selection
+    ("7b-b64-32k", dict(B=64, Hq=28, Hkv=4, S=32768, n_vis=16384, k_cap=819), 0),
+    # 8 x 11008 tokens of the 72B-class shape
+    ("72b-b8", dict(B=8, Hq=64, Hkv=8, S=11008, n_vis=6400, k_cap=320), 1),
+    # fp32 caches never read their kept rows in the merge
+    ("7b-b1-f32", dict(B=1, Hq=28, Hkv=4, S=3358, n_vis=1296, k_cap=64, dtype=vp.VP_F32), 1),
+    # a kept list longer than the merge holds in one batch
+    ("7b-b1-long-list", dict(B=1, Hq=28, Hkv=4, S=3358, n_vis=1296, k_cap=96), 1),
+])
+def test_step_plan_of_the_benchmark_shapes(L, name, shape_kw, want):
+    """vp_step_plan is pure host logic: the launch plans the benchmark shapes take."""
+    assert vp.vp_step_plan(_bench_shape(**shape_kw), _params()) == want, name
+
+
 def test_status_strings(L):
     assert vp.vp_status_string(0) == "VP_OK" and vp.vp_status_string(7) == "VP_ERR_HIP"
 
