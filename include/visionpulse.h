@@ -254,7 +254,9 @@ vp_status vp_select_topk(const vp_shape* shape, const vp_layout* layout,
  *   out[b, h] = sum_{j in J_b} softmax_{J_b}(Z_{h, j}) V_{g(h), j}      [B, T, Hq, d]
  *
  * An empty J_b yields zeros. Kept indices outside [0, seq_len) or equal to -1
- * are skipped. With flags & VP_ATTN_TEXT_FROM_WORKSPACE the text part is taken
+ * are skipped. The kept indices are taken to be distinct visual positions, as
+ * vp_select_topk writes them: a repeated index, or a text position, adds that
+ * row's term once more (the union above then counts it twice). With flags & VP_ATTN_TEXT_FROM_WORKSPACE the text part is taken
  * from the workspace filled by vp_visual_mass (V non-NULL, same inputs);
  * otherwise this call reads the text K/V itself.
  */
