@@ -156,8 +156,11 @@ __device__ __forceinline__ float4 bf16x4_to_f32(uint2 u) {
 // the log2 domain, summed over the lane group's columns in a fixed butterfly),
 // sum 1 and value row V (the weight is 2^(z - M) like a partial's). For small
 // steps (a handful of kept work-groups would leave the GPU idle): one launch
-// fewer. Every path that merges uses this kernel for such steps, so the step and
-// the four calls give the same bits.
+// fewer. Every path that merges with the text part from the workspace (the step,
+// and vp_sparse_decode_attn given VP_ATTN_TEXT_FROM_WORKSPACE) uses this kernel
+// for such steps, so the step and the four calls give the same bits; a layer
+// that reads its own text rows keeps its kept pass (there the kept work-groups
+// fill the text pass's tail).
 // Every kept slot up to k_cap is requested with the budget, the length and the
 // text partials; entries past the budget and positions outside [0, L) are skipped.
 template <int D>
