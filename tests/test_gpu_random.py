@@ -15,7 +15,7 @@ from paper_2605_31457_amd import workloads as W
 pytestmark = pytest.mark.gpu
 
 KEYS = ("mass_head", "mass_seq", "scores", "k", "vis_idx", "out")
-N_CASES = 40
+N_CASES = 120
 
 
 def _case(i):
