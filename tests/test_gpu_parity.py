@@ -270,6 +270,46 @@ def test_sparse_attention_on_given_selection():
         np.testing.assert_allclose(got, rr.out, atol=2e-2, rtol=1e-2)
 
 
+def test_kept_list_entries_that_are_skipped():
+    """vp_sparse_decode_attn with the text part from the workspace, on a kept list
+    holding -1, positions at or past the sequence length and entries past the
+    budget among real kept positions: the skipped entries add nothing, on the
+    launch plan of this shape (the kept rows read in the merge at the 1-sequence
+    batch, a kept pass otherwise), against the reference attention over the rest."""
+    for cfg, B in ((2, None), (3, 4)):
+        w = W.generate(cfg, B=B) if B else W.generate(cfg)
+        ds = S.DeviceStep(w)
+        ds.visual_mass(fused=True)
+        G = w.Hq // w.Hkv
+        sm = 1.0 / np.sqrt(w.d)
+        kc = ds.k_cap
+        idx = np.full((w.B, kc), -1, np.int32)
+        k = np.zeros(w.B, np.int32)
+        want = []
+        for b in range(w.B):
+            L = int(w.seq_len[b])
+            vis = O.visual_positions(L, w.segments[b])
+            rng = np.random.default_rng(40 + b)
+            take = np.sort(rng.choice(vis, size=min(len(vis), kc // 2), replace=False)).astype(np.int32)
+            row = list(take[: len(take) // 2]) + [-1, L, L + 5] + list(take[len(take) // 2:])
+            k[b] = min(kc - 2, len(row))
+            row = row[: k[b]] + [int(take[0]), int(take[1])]  # entries past the budget: ignored
+            idx[b, : len(row)] = row
+            kept = np.array([x for x in row[: k[b]] if 0 <= x < L], np.int64)
+            J = np.sort(np.concatenate([kept, O.text_positions(L, w.segments[b])]))
+            qf = O.as_f64(w.q[b])
+            want.append(np.stack([O.pruned_attention(qf[h], w.K[b, h // G], w.V[b, h // G], J, sm)
+                                  for h in range(w.Hq)]))
+        ds.vis_idx.copy_(torch.from_numpy(idx))
+        ds.k.copy_(torch.from_numpy(k))
+        ds.sparse_decode_attn(fused=True)
+        got = ds.results()["out"]
+        plan = S.vp.vp_step_plan(ds.shape, ds.params)
+        for b in range(w.B):
+            np.testing.assert_allclose(got[b], want[b], atol=2e-2, rtol=1e-2,
+                                       err_msg=f"config {cfg} seq {b} (plan flags {plan})")
+
+
 def _clip_layout(L, segs):
     """The documented reading of an unclean device layout: segments are taken in
     order, each clipped to [end of the previous one, L); lengths < 0 count as 0."""
