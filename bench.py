@@ -161,7 +161,7 @@ def stream_ceiling(hip, sp, nbytes=4 << 30, reps=5):
 
 def _cores():
     """Cores this process may use for the reference: its CPU affinity, capped by
-    OMP_NUM_THREADS when that is set (a GPU machine's share of a larger host)."""
+    OMP_NUM_THREADS when that is set (one machine's share of a larger host)."""
     n = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else (os.cpu_count() or 1)
     env = os.environ.get("OMP_NUM_THREADS")
     if env and env.isdigit() and int(env) > 0:
