@@ -292,10 +292,11 @@ def measured_parity(w, gpu, ref, p, O):
 
 
 def bench_layers(args, w, ds, bufs, loop, steps, warmup, sp, hip):
-    """A per-token attention step over L layers, timed as a whole: the anchor
-    layer's vp_decode_step and L-1 calls of vp_sparse_decode_attn on the other
-    layers' caches with the anchor's kept set (Sec. 4.1: layers after the
-    anchor reuse its selection); with --dense, L layers of full attention
+    """A per-token attention step over L layers, timed as a whole: A =
+    --anchor-layer layers of full attention (pruning starts at the anchor layer,
+    Sec. 4.1), the anchor layer's vp_decode_step, and L-A-1 calls of
+    vp_sparse_decode_attn on the later layers' caches with the anchor's kept set
+    (they reuse its selection); with --dense, L layers of full attention
     (vp_sparse_decode_attn on a layout with no visual segments, so every cached
     row goes through the streaming text pass). Layer l of step i reads cache
     copy (i * L + l) mod R."""
@@ -303,9 +304,10 @@ def bench_layers(args, w, ds, bufs, loop, steps, warmup, sp, hip):
     import torch
     from paper_2605_31457_amd import vp
     L, R = args.layers, len(bufs)
+    A = 0 if args.dense else args.anchor_layer
     out_l = torch.empty_like(ds.out)
     lay_dense = None
-    if args.dense:
+    if args.dense or A > 0:
         seg_off0 = torch.zeros(w.B + 1, dtype=torch.int32, device=ds.device)
         seg0 = torch.zeros(2, dtype=torch.int32, device=ds.device)
         k0 = torch.zeros(w.B, dtype=torch.int32, device=ds.device)
@@ -324,10 +326,14 @@ def bench_layers(args, w, ds, bufs, loop, steps, warmup, sp, hip):
                 vp.vp_sparse_decode_attn(ds.shape, lay_dense[t], ds.params, q, K, V, ds.vis_idx, k0, out_l, 0,
                                          ds.ws, ds.ws_bytes, sp)
             return
-        K, V = bufs[(i * L) % R]
+        for layer in range(A):
+            K, V = bufs[(i * L + layer) % R]
+            vp.vp_sparse_decode_attn(ds.shape, lay_dense[t], ds.params, q, K, V, ds.vis_idx, k0, out_l, 0,
+                                     ds.ws, ds.ws_bytes, sp)
+        K, V = bufs[(i * L + A) % R]
         vp.vp_decode_step(ds.shape, lay, ds.params, q, K, V, ds.mass_head, ds.mass_seq, ds.scores, ds.k,
                           ds.vis_idx, ds.out, ds.ws, ds.ws_bytes, sp)
-        for layer in range(1, L):
+        for layer in range(A + 1, L):
             K, V = bufs[(i * L + layer) % R]
             vp.vp_sparse_decode_attn(ds.shape, lay, ds.params, q, K, V, ds.vis_idx, ds.k, out_l, 0,
                                      ds.ws, ds.ws_bytes, sp)
@@ -345,19 +351,20 @@ def bench_layers(args, w, ds, bufs, loop, steps, warmup, sp, hip):
                            kv_per_row=w.Hkv // ds.rows)
     esz = 2 if w.dtype == "bf16" else 4
     row = w.Hkv * w.d * esz
-    if args.dense:
-        # every cached K and V row of every sequence, per layer
-        if loop:
-            per_layer = w.B * 2 * row * sum(loop[3]) / len(loop[3])
-        else:
-            per_layer = sum(2 * int(n) * row for n in w.seq_len)
-        step_bytes = L * per_layer
+    # a dense layer: every cached K and V row of every sequence
+    if loop:
+        per_dense = w.B * 2 * row * sum(loop[3]) / len(loop[3])
     else:
-        step_bytes = nb["visual"] + nb["text"] + nb["kept"] + (L - 1) * (nb["text"] + nb["kept"])
+        per_dense = sum(2 * int(n) * row for n in w.seq_len)
+    if args.dense:
+        step_bytes = L * per_dense
+    else:
+        step_bytes = A * per_dense + nb["visual"] + nb["text"] + nb["kept"] + (L - A - 1) * (nb["text"] + nb["kept"])
     ms = wall * 1e3 / steps
     res = {"metric": "per-token attention steps/s over several layers", "value": steps / wall, "unit": "steps/s",
            "n_gpus": 1, "steps": steps, "warmup": warmup, "ms_per_step": ms, "higher_is_better": True,
-           "layers": L, "mode": "dense" if args.dense else "anchor decode step + sparse layers",
+           "layers": L, "anchor_layer": A,
+           "mode": "dense" if args.dense else "dense layers, anchor decode step, sparse layers",
            "step_algorithmic_bytes": step_bytes, "step_achieved_GBps": step_bytes / (ms * 1e-3) / 1e9,
            "dtype": w.dtype, "data": "synthetic", "config": {"workload": f"config {args.config}: "
                                                              f"{WORKLOAD_NAMES[args.config]}", "kv_copies": R}}
@@ -378,6 +385,8 @@ def main():
     ap.add_argument("--layers", type=int, default=1,
                     help="time a per-token step over this many layers: the anchor layer's decode step, then "
                          "every other layer's attention over the anchor's kept set on its own KV cache")
+    ap.add_argument("--anchor-layer", type=int, default=0, metavar="A",
+                    help="with --layers L: layers 0..A-1 attend densely, layer A is the anchor (0 <= A < L)")
     ap.add_argument("--dense", action="store_true",
                     help="with --layers: every layer attends to all of its cached tokens instead")
     ap.add_argument("--paged", type=int, default=0, metavar="P",
@@ -419,6 +428,9 @@ def main():
         return
 
     cfg = args.config
+    if not 0 <= args.anchor_layer < max(1, args.layers):
+        print("bench.py --anchor-layer A: 0 <= A < --layers", file=sys.stderr)
+        sys.exit(2)
     if args.graph and (cfg == 5 or args.calls or args.layers > 1 or args.dense):
         print("bench.py --graph: configs 1-4, one-call steps, one layer", file=sys.stderr)
         sys.exit(2)

@@ -103,3 +103,9 @@ def test_held_back_cases_are_refused():
     assert r.returncode == 2 and "held back" in r.stderr
     r = _run("--config", "5", "--queries", "2")
     assert r.returncode == 2
+
+
+def test_anchor_layer_must_precede_the_last_layer():
+    for args in (("--layers", "4", "--anchor-layer", "4"), ("--anchor-layer", "-1")):
+        r = _run("--config", "2", *args)
+        assert r.returncode == 2 and "--anchor-layer" in r.stderr
