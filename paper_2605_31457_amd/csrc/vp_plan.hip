@@ -21,6 +21,13 @@ int rows_per_seq(const vp_shape& s) { return queries(s) * rows_per_query(s); }
 #ifndef VP_TARGET_PARTS
 #define VP_TARGET_PARTS 2048
 #endif
+// The visual and text passes in two launches (large caches) take three
+// quarters of that: 6 parts per KV head at the 64 x 32k batch, where 4, 5, 6,
+// 7 and 8 parts measured 660, 631, 613.6, 618.5 and 616.5 us per step (the
+// visual pass 265 / 238 / 222 / 226 / 225 us; the text pass within 1 us but at 4).
+#ifndef VP_TWO_LAUNCH_PARTS
+#define VP_TWO_LAUNCH_PARTS 1536
+#endif
 #ifndef VP_MIN_TILES
 #define VP_MIN_TILES 2  // 32-row tiles per context-pass part, at least
 #endif
@@ -63,7 +70,7 @@ Plan make_plan(const vp_shape& s) {
   const int64_t pairs = static_cast<int64_t>(s.batch) * s.n_kv_heads;
   const int64_t tiles = (s.max_seq_len + 31) / 32;
   // the one-launch context pass runs a visual and a text work-group per part
-  const int64_t target = use_dual(&s) ? VP_TARGET_PARTS / VP_DUAL_PART_DIV : VP_TARGET_PARTS;
+  const int64_t target = use_dual(&s) ? VP_TARGET_PARTS / VP_DUAL_PART_DIV : VP_TWO_LAUNCH_PARTS;
   int64_t parts = (target + pairs - 1) / pairs;
   if (parts > (tiles + VP_MIN_TILES - 1) / VP_MIN_TILES) parts = (tiles + VP_MIN_TILES - 1) / VP_MIN_TILES;
   if (parts < 1) parts = 1;
