@@ -101,8 +101,12 @@ def test_more_than_one_gpu_is_refused():
 def test_held_back_cases_are_refused():
     r = _run("--config", "4", "--paged", "32")
     assert r.returncode == 2 and "held back" in r.stderr
+    r = _run("--config", "4", "--paged", "32", "--batch", "32")
+    assert r.returncode == 2 and "held back" in r.stderr
     r = _run("--config", "5", "--queries", "2")
     assert r.returncode == 2
+    r = _run("--config", "2", "--batch", "4")
+    assert r.returncode == 2 and "--batch" in r.stderr
 
 
 def test_anchor_layer_must_precede_the_last_layer():
