@@ -14,10 +14,10 @@ int queries(const vp_shape& s) { return s.n_queries > 1 ? s.n_queries : 1; }
 int rows_per_query(const vp_shape& s) { return s.scope == VP_SCOPE_KV_GROUP ? s.n_kv_heads : 1; }
 int rows_per_seq(const vp_shape& s) { return queries(s) * rows_per_query(s); }
 
-// Context-pass work-groups per launch: 2048 is one resident round of the text
-// pass (8 work-groups per CU x 256 CUs), so no work-group waits for a second
-// round; measured best against 1024, 4096 and 8192 on every configuration
-// (the 64 x 32k batch: 689 -> 665 us per step).
+// Context-pass work-groups of the one launch of both passes: 2048 (1024 parts
+// per role) is one resident round (8 work-groups per CU x 256 CUs), so no
+// work-group waits for a second round; measured best against 768 to 1280
+// parts per role at the ragged 16-sequence batch and the 72B-class loop.
 #ifndef VP_TARGET_PARTS
 #define VP_TARGET_PARTS 2048
 #endif
