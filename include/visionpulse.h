@@ -314,7 +314,7 @@ vp_status vp_decode_step(const vp_shape* shape, const vp_layout* layout, const v
  * Errors: as vp_decode_step; VP_ERR_WORKSPACE, before anything is enqueued,
  * when vp_workspace_size(shape) exceeds VP_STATIC_SCRATCH_BYTES (the 16-sequence
  * 12k-token batch of the 7B shape needs about 29 MiB; 64 sequences of 32k
- * tokens need 270 MiB and must use vp_decode_step); VP_ERR_HIP if the scratch
+ * tokens need 268 MiB and must use vp_decode_step); VP_ERR_HIP if the scratch
  * address cannot be obtained.
  */
 #define VP_STATIC_SCRATCH_BYTES (32u << 20)

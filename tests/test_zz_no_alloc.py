@@ -54,7 +54,7 @@ def test_static_scratch_matches_workspace_step():
 
 
 def test_static_scratch_refuses_a_larger_shape():
-    # the 64 x 32k batch needs ~270 MiB of scratch: refused before any launch
+    # the 64 x 32k batch needs ~268 MiB of scratch: refused before any launch
     sh = vp.vp_shape(batch=64, n_q_heads=28, n_kv_heads=4, head_dim=128, dtype=vp.VP_BF16, max_seq_len=32768,
                      max_vis=16384, max_segs=4, k_cap=819, block_size=0, scope=0, n_queries=1,
                      kv_stride_b=4 * 32768 * 128, kv_stride_h=32768 * 128, kv_stride_s=128)
