@@ -392,8 +392,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calls", action="store_true", help="time the four separate calls instead of vp_decode_step")
     ap.add_argument("--layers", type=int, default=1,
-                    help="time a per-token step over this many layers: the anchor layer's decode step, then "
-                         "every other layer's attention over the anchor's kept set on its own KV cache")
+                    help="time a per-token step over this many layers, each on its own KV cache: the layers "
+                         "before the anchor (--anchor-layer) attend densely, the anchor runs the decode step, the "
+                         "later layers attend over the anchor's kept set")
     ap.add_argument("--batch", type=int, default=None, metavar="B",
                     help="configs 3 and 4: B sequences of the configuration's per-sequence shape")
     ap.add_argument("--anchor-layer", type=int, default=0, metavar="A",
