@@ -24,7 +24,8 @@ int rows_per_seq(const vp_shape& s) { return queries(s) * rows_per_query(s); }
 // The visual and text passes in two launches (large caches) take three
 // quarters of that: 6 parts per KV head at the 64 x 32k batch, where 4, 5, 6,
 // 7 and 8 parts measured 660, 631, 613.6, 618.5 and 616.5 us per step (the
-// visual pass 265 / 238 / 222 / 226 / 225 us; the text pass within 1 us but at 4).
+// visual pass 265 / 238 / 222 / 226 / 225 us; the text pass 328.5 us at 4 parts
+// and within 1 us of 325 us at 5 to 8).
 #ifndef VP_TWO_LAUNCH_PARTS
 #define VP_TWO_LAUNCH_PARTS 1536
 #endif
